@@ -1,0 +1,480 @@
+"""Plain CPU oracle for attention-based LSTM encoder-decoder beam-search translation.
+
+TEST INFRASTRUCTURE ONLY. Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import or run this module. The product
+path (the HIP library and its Python binding) never calls it and shares no code
+with it; the two meet only in the seeded inputs of the ``workloads`` package.
+
+Everything is float64 NumPy, written for a reader holding the OpenNMT paper
+(Klein et al., arXiv 1805.11462). The paper names the pieces but prints no
+equations, so the standard published forms of the cited works are written out
+here; every place where the paper is silent carries its reading (R1..R16, the
+same numbering as the design notes).
+
+What the paper fixes, and where:
+
+* Section 2 (Background): the conditional language model
+  ``p(w_1:T | x) = prod_t p(w_t | w_1:t-1, x)``; a source encoder RNN maps word
+  vectors to hidden vectors h_1..h_S; a target decoder RNN combines its hidden
+  state with the source vectors through an attention pooling layer; a softmax
+  layer gives the next-word distribution.
+* Section 2, items (a)-(d): gated cell (LSTM), stacked layers, input feeding
+  (previous attention vector fed back with the predicted word), beam search.
+* Figure 1(a) caption: the encoder's final step initialises the target RNN;
+  attention is combined with the current hidden state to make the prediction,
+  which is fed back.
+* Section 4.2 ("Extensible Data, Models, and Search"): attention types
+  general / dot / concat; beam search with length normalisation.
+* Tables 3 and 4 captions: bidirectional RNN encoders.
+
+Readings where the paper is silent (R-numbers):
+
+R1  LSTM: forget-gate LSTM without peepholes, one bias per gate, gate order
+    (i, f, g, o), sigma(x) = 1 / (1 + exp(-x)).
+R2  Encoder initial state is zero.
+R3  No BOS/EOS is added to the source.
+R4  Padding is packed: pad positions never update the state; memory rows at
+    pads are 0; attention weight at pads is exactly 0.
+R5  Bidirectional final state handed to the decoder, per layer:
+    [forward state after the last real token ; backward state after token 0].
+R6  "general" score e_s = q^T W_a m_s with no bias; attentional vector
+    tanh(W_c [ctx ; q]) with no bias.
+R7  Input feed starts at 0; decoder layer-1 input is [embedding ; feed].
+R8  Generator has a bias; no token is masked.
+R9  Beam: scores s_0 = 0, s_1.. = -inf; candidates cand = s_k + logp_k(w) in
+    fp64; top-K finite candidates, ties to the smaller flat index k*V + w; a
+    chosen EOS (or any choice at t = T_max) enters the finished pool; the rest
+    fill live slots in rank order; stop when t = T_max, or no live slot, or the
+    pool's best normalised score >= best live score / lp(T_max).
+R10 GNMT length penalty lp(n) = ((5 + n) / 6) ** alpha, applied to finished
+    hypotheses only; n counts EOS.
+R11 max_len = most generated tokens, EOS included.
+R12 bf16 workloads: the oracle runs in fp64 on the bf16-rounded weights.
+R15 Throughput counts target tokens of the 1-best, EOS included.
+R16 Near-ties: any choice within the tolerance is a correct result.
+
+Pins (tests that tie this file to the mathematics rather than to itself) live
+in ``tests/test_oracle_*.py``. The whole pipeline against the paper's printed
+results is parity unpinned: the paper prints only BLEU and speed on data and
+trained weights that are not available.
+"""
+
+from dataclasses import dataclass, field
+import numpy as np
+
+from workloads.configs import PAD_ID, BOS_ID, EOS_ID
+
+F64 = np.float64
+
+
+# --------------------------------------------------------------------------
+# Model container
+# --------------------------------------------------------------------------
+
+@dataclass
+class Model:
+    """fp64 copy of the weights plus the shape fields the oracle needs."""
+    enc_layers: int
+    dec_layers: int
+    bidirectional: bool
+    emb: int
+    hidden: int
+    src_vocab: int
+    tgt_vocab: int
+    w: dict = field(repr=False)
+
+    @property
+    def enc_hidden(self):
+        return self.hidden // 2 if self.bidirectional else self.hidden
+
+
+def model_from(workload, weights) -> Model:
+    return Model(workload.enc_layers, workload.dec_layers, workload.bidirectional,
+                 workload.emb, workload.hidden, workload.src_vocab, workload.tgt_vocab,
+                 {k: np.asarray(v, dtype=F64) for k, v in weights.items()})
+
+
+# --------------------------------------------------------------------------
+# Cell (Section 2 item (a); R1)
+# --------------------------------------------------------------------------
+
+def sigmoid(x):
+    with np.errstate(over="ignore"):
+        return 1.0 / (1.0 + np.exp(-x))
+
+
+def lstm_cell(W, b, x, h, c):
+    """One LSTM step on rows of x, h, c.
+
+    z = W[:, :in] x + W[:, in:] h + b ; (z_i, z_f, z_g, z_o) blocks of z;
+    c' = sigma(z_f) * c + sigma(z_i) * tanh(z_g) ; h' = sigma(z_o) * tanh(c').
+    """
+    n_in = x.shape[-1]
+    Hl = h.shape[-1]
+    z = x @ W[:, :n_in].T + h @ W[:, n_in:].T + b
+    i = sigmoid(z[..., 0 * Hl:1 * Hl])
+    f = sigmoid(z[..., 1 * Hl:2 * Hl])
+    g = np.tanh(z[..., 2 * Hl:3 * Hl])
+    o = sigmoid(z[..., 3 * Hl:4 * Hl])
+    c_new = f * c + i * g
+    h_new = o * np.tanh(c_new)
+    return h_new, c_new
+
+
+# --------------------------------------------------------------------------
+# Encoder (Section 2; Figure 1(a); stacked layers item (b); bi-RNN Tables 3-4)
+# --------------------------------------------------------------------------
+
+@dataclass
+class Encoded:
+    memory: np.ndarray      # [B, S, Hm], zero at pads (R4)
+    mask: np.ndarray        # [B, S] bool, True on real positions
+    final_h: list           # per layer [B, H] (R5 for bi)
+    final_c: list
+
+
+def run_direction(W, b, x, real, reverse):
+    """One LSTM direction over [B, S, in] with packed padding (R2, R4)."""
+    B, S, _ = x.shape
+    Hl = W.shape[0] // 4
+    h = np.zeros((B, Hl), F64)
+    c = np.zeros((B, Hl), F64)
+    out = np.zeros((B, S, Hl), F64)
+    steps = range(S - 1, -1, -1) if reverse else range(S)
+    for s in steps:
+        h_new, c_new = lstm_cell(W, b, x[:, s], h, c)
+        act = real[:, s][:, None]
+        h = np.where(act, h_new, h)
+        c = np.where(act, c_new, c)
+        out[:, s] = np.where(act, h_new, 0.0)
+    return out, h, c
+
+
+def encode(m: Model, src, lens) -> Encoded:
+    src = np.asarray(src)
+    lens = np.asarray(lens)
+    B, S = src.shape
+    real = np.arange(S)[None, :] < lens[:, None]
+    x = m.w["E_src"][src]                                   # word vectors (R3: no BOS/EOS)
+    final_h, final_c = [], []
+    for l in range(m.enc_layers):
+        outs, hs, cs = [], [], []
+        for d in (("fwd", "bwd") if m.bidirectional else ("fwd",)):
+            o, h, c = run_direction(m.w[f"enc{l}_{d}_W"], m.w[f"enc{l}_{d}_b"], x, real,
+                                    reverse=(d == "bwd"))
+            outs.append(o)
+            hs.append(h)
+            cs.append(c)
+        x = np.concatenate(outs, axis=-1)
+        final_h.append(np.concatenate(hs, axis=-1))
+        final_c.append(np.concatenate(cs, axis=-1))
+    return Encoded(x, real, final_h, final_c)
+
+
+# --------------------------------------------------------------------------
+# Decoder step (Section 2; items (b), (c); Figure 1(a); Section 4.2 attention)
+# --------------------------------------------------------------------------
+
+@dataclass
+class State:
+    h: list      # per layer [N, H]
+    c: list      # per layer [N, H]
+    feed: np.ndarray   # [N, H], the previous attentional vector (R7)
+
+    def take(self, rows):
+        rows = np.asarray(rows)
+        return State([a[rows] for a in self.h], [a[rows] for a in self.c], self.feed[rows])
+
+
+def init_state(m: Model, enc: Encoded, K: int) -> State:
+    """Decoder state from the encoder's final step (Figure 1(a)), copied to K beam rows."""
+    rep = lambda a: np.repeat(a, K, axis=0)
+    N = enc.memory.shape[0] * K
+    return State([rep(h) for h in enc.final_h], [rep(c) for c in enc.final_c],
+                 np.zeros((N, m.hidden), F64))
+
+
+def attention(m: Model, q, memory, mask):
+    """Global "general" attention for rows q [N, H] over their sentences' memory.
+
+    memory [N, S, Hm] and mask [N, S] are already per row. Returns (a [N, S],
+    ctx [N, Hm], h_tilde [N, H]). R4, R6.
+    """
+    Wm = memory @ m.w["W_a"].T                               # W_a m_s, [N, S, H]
+    e = np.einsum("nh,nsh->ns", q, Wm)
+    e = np.where(mask, e, -np.inf)
+    e_max = e.max(axis=1, keepdims=True)
+    p = np.exp(e - e_max)                                    # exactly 0 on pads
+    a = p / p.sum(axis=1, keepdims=True)
+    ctx = np.einsum("ns,nsh->nh", a, memory)
+    h_tilde = np.tanh(np.concatenate([ctx, q], axis=-1) @ m.w["W_c"].T)
+    return a, ctx, h_tilde
+
+
+def log_softmax(z):
+    z_max = z.max(axis=-1, keepdims=True)
+    return z - (z_max + np.log(np.exp(z - z_max).sum(axis=-1, keepdims=True)))
+
+
+def generator(m: Model, h_tilde):
+    """Next-word log-distribution over the whole target vocabulary (Section 2; R8)."""
+    return log_softmax(h_tilde @ m.w["W_s"].T + m.w["b_s"])
+
+
+def decode_step(m: Model, enc: Encoded, st: State, prev_tok, row_sentence):
+    """p(w_t | w_<t, x) for every row: returns (new state, logp [N, V], attention [N, S])."""
+    x = np.concatenate([m.w["E_tgt"][np.asarray(prev_tok)], st.feed], axis=-1)
+    hs, cs = [], []
+    for l in range(m.dec_layers):
+        h, c = lstm_cell(m.w[f"dec{l}_W"], m.w[f"dec{l}_b"], x, st.h[l], st.c[l])
+        hs.append(h)
+        cs.append(c)
+        x = h
+    rows = np.asarray(row_sentence)
+    a, _, h_tilde = attention(m, x, enc.memory[rows], enc.mask[rows])
+    return State(hs, cs, h_tilde), generator(m, h_tilde), a
+
+
+# --------------------------------------------------------------------------
+# Search (Section 2 item (d); Section 4.2 length normalisation; R9-R11)
+# --------------------------------------------------------------------------
+
+def length_penalty(n, alpha):
+    """GNMT length penalty ((5 + n) / 6) ** alpha (R10)."""
+    return ((5.0 + n) / 6.0) ** alpha
+
+
+@dataclass
+class Hyp:
+    tokens: list
+    logps: list
+
+
+@dataclass
+class Result:
+    tokens: list            # 1-best tokens per sentence (BOS excluded, EOS included if chosen)
+    raw: np.ndarray         # [B] summed log-prob
+    norm: np.ndarray        # [B] raw / lp(len)
+    logps: list             # per-token log-probs of the 1-best
+    steps: np.ndarray       # [B] step after which the sentence was done
+    trace: dict = None      # per step: chosen (slot, token, cand) by rank
+
+
+def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, record=False):
+    """Beam search for every sentence, one set of K slots per sentence.
+
+    Sentences are independent; the decoder runs all B*K rows at once only to
+    share the matrix products.
+    """
+    src = np.asarray(src)
+    B = src.shape[0]
+    V = m.tgt_vocab
+    enc = encode(m, src, lens)
+    st = init_state(m, enc, K)
+    row_sentence = np.repeat(np.arange(B), K)
+    scores = np.full((B, K), -np.inf)
+    scores[:, 0] = 0.0
+    hyps = [[Hyp([], []) for _ in range(K)] for _ in range(B)]
+    tok = np.full(B * K, BOS_ID, np.int64)
+    done = np.zeros(B, bool)
+    steps = np.zeros(B, np.int64)
+    best = [None] * B              # (norm, raw, Hyp)
+    trace = {"slot": [], "tok": [], "cand": []} if record else None
+    lp_max = length_penalty(max_len, alpha)
+    for t in range(1, max_len + 1):
+        st_new, logp, _ = decode_step(m, enc, st, tok, row_sentence)
+        parent = np.arange(B * K)
+        new_tok = np.full(B * K, PAD_ID, np.int64)
+        if record:
+            t_slot = np.full((B, K), -1, np.int64)
+            t_tok = np.full((B, K), -1, np.int64)
+            t_cand = np.full((B, K), -np.inf)
+        for b in range(B):
+            if done[b]:
+                continue
+            rows = slice(b * K, (b + 1) * K)
+            cand = scores[b][:, None] + logp[rows]              # [K, V]; dead slots stay -inf
+            flat = cand.ravel()
+            order = np.argsort(-flat, kind="stable")            # ties: smaller flat index first
+            chosen = [i for i in order[:K] if np.isfinite(flat[i])]
+            new_scores = np.full(K, -np.inf)
+            new_hyps = [Hyp([], []) for _ in range(K)]
+            j = 0
+            for rank, i in enumerate(chosen):
+                k, w = divmod(int(i), V)
+                hyp = Hyp(hyps[b][k].tokens + [w], hyps[b][k].logps + [logp[b * K + k, w]])
+                if record:
+                    t_slot[b, rank], t_tok[b, rank], t_cand[b, rank] = k, w, flat[i]
+                if w == EOS_ID or t == max_len:
+                    norm = flat[i] / length_penalty(t, alpha)
+                    if best[b] is None or norm > best[b][0]:
+                        best[b] = (norm, flat[i], hyp)
+                else:
+                    new_hyps[j] = hyp
+                    new_scores[j] = flat[i]
+                    parent[b * K + j] = b * K + k
+                    new_tok[b * K + j] = w
+                    j += 1
+            scores[b] = new_scores
+            hyps[b] = new_hyps
+            live = new_scores[np.isfinite(new_scores)]
+            if (t == max_len or live.size == 0
+                    or (stop_rule and best[b] is not None and best[b][0] >= live.max() / lp_max)):
+                done[b] = True
+                steps[b] = t
+        if record:
+            trace["slot"].append(t_slot)
+            trace["tok"].append(t_tok)
+            trace["cand"].append(t_cand)
+        st = st_new.take(parent)
+        tok = new_tok
+        if done.all():
+            break
+    return Result([bst[2].tokens for bst in best],
+                  np.array([bst[1] for bst in best]), np.array([bst[0] for bst in best]),
+                  [bst[2].logps for bst in best], steps, trace)
+
+
+def greedy(m: Model, src, lens, max_len):
+    """Argmax decoding (smallest id on ties), stopping at EOS or max_len. Separate code from beam_search."""
+    src = np.asarray(src)
+    B = src.shape[0]
+    enc = encode(m, src, lens)
+    st = init_state(m, enc, 1)
+    tok = np.full(B, BOS_ID, np.int64)
+    out = [[] for _ in range(B)]
+    lps = [[] for _ in range(B)]
+    finished = np.zeros(B, bool)
+    for _ in range(max_len):
+        st, logp, _ = decode_step(m, enc, st, tok, np.arange(B))
+        tok = logp.argmax(axis=1)
+        for b in range(B):
+            if not finished[b]:
+                out[b].append(int(tok[b]))
+                lps[b].append(logp[b, tok[b]])
+                finished[b] = tok[b] == EOS_ID
+        if finished.all():
+            break
+    return out, np.array([sum(x) for x in lps])
+
+
+def score_forced(m: Model, src_row, n_src, target):
+    """Teacher-forced per-token log-probs of ``target`` for one sentence, from scratch."""
+    src_row = np.asarray(src_row)[None, :]
+    enc = encode(m, src_row, np.array([n_src]))
+    st = init_state(m, enc, 1)
+    prev = BOS_ID
+    out = []
+    for w in target:
+        st, logp, _ = decode_step(m, enc, st, np.array([prev]), np.array([0]))
+        out.append(logp[0, w])
+        prev = w
+    return np.array(out)
+
+
+def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0):
+    """Best normalised score over every output sequence (exhaustive; tiny vocabularies only).
+
+    Sequences: those whose first EOS ends them at length n <= max_len, plus
+    every EOS-free sequence of length max_len. Returns (tokens, raw, norm).
+    """
+    V = m.tgt_vocab
+    best = None
+    stack = [[]]
+    while stack:
+        prefix = stack.pop()
+        for w in range(V):
+            seq = prefix + [w]
+            if w == EOS_ID or len(seq) == max_len:
+                raw = score_forced(m, src_row, n_src, seq).sum()
+                norm = raw / length_penalty(len(seq), alpha)
+                if best is None or norm > best[2]:
+                    best = (seq, raw, norm)
+            else:
+                stack.append(seq)
+    return best
+
+
+# --------------------------------------------------------------------------
+# Replay of a recorded search (parity protocol for near-ties, R16)
+# --------------------------------------------------------------------------
+
+def replay_verify(m: Model, src, lens, K, max_len, alpha, trace, tau, sentences=None):
+    """Check another implementation's beam decisions step by step.
+
+    ``trace`` holds, per step t (list index t-1), arrays [B, K] by rank:
+    ``slot`` (parent slot, -1 = nothing chosen), ``tok`` and ``cand`` (that
+    implementation's fp64 score). The oracle follows the recorded decisions
+    (teacher forcing its own fp64 decoder through them) and checks that
+      * every chosen candidate's log-prob agrees with the oracle's within tau;
+      * the chosen set is a valid top-K under the oracle's log-probs added to
+        the recorded scores (chosen >= K-th - tau, rejected <= K-th + tau);
+      * every recorded score stays within t * tau of the oracle's running sum.
+    Returns a list of violation strings (empty = pass).
+    """
+    src = np.asarray(src)
+    B = src.shape[0]
+    V = m.tgt_vocab
+    if sentences is None:
+        sentences = range(B)
+    bad = []
+    for b in sentences:
+        enc = encode(m, src[b:b + 1], np.asarray(lens)[b:b + 1])
+        st = init_state(m, enc, K)
+        s_rec = np.full(K, -np.inf)       # recorded scores of live slots
+        s_orc = np.full(K, -np.inf)       # oracle running sums along the same hypotheses
+        s_rec[0] = s_orc[0] = 0.0
+        tok = np.full(K, BOS_ID, np.int64)
+        for t in range(1, len(trace["slot"]) + 1):
+            slot = np.asarray(trace["slot"][t - 1][b])
+            if (slot < 0).all():
+                break
+            wtok = np.asarray(trace["tok"][t - 1][b])
+            cand_rec = np.asarray(trace["cand"][t - 1][b])
+            st_new, logp, _ = decode_step(m, enc, st, tok, np.zeros(K, np.int64))
+            oc = s_rec[:, None] + logp                       # oracle log-probs on recorded scores
+            flat = np.sort(oc.ravel())[::-1]
+            n_fin = int(np.isfinite(flat).sum())
+            kk = min(K, n_fin)
+            theta = flat[kk - 1]
+            chosen = set()
+            parent = np.zeros(K, np.int64)
+            new_tok = np.full(K, PAD_ID, np.int64)
+            ns_rec = np.full(K, -np.inf)
+            ns_orc = np.full(K, -np.inf)
+            j = 0
+            for r in range(K):
+                k = int(slot[r])
+                if k < 0:
+                    continue
+                w = int(wtok[r])
+                chosen.add(k * V + w)
+                if not np.isfinite(s_rec[k]):
+                    bad.append(f"b{b} t{t} r{r}: chose dead slot {k}")
+                    continue
+                lp_rec = cand_rec[r] - s_rec[k]
+                if abs(lp_rec - logp[k, w]) > tau:
+                    bad.append(f"b{b} t{t} r{r}: logp {lp_rec:.6g} vs oracle {logp[k, w]:.6g}")
+                if oc[k, w] < theta - tau:
+                    bad.append(f"b{b} t{t} r{r}: chosen {oc[k, w]:.8g} below K-th {theta:.8g} - tau")
+                run = s_orc[k] + logp[k, w]
+                if abs(cand_rec[r] - run) > t * tau:
+                    bad.append(f"b{b} t{t} r{r}: score drift {cand_rec[r] - run:.3g}")
+                if not (w == EOS_ID or t == max_len):
+                    parent[j] = k
+                    new_tok[j] = w
+                    ns_rec[j] = cand_rec[r]
+                    ns_orc[j] = run
+                    j += 1
+            if len(chosen) != kk:
+                bad.append(f"b{b} t{t}: {len(chosen)} chosen, expected {kk}")
+            # rejected candidates must not beat the K-th by more than tau
+            masked = oc.copy().ravel()
+            if chosen:
+                masked[np.fromiter(chosen, np.int64)] = -np.inf
+            if masked.max() > theta + tau:
+                bad.append(f"b{b} t{t}: rejected {masked.max():.8g} above K-th {theta:.8g} + tau")
+            st = st_new.take(parent)
+            tok = new_tok
+            s_rec, s_orc = ns_rec, ns_orc
+    return bad

@@ -1,0 +1,174 @@
+/*
+ * onmt.h — C interface of libonmt, batched beam-search translation with an attention-based LSTM
+ * encoder-decoder on one AMD Instinct MI355X (gfx950).
+ *
+ * The model is the one the OpenNMT paper (Klein et al., arXiv 1805.11462) describes in Section 2
+ * ("Background") and Figure 1(a): a conditional language model p(w_1:T | x) = prod_t p(w_t | w_<t, x)
+ * computed by a stacked (optionally bidirectional, Tables 3-4) LSTM encoder, an input-feeding LSTM
+ * decoder (Section 2 item (c)) with global "general" attention (Section 4.2), a softmax generator and
+ * beam search with length normalisation (Section 2 item (d); Section 4.2). The paper's deployment
+ * section (Section 4.1, "C/Mobile/GPU Translation") describes a batched GPU translator and a C
+ * implementation; this library is that translator behind a C ABI.
+ *
+ * Where the paper is silent the library follows these readings: forget-gate LSTM without peepholes,
+ * one bias per gate, gate order (i, f, g, o); zero initial encoder state; no source BOS/EOS; packed
+ * padding (pads never update state, memory is 0 and attention weight exactly 0 at pads);
+ * bidirectional final state [forward after last token ; backward after token 0]; score
+ * q^T W_a m_s without bias; attentional vector tanh(W_c [ctx ; q]) without bias; input feed starts at
+ * 0 and the first decoder layer sees [embedding ; feed]; generator with bias, nothing masked.
+ *
+ * Conventions for every function:
+ *   - Return 0 (ONMT_OK) or a negative error code; never throw or abort. onmt_last_error() gives a
+ *     thread-local message for the last failure.
+ *   - All size and id checks happen before any compute is enqueued. On error no kernel has been
+ *     launched and output buffers are unspecified.
+ *   - The caller owns all device memory: it allocates the buffers whose sizes the *_bytes queries
+ *     return and passes device pointers. The library never allocates device memory.
+ *   - `stream` is a hipStream_t (NULL = default stream). Work is ordered on that stream.
+ *   - Matrices are row-major. Beam rows are numbered r = b * K + k (sentence b, slot k).
+ *   - A model handle is not thread-safe; separate handles are independent.
+ */
+#ifndef ONMT_H
+#define ONMT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  ONMT_OK = 0,
+  ONMT_EINVAL = -1,       /* bad argument: null pointer, out-of-range id/length/size */
+  ONMT_ESIZE = -2,        /* a device buffer is smaller than the matching *_bytes query */
+  ONMT_EDEVICE = -3,      /* a HIP runtime call failed */
+  ONMT_EUNSUPPORTED = -4  /* valid but outside what the kernels support (e.g. beam > 16) */
+};
+
+/* Model shape. enc_layers must equal dec_layers (the decoder starts from the encoder's final states,
+ * Figure 1(a)). When bidirectional, each encoder direction has hidden/2 units and their outputs are
+ * concatenated, so the memory width is `hidden` either way. emb and hidden (and hidden/2 when
+ * bidirectional) must be multiples of 4; with wdtype = 1 emb must be a multiple of 8. */
+typedef struct {
+  int enc_layers, dec_layers, bidirectional;
+  int emb, hidden;
+  int src_vocab, tgt_vocab;
+  int wdtype;                      /* 0 = fp32 weights and products; 1 = bf16 weights and MFMA operands,
+                                      fp32 accumulation, cell state and softmax */
+  int pad_id, unk_id, bos_id, eos_id;
+} onmt_config;
+
+/* Beam search settings (Section 2 item (d); Section 4.2 length normalisation, GNMT form
+ * lp(n) = ((5 + n) / 6)^alpha). max_len counts generated tokens including EOS. The host reads an
+ * "all sentences finished" counter every check_every steps (<= 0: every step when
+ * max_len <= 32, else every 8). */
+typedef struct {
+  int beam;
+  int max_len;
+  double alpha;
+  int check_every;
+} onmt_search_params;
+
+/* Optional per-step record of the search, device pointers, each [max_len, B, beam] by rank:
+ * slot = parent slot of the chosen candidate (-1 = none), tok = chosen token, cand = its fp64
+ * score (parent score + log-prob). steps[B] = step after which the sentence finished. */
+typedef struct {
+  int32_t* slot;
+  int32_t* tok;
+  double* cand;
+  int32_t* steps;
+} onmt_trace;
+
+typedef struct onmt_model onmt_model;
+
+const char* onmt_last_error(void);
+
+/* Number of host weight arrays onmt_model_create expects, and the element count of array i, in this
+ * order: E_src [src_vocab, emb]; for each encoder layer l and direction (forward, then backward when
+ * bidirectional): W [4*Hd, in + Hd] (gate row blocks i, f, g, o; columns [input | recurrent]) and
+ * b [4*Hd], with Hd = hidden (/2 if bidirectional) and in = emb for l = 0, hidden above; E_tgt
+ * [tgt_vocab, emb]; for each decoder layer l: W [4*hidden, in + hidden] with in = emb + hidden for
+ * l = 0 (columns [embedding | input feed | recurrent]) and hidden above, b [4*hidden];
+ * W_a [hidden, hidden]; W_c [hidden, 2*hidden] (columns [context | decoder state]);
+ * W_s [tgt_vocab, hidden]; b_s [tgt_vocab]. Returns < 0 for an invalid config. */
+int onmt_num_weights(const onmt_config* cfg);
+int64_t onmt_weight_numel(const onmt_config* cfg, int i);
+
+/* Device bytes for the packed weights of `cfg` (0 for an invalid config). */
+size_t onmt_model_bytes(const onmt_config* cfg);
+
+/* Validate cfg, copy and pack the host fp32 weights (order above; the host arrays may be freed when the
+ * call returns) into dev_buf, which must hold onmt_model_bytes(cfg) bytes, 256-byte aligned, and stay
+ * allocated while the model lives. With wdtype = 1 weights are rounded to bf16 (nearest, ties to even).
+ * Synchronizes `stream`. On success *out receives a handle that owns host metadata only. */
+int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, int n_weights, void* dev_buf,
+                      size_t dev_bytes, void* stream, onmt_model** out);
+int onmt_model_destroy(onmt_model* model);
+
+/* ---- Encoder (Section 2: encoder RNN over word vectors; Figure 1(a)) -------------------------------
+ * src [B, S_max] int32 token ids (device), len [B] int32 true lengths (device), 1 <= len[b] <= S_max,
+ * ids in [0, src_vocab). Positions >= len[b] are ignored. Writes the memory bank, the attention keys
+ * W_a m_s and the final states into enc_ws (>= onmt_encode_ws_bytes(model, B, S_max)), which the
+ * decoder calls then read. Copies src and len to the host to validate them (one stream sync), then
+ * enqueues the encoder asynchronously. */
+size_t onmt_encode_ws_bytes(const onmt_model* model, int B, int S_max);
+int onmt_encode(onmt_model* model, const int32_t* src, const int32_t* len, int B, int S_max, void* enc_ws,
+                size_t enc_ws_bytes, void* stream);
+
+/* ---- Decoder step: one evaluation of p(w_t | w_<t, x) for N = B*K rows (Section 2; Figure 1(a)) ----
+ * A decoder state buffer holds, fp32: h [dec_layers, N, hidden], c [dec_layers, N, hidden],
+ * feed [N, hidden] (the previous attentional vector), in that order, onmt_state_bytes(model, N) bytes.
+ *
+ * onmt_decode_init writes into state_out the decoder's initial state: every layer's (h, c) from the
+ * encoder's final step of sentence b = r / K, and feed = 0.
+ *
+ * onmt_decode_step reads row parent[r] of state_in (parent NULL = row r) and prev_tok[r] (ids in
+ * [0, tgt_vocab); parent in [0, N)), runs the decoder layers, attention over sentence r / K's memory,
+ * the attentional vector and the generator, and writes row r of state_out (state_in != state_out).
+ *   mode 0 (full):  logp [N, tgt_vocab] = log-softmax of the logits; ids unused (may be NULL).
+ *   mode 1 (top-K): logp [N, K] and ids [N, K] = the K largest log-probs of each row, larger first,
+ *                   smaller id on ties.
+ *   lse [N] (optional) = logsumexp of each row's logits. attn [N, S_max] (optional) = attention weights,
+ *   exactly 0 at pads.
+ * step_ws holds onmt_step_ws_bytes(model, B, S_max, K) bytes of scratch. prev_tok and parent are copied
+ * to the host for validation (one stream sync); the compute is then enqueued asynchronously. */
+size_t onmt_state_bytes(const onmt_model* model, int N);
+size_t onmt_step_ws_bytes(const onmt_model* model, int B, int S_max, int K);
+int onmt_decode_init(onmt_model* model, const void* enc_ws, int B, int S_max, int K, void* state_out,
+                     void* stream);
+int onmt_decode_step(onmt_model* model, const void* enc_ws, int B, int S_max, int K, const void* state_in,
+                     void* state_out, const int32_t* prev_tok, const int32_t* parent, int mode, float* logp,
+                     int32_t* ids, float* lse, float* attn, void* step_ws, size_t step_ws_bytes, void* stream);
+
+/* ---- Beam search (Section 2 item (d); Section 4.2; Section 4.1 batched GPU translator) --------------
+ * Translates B sentences with beam width K = params->beam (1 <= K <= 16, K <= tgt_vocab). Per sentence:
+ * slot scores start [0, -inf, ...] with input BOS; each step scores cand = s_k + logp_k(w) in fp64 and
+ * keeps the K best (larger first, smaller k*V + w on ties); a chosen EOS, or any choice at step
+ * max_len, enters the finished pool with norm = cand / lp(t); the others become the next live slots in
+ * rank order. A sentence stops at max_len, when no live slot remains, or when the pool's best norm is
+ * >= best live score / lp(max_len) (no descendant can beat it). The result is the pool entry with the
+ * largest norm (earlier step, then better rank, on ties).
+ * Outputs (device pointers): out_tok [B, max_len] (BOS excluded, EOS included if chosen, pad_id after
+ * the end), out_len [B], out_raw [B] (sum of log-probs), out_norm [B], out_tok_logp [B, max_len]
+ * (optional; 0 after the end), trace (optional). ws holds onmt_search_ws_bytes(...) bytes. src/len as
+ * in onmt_encode. Returns when the outputs are written (the stream is synchronized). */
+size_t onmt_search_ws_bytes(const onmt_model* model, int B, int S_max, const onmt_search_params* params);
+int onmt_beam_search(onmt_model* model, const int32_t* src, const int32_t* len, int B, int S_max,
+                     const onmt_search_params* params, void* ws, size_t ws_bytes, int32_t* out_tok,
+                     int32_t* out_len, double* out_raw, double* out_norm, float* out_tok_logp,
+                     const onmt_trace* trace, void* stream);
+
+/* ---- Kernel timing -----------------------------------------------------------------------------------
+ * When enabled, onmt_beam_search records HIP events around every launch of the decoder's generator
+ * kernel (the vocabulary projection with its fused log-softmax/top-K epilogue) on `stream`, and
+ * onmt_profile_read returns how many launches were timed and their summed duration in milliseconds since
+ * the last reset. Timing adds two event records per step. */
+int onmt_profile_enable(onmt_model* model, int on);
+int onmt_profile_read(onmt_model* model, int* n_launches, double* total_ms, int reset);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ONMT_H */

@@ -1,0 +1,126 @@
+// Host-visible launch interface of the libonmt kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace onmt {
+
+// One K-segment of a GEMM's A operand: A[r, off + k] = base[map(r) * ld + k] for k < width,
+// 0 for width <= k < kpad. map(r) = idx ? idx[r] : r.
+struct Seg {
+  const void* base;
+  const int32_t* idx;
+  int ld;
+  int width;
+  int kpad;
+  int bf16;
+};
+
+struct AOp {
+  Seg seg[3];
+  int nseg;
+  int M;
+};
+
+// Packed weight matrix [Np, Kp], K contiguous. Np is a multiple of 128, Kp of 8.
+struct BOp {
+  const void* W;
+  int Np;
+  int Kp;
+};
+
+// Plain store epilogue: out[r, n] = act(acc + bias[n]) for n < ncols. act: 0 none, 1 tanh.
+struct StoreParams {
+  const float* bias;
+  float* out;
+  int ldo;
+  int ncols;
+  int act;
+};
+
+// LSTM cell epilogue over gate-blocked columns (groups of 64 = 4 gates x 16 units).
+struct LstmParams {
+  const float* bias;            // packed [Np]
+  const float* gx;              // optional precomputed input projection (packed columns)
+  int ld_gx, gx_col0, gx_S, gx_s;   // gx row for GEMM row b is b * gx_S + gx_s
+  const float* c_in;            // previous cell state rows, through c_idx (nullable = identity)
+  const int32_t* c_idx;
+  int ld_c;
+  const float* h_in;            // previous hidden (identity rows), used when a row is masked
+  int ld_h_in;
+  float* h_out;
+  float* c_out;
+  int ld_out;
+  float* y_out;                 // optional layer output row b * y_S + y_s, column offset y_col0
+  int ld_y, y_S, y_s, y_col0;
+  const int32_t* lens;          // optional: GEMM row b is active iff y_s < lens[b]
+  int H;                        // real units
+};
+
+// Generator epilogue: per (row, column tile) max, sum of exp and top-K; optional raw logits.
+struct GenParams {
+  const float* bias;
+  int V;
+  int K;
+  int ntiles;
+  float* pmax;                  // [M, ntiles]
+  float* psum;                  // [M, ntiles]
+  float* pval;                  // [M, ntiles, K]
+  int32_t* pid;                 // [M, ntiles, K]
+  float* logits;                // optional [M, ld_logits]
+  int ld_logits;
+};
+
+enum GemmShape { kShapeWide = 0, kShapeSplitK = 1, kShapeSplitKThin = 2 };
+
+hipError_t gemm_store(int bf16, int shape, const AOp& a, const BOp& b, const StoreParams& p, hipStream_t st);
+hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const LstmParams& p, hipStream_t st);
+hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st);
+int gen_tile_cols();
+int gemm_tile_cols(int shape);
+
+hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens,
+                     int B, int S_max, int H, int Hm, int K, float* ctx, float* attn, hipStream_t st);
+size_t attention_lds_bytes(int S_max, int H, int K);
+
+hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pval, const int32_t* pid, int M,
+                          int ntiles, int K, float* out_val, int32_t* out_id, float* out_lse, hipStream_t st);
+hipError_t subtract_rows(float* x, int ld, const float* lse, int M, int ncols, hipStream_t st);
+
+struct BeamParams {
+  int B, K, V, T_max, eos, pad;
+  double alpha, lp_tmax;
+  const float* tk_val;
+  const int32_t* tk_id;
+  double* score;
+  int32_t* parent;
+  int32_t* tok;
+  int32_t* bp_slot;
+  int32_t* bp_tok;
+  float* bp_logp;
+  int32_t* done;
+  int32_t* steps;
+  int32_t* done_count;
+  double* best_norm;
+  double* best_raw;
+  int32_t* best_t;
+  int32_t* best_slot;
+  int32_t* best_tok;
+  float* best_logp;
+  int32_t* tr_slot;             // optional trace [T_max, B, K]
+  int32_t* tr_tok;
+  double* tr_cand;
+};
+
+hipError_t beam_init(const BeamParams& p, int bos, hipStream_t st);
+hipError_t beam_step(const BeamParams& p, int t, hipStream_t st);
+hipError_t backtrack(const BeamParams& p, int32_t* out_tok, int32_t* out_len, double* out_raw, double* out_norm,
+                     float* out_tok_logp, hipStream_t st);
+
+hipError_t replicate_rows(const float* src, int ld_src, int rows, int K, float* dst, int ld_dst, int ncols,
+                          hipStream_t st);
+hipError_t fill_f32(float* dst, size_t n, float v, hipStream_t st);
+hipError_t copy_cols(const float* src, int ld_src, float* dst, int ld_dst, int rows, int ncols, hipStream_t st);
+
+}  // namespace onmt

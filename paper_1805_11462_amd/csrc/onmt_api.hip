@@ -1,0 +1,926 @@
+// C ABI of libonmt: validation, weight packing, workspace carving and the encode / decode-step /
+// beam-search orchestration. All arithmetic runs in the kernels of gemm.hip, attention.hip and beam.hip.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/onmt.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace onmt;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                              \
+  do {                                                                                             \
+    hipError_t e_ = (expr);                                                                        \
+    if (e_ != hipSuccess) return fail(ONMT_EDEVICE, "%s: %s", #expr, hipGetErrorString(e_));       \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+inline int ceil_to(int x, int m) { return (x + m - 1) / m * m; }
+
+// Byte-offset allocator over a caller-provided buffer (used for sizing with base == 0, then carving).
+struct Carver {
+  size_t off = 0;
+  char* base = nullptr;
+  template <class T>
+  T* take(size_t count) {
+    off = align_up(off);
+    T* p = base ? (T*)(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+struct Packed {      // packed weight matrix inside the model buffer
+  const void* W = nullptr;
+  int Np = 0, Kp = 0;
+  size_t off = 0;
+};
+
+struct Dims {
+  int L, ndir, Hd, Hm, H, E, Vs, Vt;
+  int Hd_pad, H_pad;   // units padded to multiples of 32 (gate-blocked groups, 128-column tiles)
+  bool bf16;
+  int kq;              // K-padding quantum: 8 elements for bf16 operands, 4 for fp32
+  int esz;             // operand element size
+  int pad(int w) const { return ceil_to(w, kq); }
+};
+
+bool dims_of(const onmt_config* c, Dims* d) {
+  if (!c) return false;
+  d->L = c->enc_layers;
+  d->ndir = c->bidirectional ? 2 : 1;
+  d->H = c->hidden;
+  d->Hd = c->bidirectional ? c->hidden / 2 : c->hidden;
+  d->Hm = d->ndir * d->Hd;
+  d->E = c->emb;
+  d->Vs = c->src_vocab;
+  d->Vt = c->tgt_vocab;
+  d->Hd_pad = ceil_to(d->Hd, 32);
+  d->H_pad = ceil_to(d->H, 32);
+  d->bf16 = c->wdtype == 1;
+  d->kq = d->bf16 ? 8 : 4;
+  d->esz = d->bf16 ? 2 : 4;
+  return true;
+}
+
+int check_config(const onmt_config* c) {
+  if (!c) return fail(ONMT_EINVAL, "config is NULL");
+  if (c->enc_layers < 1 || c->dec_layers < 1) return fail(ONMT_EINVAL, "layers must be >= 1");
+  if (c->enc_layers != c->dec_layers)
+    return fail(ONMT_EINVAL, "enc_layers (%d) must equal dec_layers (%d)", c->enc_layers, c->dec_layers);
+  if (c->bidirectional != 0 && c->bidirectional != 1) return fail(ONMT_EINVAL, "bidirectional must be 0 or 1");
+  if (c->wdtype != 0 && c->wdtype != 1) return fail(ONMT_EINVAL, "wdtype must be 0 (fp32) or 1 (bf16)");
+  if (c->emb < 4 || c->hidden < 4 || c->src_vocab < 1 || c->tgt_vocab < 4)
+    return fail(ONMT_EINVAL, "emb/hidden >= 4, src_vocab >= 1, tgt_vocab >= 4 required");
+  if (c->emb > 8192 || c->hidden > 8192 || c->enc_layers > 64) return fail(ONMT_EUNSUPPORTED, "model too large");
+  const int Hd = c->bidirectional ? c->hidden / 2 : c->hidden;
+  if (c->bidirectional && c->hidden % 2) return fail(ONMT_EINVAL, "bidirectional needs an even hidden size");
+  if (c->emb % 4 || c->hidden % 4 || Hd % 4)
+    return fail(ONMT_EUNSUPPORTED, "emb, hidden and per-direction hidden must be multiples of 4");
+  if (c->wdtype == 1 && c->emb % 8) return fail(ONMT_EUNSUPPORTED, "bf16 models need emb a multiple of 8");
+  const int ids[4] = {c->pad_id, c->unk_id, c->bos_id, c->eos_id};
+  for (int i = 0; i < 4; ++i)
+    if (ids[i] < 0 || ids[i] >= c->tgt_vocab) return fail(ONMT_EINVAL, "special ids must be in [0, tgt_vocab)");
+  return ONMT_OK;
+}
+
+struct WeightSpec {
+  int64_t rows, cols;   // cols = 1 for vectors
+};
+
+std::vector<WeightSpec> weight_specs(const onmt_config* c) {
+  Dims d;
+  dims_of(c, &d);
+  std::vector<WeightSpec> v;
+  v.push_back({d.Vs, d.E});
+  for (int l = 0; l < d.L; ++l) {
+    const int in = l == 0 ? d.E : d.Hm;
+    for (int dir = 0; dir < d.ndir; ++dir) {
+      v.push_back({4LL * d.Hd, in + d.Hd});
+      v.push_back({4LL * d.Hd, 1});
+    }
+  }
+  v.push_back({d.Vt, d.E});
+  for (int l = 0; l < d.L; ++l) {
+    const int in = l == 0 ? d.E + d.H : d.H;
+    v.push_back({4LL * d.H, in + d.H});
+    v.push_back({4LL * d.H, 1});
+  }
+  v.push_back({d.H, d.Hm});
+  v.push_back({d.H, d.Hm + d.H});
+  v.push_back({d.Vt, d.H});
+  v.push_back({d.Vt, 1});
+  return v;
+}
+
+// Row of packed gate-blocked matrices for (gate, unit): groups of 16 units hold 4 gates x 16 rows.
+inline int gate_row(int gate, int unit) { return (unit / kUnitGroup) * 64 + gate * kUnitGroup + unit % kUnitGroup; }
+
+}  // namespace
+
+struct onmt_model {
+  onmt_config cfg;
+  Dims d;
+  char* dev = nullptr;
+  const void* E_src = nullptr;
+  const void* E_tgt = nullptr;
+  std::vector<Packed> enc_x;               // per layer: both directions stacked [ndir * 4 Hd_pad, pad(in)]
+  std::vector<const float*> enc_bias;      // per layer [ndir * 4 Hd_pad]
+  std::vector<Packed> enc_h;               // per layer * ndir: [4 Hd_pad, pad(Hd)]
+  std::vector<Packed> dec_w;               // per layer [4 H_pad, sum of padded segment widths]
+  std::vector<const float*> dec_bias;      // per layer [4 H_pad]
+  Packed W_a, W_c, W_s;
+  const float* b_s = nullptr;
+  // kernel timing
+  bool prof = false;
+  int prof_n = 0;
+  double prof_ms = 0.0;
+  std::vector<hipEvent_t> ev;
+};
+
+namespace {
+
+// Model buffer layout (offsets only); fills m's offsets when m != nullptr.
+size_t model_layout(const onmt_config* c, onmt_model* m) {
+  Dims d;
+  dims_of(c, &d);
+  Carver cv;
+  auto mat = [&](int Np, int Kp) {
+    Packed p;
+    cv.off = align_up(cv.off);
+    p.off = cv.off;
+    p.Np = Np;
+    p.Kp = Kp;
+    cv.off += (size_t)Np * Kp * d.esz;
+    return p;
+  };
+  auto vec = [&](size_t n) {
+    cv.off = align_up(cv.off);
+    size_t o = cv.off;
+    cv.off += n * sizeof(float);
+    return o;
+  };
+  Packed esrc = mat(d.Vs, d.E);
+  std::vector<Packed> ex, eh, dw;
+  std::vector<size_t> eb, db;
+  for (int l = 0; l < d.L; ++l) {
+    const int in = l == 0 ? d.E : d.Hm;
+    ex.push_back(mat(d.ndir * 4 * d.Hd_pad, d.pad(in)));
+    eb.push_back(vec((size_t)d.ndir * 4 * d.Hd_pad));
+    for (int dir = 0; dir < d.ndir; ++dir) eh.push_back(mat(4 * d.Hd_pad, d.pad(d.Hd)));
+  }
+  Packed etgt = mat(d.Vt, d.E);
+  for (int l = 0; l < d.L; ++l) {
+    const int kp = l == 0 ? d.pad(d.E) + 2 * d.pad(d.H) : 2 * d.pad(d.H);
+    dw.push_back(mat(4 * d.H_pad, kp));
+    db.push_back(vec((size_t)4 * d.H_pad));
+  }
+  Packed wa = mat(ceil_to(d.H, 128), d.pad(d.Hm));
+  Packed wc = mat(ceil_to(d.H, 128), d.pad(d.Hm) + d.pad(d.H));
+  Packed ws = mat(ceil_to(d.Vt, 128), d.pad(d.H));
+  size_t bs = vec(ceil_to(d.Vt, 128));
+  const size_t total = align_up(cv.off);
+  if (m) {
+    char* base = m->dev;
+    auto fix = [&](Packed p) {
+      p.W = base + p.off;
+      return p;
+    };
+    m->E_src = base + esrc.off;
+    m->E_tgt = base + etgt.off;
+    for (auto& p : ex) m->enc_x.push_back(fix(p));
+    for (auto o : eb) m->enc_bias.push_back((const float*)(base + o));
+    for (auto& p : eh) m->enc_h.push_back(fix(p));
+    for (auto& p : dw) m->dec_w.push_back(fix(p));
+    for (auto o : db) m->dec_bias.push_back((const float*)(base + o));
+    m->W_a = fix(wa);
+    m->W_c = fix(wc);
+    m->W_s = fix(ws);
+    m->b_s = (const float*)(base + bs);
+  }
+  return total;
+}
+
+// Host-side packing into the image of the device buffer.
+struct HostImage {
+  std::vector<char> buf;
+  bool bf16;
+  void put(size_t off, size_t idx, float v) {
+    if (bf16) {
+      ((uint16_t*)(buf.data() + off))[idx] = f32_to_bf16_bits(v);
+    } else {
+      ((float*)(buf.data() + off))[idx] = v;
+    }
+  }
+  void putf(size_t off, size_t idx, float v) { ((float*)(buf.data() + off))[idx] = v; }
+};
+
+// Copy columns [c0, c0 + w) of src rows into packed row `prow` at packed column pc0.
+void pack_row(HostImage& img, const Packed& p, int prow, int pc0, const float* src_row, int c0, int w) {
+  for (int j = 0; j < w; ++j) img.put(p.off, (size_t)prow * p.Kp + pc0 + j, src_row[c0 + j]);
+}
+
+}  // namespace
+
+// ====================================================================== ABI
+
+extern "C" {
+
+const char* onmt_last_error(void) { return g_err.c_str(); }
+
+int onmt_num_weights(const onmt_config* cfg) {
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  return (int)weight_specs(cfg).size();
+}
+
+int64_t onmt_weight_numel(const onmt_config* cfg, int i) {
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  auto v = weight_specs(cfg);
+  if (i < 0 || i >= (int)v.size()) return fail(ONMT_EINVAL, "weight index %d out of range", i);
+  return v[i].rows * v[i].cols;
+}
+
+size_t onmt_model_bytes(const onmt_config* cfg) {
+  if (check_config(cfg)) return 0;
+  return model_layout(cfg, nullptr);
+}
+
+int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, int n_weights, void* dev_buf,
+                      size_t dev_bytes, void* stream, onmt_model** out) {
+  int rc = check_config(cfg);
+  if (rc) return rc;
+  if (!out) return fail(ONMT_EINVAL, "out is NULL");
+  *out = nullptr;
+  auto specs = weight_specs(cfg);
+  if (n_weights != (int)specs.size()) return fail(ONMT_EINVAL, "expected %d weight arrays, got %d", (int)specs.size(), n_weights);
+  if (!host_weights) return fail(ONMT_EINVAL, "host_weights is NULL");
+  for (int i = 0; i < n_weights; ++i)
+    if (!host_weights[i]) return fail(ONMT_EINVAL, "host weight %d is NULL", i);
+  if (!dev_buf) return fail(ONMT_EINVAL, "dev_buf is NULL");
+  if ((uintptr_t)dev_buf % kAlign) return fail(ONMT_EINVAL, "dev_buf must be 256-byte aligned");
+  const size_t need = model_layout(cfg, nullptr);
+  if (dev_bytes < need) return fail(ONMT_ESIZE, "model buffer %zu bytes < %zu", dev_bytes, need);
+
+  onmt_model* m = new onmt_model();
+  m->cfg = *cfg;
+  dims_of(cfg, &m->d);
+  m->dev = (char*)dev_buf;
+  model_layout(cfg, m);
+  const Dims& d = m->d;
+
+  HostImage img;
+  img.bf16 = d.bf16;
+  img.buf.assign(need, 0);
+  auto off_of = [&](const void* p) { return (size_t)((const char*)p - m->dev); };
+  int wi = 0;
+  // E_src
+  {
+    const float* s = host_weights[wi++];
+    const size_t o = off_of(m->E_src);
+    for (size_t i = 0; i < (size_t)d.Vs * d.E; ++i) img.put(o, i, s[i]);
+  }
+  for (int l = 0; l < d.L; ++l) {
+    const int in = l == 0 ? d.E : d.Hm;
+    const Packed& X = m->enc_x[l];
+    const size_t bo = off_of(m->enc_bias[l]);
+    for (int dir = 0; dir < d.ndir; ++dir) {
+      const float* W = host_weights[wi++];
+      const float* bvec = host_weights[wi++];
+      const Packed& Hh = m->enc_h[l * d.ndir + dir];
+      for (int g = 0; g < 4; ++g)
+        for (int u = 0; u < d.Hd; ++u) {
+          const float* row = W + (size_t)(g * d.Hd + u) * (in + d.Hd);
+          const int xr = dir * 4 * d.Hd_pad + gate_row(g, u);
+          pack_row(img, X, xr, 0, row, 0, in);
+          pack_row(img, Hh, gate_row(g, u), 0, row, in, d.Hd);
+          img.putf(bo, xr, bvec[g * d.Hd + u]);
+        }
+    }
+  }
+  {
+    const float* s = host_weights[wi++];
+    const size_t o = off_of(m->E_tgt);
+    for (size_t i = 0; i < (size_t)d.Vt * d.E; ++i) img.put(o, i, s[i]);
+  }
+  for (int l = 0; l < d.L; ++l) {
+    const float* W = host_weights[wi++];
+    const float* bvec = host_weights[wi++];
+    const Packed& P = m->dec_w[l];
+    const size_t bo = off_of(m->dec_bias[l]);
+    const int in = l == 0 ? d.E + d.H : d.H;
+    for (int g = 0; g < 4; ++g)
+      for (int u = 0; u < d.H; ++u) {
+        const float* row = W + (size_t)(g * d.H + u) * (in + d.H);
+        const int pr = gate_row(g, u);
+        if (l == 0) {   // segments [embedding | feed | recurrent]
+          pack_row(img, P, pr, 0, row, 0, d.E);
+          pack_row(img, P, pr, d.pad(d.E), row, d.E, d.H);
+          pack_row(img, P, pr, d.pad(d.E) + d.pad(d.H), row, d.E + d.H, d.H);
+        } else {        // segments [layer below | recurrent]
+          pack_row(img, P, pr, 0, row, 0, d.H);
+          pack_row(img, P, pr, d.pad(d.H), row, d.H, d.H);
+        }
+        img.putf(bo, pr, bvec[g * d.H + u]);
+      }
+  }
+  {
+    const float* Wa = host_weights[wi++];
+    for (int r = 0; r < d.H; ++r) pack_row(img, m->W_a, r, 0, Wa + (size_t)r * d.Hm, 0, d.Hm);
+    const float* Wc = host_weights[wi++];
+    for (int r = 0; r < d.H; ++r) {
+      pack_row(img, m->W_c, r, 0, Wc + (size_t)r * (d.Hm + d.H), 0, d.Hm);
+      pack_row(img, m->W_c, r, d.pad(d.Hm), Wc + (size_t)r * (d.Hm + d.H), d.Hm, d.H);
+    }
+    const float* Ws = host_weights[wi++];
+    for (int r = 0; r < d.Vt; ++r) pack_row(img, m->W_s, r, 0, Ws + (size_t)r * d.H, 0, d.H);
+    const float* bs = host_weights[wi++];
+    const size_t bo = off_of(m->b_s);
+    for (int r = 0; r < d.Vt; ++r) img.putf(bo, r, bs[r]);
+  }
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipMemcpyAsync(dev_buf, img.buf.data(), need, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) {
+    delete m;
+    return fail(ONMT_EDEVICE, "weight upload failed: %s", hipGetErrorString(e));
+  }
+  *out = m;
+  return ONMT_OK;
+}
+
+int onmt_model_destroy(onmt_model* m) {
+  if (!m) return fail(ONMT_EINVAL, "model is NULL");
+  for (auto e : m->ev) hipEventDestroy(e);
+  delete m;
+  return ONMT_OK;
+}
+
+}  // extern "C"
+
+// ====================================================================== workspaces
+
+namespace {
+
+struct EncWs {
+  int32_t* lens;
+  int32_t* src;
+  float* memory;     // [B*S, Hm]
+  float* keys;       // [B*S, H]
+  float* final_h;    // [L, B, H]
+  float* final_c;
+  float* gx;         // [B*S, ndir * 4 Hd_pad]
+  float* y[2];       // [B*S, Hm]
+  float* hs[2];      // [ndir, B, Hd]
+  float* cs[2];
+};
+
+size_t enc_layout(const Dims& d, int B, int S, char* base, EncWs* w) {
+  Carver c;
+  c.base = base;
+  EncWs t;
+  const size_t BS = (size_t)B * S;
+  t.lens = c.take<int32_t>(B);
+  t.src = c.take<int32_t>(BS);
+  t.memory = c.take<float>(BS * d.Hm);
+  t.keys = c.take<float>(BS * d.H);
+  t.final_h = c.take<float>((size_t)d.L * B * d.H);
+  t.final_c = c.take<float>((size_t)d.L * B * d.H);
+  t.gx = c.take<float>(BS * d.ndir * 4 * d.Hd_pad);
+  for (int i = 0; i < 2; ++i) t.y[i] = c.take<float>(BS * d.Hm);
+  for (int i = 0; i < 2; ++i) t.hs[i] = c.take<float>((size_t)d.ndir * B * d.Hd);
+  for (int i = 0; i < 2; ++i) t.cs[i] = c.take<float>((size_t)d.ndir * B * d.Hd);
+  if (w) *w = t;
+  return align_up(c.off);
+}
+
+struct State {
+  float* h;      // [L, N, H]
+  float* c;
+  float* feed;   // [N, H]
+};
+
+size_t state_layout(const Dims& d, int N, char* base, State* s) {
+  Carver c;
+  c.base = base;
+  State t;
+  t.h = c.take<float>((size_t)d.L * N * d.H);
+  t.c = c.take<float>((size_t)d.L * N * d.H);
+  t.feed = c.take<float>((size_t)N * d.H);
+  if (s) *s = t;
+  return align_up(c.off);
+}
+
+struct StepWs {
+  float* ctx;      // [N, Hm]
+  float* pmax;     // [N, ntiles]
+  float* psum;
+  float* pval;     // [N, ntiles, K]
+  int32_t* pid;
+  float* tk_val;   // [N, K]
+  int32_t* tk_id;
+  float* lse;      // [N]
+  int ntiles;
+};
+
+size_t step_layout(const Dims& d, int B, int S, int K, char* base, StepWs* w) {
+  (void)S;
+  Carver c;
+  c.base = base;
+  StepWs t;
+  const size_t N = (size_t)B * K;
+  t.ntiles = (d.Vt + gen_tile_cols() - 1) / gen_tile_cols();
+  t.ctx = c.take<float>(N * d.Hm);
+  t.pmax = c.take<float>(N * t.ntiles);
+  t.psum = c.take<float>(N * t.ntiles);
+  t.pval = c.take<float>(N * t.ntiles * K);
+  t.pid = c.take<int32_t>(N * t.ntiles * K);
+  t.tk_val = c.take<float>(N * K);
+  t.tk_id = c.take<int32_t>(N * K);
+  t.lse = c.take<float>(N);
+  if (w) *w = t;
+  return align_up(c.off);
+}
+
+struct SearchWs {
+  EncWs enc;
+  State st[2];
+  StepWs step;
+  BeamParams bp;
+};
+
+size_t search_layout(const Dims& d, int B, int S, int K, int T, char* base, SearchWs* w) {
+  Carver c;
+  c.base = base;
+  SearchWs t{};
+  const size_t N = (size_t)B * K;
+  const size_t eb = enc_layout(d, B, S, nullptr, nullptr);
+  char* e = c.take<char>(eb);
+  enc_layout(d, B, S, e, &t.enc);
+  for (int i = 0; i < 2; ++i) {
+    const size_t sb = state_layout(d, (int)N, nullptr, nullptr);
+    char* s = c.take<char>(sb);
+    state_layout(d, (int)N, s, &t.st[i]);
+  }
+  const size_t pb = step_layout(d, B, S, K, nullptr, nullptr);
+  char* p = c.take<char>(pb);
+  step_layout(d, B, S, K, p, &t.step);
+  BeamParams& q = t.bp;
+  q.score = c.take<double>(N);
+  q.parent = c.take<int32_t>(N);
+  q.tok = c.take<int32_t>(N);
+  q.bp_slot = c.take<int32_t>((size_t)T * N);
+  q.bp_tok = c.take<int32_t>((size_t)T * N);
+  q.bp_logp = c.take<float>((size_t)T * N);
+  q.done = c.take<int32_t>(B);
+  q.steps = c.take<int32_t>(B);
+  q.done_count = c.take<int32_t>(1);
+  q.best_norm = c.take<double>(B);
+  q.best_raw = c.take<double>(B);
+  q.best_t = c.take<int32_t>(B);
+  q.best_slot = c.take<int32_t>(B);
+  q.best_tok = c.take<int32_t>(B);
+  q.best_logp = c.take<float>(B);
+  if (w) *w = t;
+  return align_up(c.off);
+}
+
+Seg seg(const void* base, const int32_t* idx, int ld, int width, int kpad, int bf16) {
+  Seg s;
+  s.base = base;
+  s.idx = idx;
+  s.ld = ld;
+  s.width = width;
+  s.kpad = kpad;
+  s.bf16 = bf16;
+  return s;
+}
+
+BOp bop(const Packed& p) {
+  BOp b;
+  b.W = p.W;
+  b.Np = p.Np;
+  b.Kp = p.Kp;
+  return b;
+}
+
+// Small-M GEMMs: pick the thinner split-K tile when the 32-row tile would leave CUs idle.
+int small_shape(int M, int Np) {
+  const long tiles32 = (long)((M + 31) / 32) * (Np / 64);
+  return tiles32 >= 256 ? kShapeSplitK : kShapeSplitKThin;
+}
+
+// Copies src/len to the host, validates them, and uploads the token ids with every position at or beyond
+// its sentence's length replaced by 0 into clean_src (device, [B, S]), so no kernel gathers an embedding
+// row through an unchecked id.
+int check_len_src(const onmt_model* m, const int32_t* src, const int32_t* len, int B, int S, hipStream_t st,
+                  int* max_len, int32_t* clean_src) {
+  if (!src || !len) return fail(ONMT_EINVAL, "src/len is NULL");
+  if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
+  if ((long long)B * S > (1LL << 28)) return fail(ONMT_EUNSUPPORTED, "B * S_max too large");
+  std::vector<int32_t> hl(B), hs((size_t)B * S);
+  HIP_TRY(hipMemcpyAsync(hl.data(), len, sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipMemcpyAsync(hs.data(), src, sizeof(int32_t) * hs.size(), hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  int mx = 0;
+  for (int b = 0; b < B; ++b) {
+    if (hl[b] < 1 || hl[b] > S) return fail(ONMT_EINVAL, "len[%d] = %d outside [1, %d]", b, hl[b], S);
+    mx = hl[b] > mx ? hl[b] : mx;
+    for (int s = 0; s < hl[b]; ++s) {
+      const int v = hs[(size_t)b * S + s];
+      if (v < 0 || v >= m->cfg.src_vocab) return fail(ONMT_EINVAL, "src[%d, %d] = %d outside [0, %d)", b, s, v, m->cfg.src_vocab);
+    }
+  }
+  for (int b = 0; b < B; ++b)
+    for (int s = hl[b]; s < S; ++s) hs[(size_t)b * S + s] = 0;
+  HIP_TRY(hipMemcpyAsync(clean_src, hs.data(), sizeof(int32_t) * hs.size(), hipMemcpyHostToDevice, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  *max_len = mx;
+  return ONMT_OK;
+}
+
+// Encoder compute on validated inputs (Section 2 encoder RNN; Tables 3-4 bidirectional; readings R2-R5).
+int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B, int S, int max_len, const EncWs& w,
+                   hipStream_t st) {
+  const Dims& d = m->d;
+  const int BS = B * S;
+  (void)src;   // the validated, pad-cleaned ids are already in w.src
+  HIP_TRY(hipMemcpyAsync(w.lens, len, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(fill_f32(w.memory, (size_t)BS * d.Hm, 0.f, st));
+  const int gxw = d.ndir * 4 * d.Hd_pad;
+  for (int l = 0; l < d.L; ++l) {
+    // input projection for every position and both directions at once
+    AOp a{};
+    a.M = BS;
+    a.nseg = 1;
+    if (l == 0) a.seg[0] = seg(m->E_src, w.src, d.E, d.E, d.pad(d.E), d.bf16);
+    else a.seg[0] = seg(w.y[(l - 1) & 1], nullptr, d.Hm, d.Hm, d.pad(d.Hm), 0);
+    StoreParams sp{m->enc_bias[l], w.gx, gxw, gxw, 0};
+    HIP_TRY(gemm_store(d.bf16, kShapeWide, a, bop(m->enc_x[l]), sp, st));
+    HIP_TRY(fill_f32(w.hs[0], (size_t)d.ndir * B * d.Hd, 0.f, st));
+    HIP_TRY(fill_f32(w.cs[0], (size_t)d.ndir * B * d.Hd, 0.f, st));
+    float* yout = (l == d.L - 1) ? w.memory : w.y[l & 1];
+    int cur = 0;
+    for (int step = 0; step < max_len; ++step) {
+      for (int dir = 0; dir < d.ndir; ++dir) {
+        const int s = dir == 0 ? step : max_len - 1 - step;
+        const float* hp = w.hs[cur] + (size_t)dir * B * d.Hd;
+        const float* cp = w.cs[cur] + (size_t)dir * B * d.Hd;
+        AOp r{};
+        r.M = B;
+        r.nseg = 1;
+        r.seg[0] = seg(hp, nullptr, d.Hd, d.Hd, d.pad(d.Hd), 0);
+        LstmParams lp{};
+        lp.bias = nullptr;
+        lp.gx = w.gx;
+        lp.ld_gx = gxw;
+        lp.gx_col0 = dir * 4 * d.Hd_pad;
+        lp.gx_S = S;
+        lp.gx_s = s;
+        lp.c_in = cp;
+        lp.c_idx = nullptr;
+        lp.ld_c = d.Hd;
+        lp.h_in = hp;
+        lp.ld_h_in = d.Hd;
+        lp.h_out = w.hs[cur ^ 1] + (size_t)dir * B * d.Hd;
+        lp.c_out = w.cs[cur ^ 1] + (size_t)dir * B * d.Hd;
+        lp.ld_out = d.Hd;
+        lp.y_out = yout;
+        lp.ld_y = d.Hm;
+        lp.y_S = S;
+        lp.y_s = s;
+        lp.y_col0 = dir * d.Hd;
+        lp.lens = w.lens;
+        lp.H = d.Hd;
+        const Packed& Wh = m->enc_h[l * d.ndir + dir];
+        HIP_TRY(gemm_lstm(d.bf16, small_shape(B, Wh.Np), r, bop(Wh), lp, st));
+      }
+      cur ^= 1;
+    }
+    for (int dir = 0; dir < d.ndir; ++dir) {
+      HIP_TRY(copy_cols(w.hs[cur] + (size_t)dir * B * d.Hd, d.Hd, w.final_h + (size_t)l * B * d.H + dir * d.Hd, d.H, B,
+                        d.Hd, st));
+      HIP_TRY(copy_cols(w.cs[cur] + (size_t)dir * B * d.Hd, d.Hd, w.final_c + (size_t)l * B * d.H + dir * d.Hd, d.H, B,
+                        d.Hd, st));
+    }
+  }
+  // attention keys W_a m_s, once per batch
+  AOp a{};
+  a.M = BS;
+  a.nseg = 1;
+  a.seg[0] = seg(w.memory, nullptr, d.Hm, d.Hm, d.pad(d.Hm), 0);
+  StoreParams kp{nullptr, w.keys, d.H, d.H, 0};
+  HIP_TRY(gemm_store(d.bf16, kShapeWide, a, bop(m->W_a), kp, st));
+  return ONMT_OK;
+}
+
+int decode_init_compute(onmt_model* m, const EncWs& w, int B, int K, const State& s, hipStream_t st) {
+  const Dims& d = m->d;
+  const int N = B * K;
+  for (int l = 0; l < d.L; ++l) {
+    HIP_TRY(replicate_rows(w.final_h + (size_t)l * B * d.H, d.H, B, K, s.h + (size_t)l * N * d.H, d.H, d.H, st));
+    HIP_TRY(replicate_rows(w.final_c + (size_t)l * B * d.H, d.H, B, K, s.c + (size_t)l * N * d.H, d.H, d.H, st));
+  }
+  HIP_TRY(fill_f32(s.feed, (size_t)N * d.H, 0.f, st));
+  return ONMT_OK;
+}
+
+void time_begin(onmt_model* m, hipStream_t st) {
+  if (!m->prof) return;
+  hipEvent_t a, b;
+  if (hipEventCreate(&a) != hipSuccess) return;
+  if (hipEventCreate(&b) != hipSuccess) {
+    hipEventDestroy(a);
+    return;
+  }
+  m->ev.push_back(a);
+  m->ev.push_back(b);
+  hipEventRecord(a, st);
+}
+void time_end(onmt_model* m, hipStream_t st) {
+  if (!m->prof || m->ev.size() < 2) return;
+  hipEventRecord(m->ev.back(), st);
+}
+void time_collect(onmt_model* m) {
+  for (size_t i = 0; i + 1 < m->ev.size(); i += 2) {
+    float ms = 0.f;
+    if (hipEventSynchronize(m->ev[i + 1]) == hipSuccess && hipEventElapsedTime(&ms, m->ev[i], m->ev[i + 1]) == hipSuccess) {
+      m->prof_ms += ms;
+      m->prof_n += 1;
+    }
+  }
+  for (auto e : m->ev) hipEventDestroy(e);
+  m->ev.clear();
+}
+
+// One decoder step on validated inputs (Section 2; Figure 1(a); items (a)-(c); Section 4.2 attention).
+// mode 0: logp [N, V] full log-softmax; mode 1: top-K (logp [N, K], ids [N, K]).
+int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const State& in, const State& out,
+                   const int32_t* prev_tok, const int32_t* parent, int mode, float* logp, int32_t* ids, float* lse,
+                   float* attn, const StepWs& sw, hipStream_t st) {
+  const Dims& d = m->d;
+  const int N = B * K;
+  const size_t LH = (size_t)N * d.H;
+  for (int l = 0; l < d.L; ++l) {
+    AOp a{};
+    a.M = N;
+    if (l == 0) {
+      a.nseg = 3;
+      a.seg[0] = seg(m->E_tgt, prev_tok, d.E, d.E, d.pad(d.E), d.bf16);
+      a.seg[1] = seg(in.feed, parent, d.H, d.H, d.pad(d.H), 0);
+      a.seg[2] = seg(in.h, parent, d.H, d.H, d.pad(d.H), 0);
+    } else {
+      a.nseg = 2;
+      a.seg[0] = seg(out.h + (l - 1) * LH, nullptr, d.H, d.H, d.pad(d.H), 0);
+      a.seg[1] = seg(in.h + l * LH, parent, d.H, d.H, d.pad(d.H), 0);
+    }
+    LstmParams lp{};
+    lp.bias = m->dec_bias[l];
+    lp.c_in = in.c + l * LH;
+    lp.c_idx = parent;
+    lp.ld_c = d.H;
+    lp.h_out = out.h + l * LH;
+    lp.c_out = out.c + l * LH;
+    lp.ld_out = d.H;
+    lp.H = d.H;
+    HIP_TRY(gemm_lstm(d.bf16, small_shape(N, m->dec_w[l].Np), a, bop(m->dec_w[l]), lp, st));
+  }
+  const float* q = out.h + (d.L - 1) * LH;
+  HIP_TRY(attention(q, d.H, w.keys, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.ctx, attn, st));
+  {
+    AOp a{};
+    a.M = N;
+    a.nseg = 2;
+    a.seg[0] = seg(sw.ctx, nullptr, d.Hm, d.Hm, d.pad(d.Hm), 0);
+    a.seg[1] = seg(q, nullptr, d.H, d.H, d.pad(d.H), 0);
+    StoreParams sp{nullptr, out.feed, d.H, d.H, 1};
+    HIP_TRY(gemm_store(d.bf16, small_shape(N, m->W_c.Np), a, bop(m->W_c), sp, st));
+  }
+  {
+    AOp a{};
+    a.M = N;
+    a.nseg = 1;
+    a.seg[0] = seg(out.feed, nullptr, d.H, d.H, d.pad(d.H), 0);
+    GenParams gp{};
+    gp.bias = m->b_s;
+    gp.V = d.Vt;
+    gp.K = K;
+    gp.ntiles = sw.ntiles;
+    gp.pmax = sw.pmax;
+    gp.psum = sw.psum;
+    gp.pval = sw.pval;
+    gp.pid = sw.pid;
+    gp.logits = mode == 0 ? logp : nullptr;
+    gp.ld_logits = d.Vt;
+    time_begin(m, st);
+    HIP_TRY(gemm_gen(d.bf16, a, bop(m->W_s), gp, st));
+    time_end(m, st);
+  }
+  float* lse_out = lse ? lse : sw.lse;
+  if (mode == 0) {
+    HIP_TRY(lse_topk_merge(sw.pmax, sw.psum, sw.pval, sw.pid, N, sw.ntiles, K, sw.tk_val, sw.tk_id, lse_out, st));
+    HIP_TRY(subtract_rows(logp, d.Vt, lse_out, N, d.Vt, st));
+  } else {
+    HIP_TRY(lse_topk_merge(sw.pmax, sw.psum, sw.pval, sw.pid, N, sw.ntiles, K, logp, ids, lse_out, st));
+  }
+  return ONMT_OK;
+}
+
+int check_beam(const onmt_model* m, int S, int K) {
+  if (K < 1 || K > kMaxBeam) return fail(ONMT_EUNSUPPORTED, "beam %d outside [1, %d]", K, kMaxBeam);
+  if (K > m->cfg.tgt_vocab) return fail(ONMT_EINVAL, "beam %d larger than the vocabulary", K);
+  if (attention_lds_bytes(S, m->d.H, K) > 64 * 1024)
+    return fail(ONMT_EUNSUPPORTED, "beam * (hidden + S_max) too large for one attention workgroup");
+  return ONMT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t onmt_encode_ws_bytes(const onmt_model* m, int B, int S) {
+  if (!m || B < 1 || S < 1) return 0;
+  return enc_layout(m->d, B, S, nullptr, nullptr);
+}
+
+int onmt_encode(onmt_model* m, const int32_t* src, const int32_t* len, int B, int S, void* ws, size_t ws_bytes,
+                void* stream) {
+  if (!m) return fail(ONMT_EINVAL, "model is NULL");
+  if (!ws) return fail(ONMT_EINVAL, "enc_ws is NULL");
+  hipStream_t st = (hipStream_t)stream;
+  if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
+  if (ws_bytes < enc_layout(m->d, B, S, nullptr, nullptr)) return fail(ONMT_ESIZE, "encoder workspace too small");
+  EncWs w;
+  enc_layout(m->d, B, S, (char*)ws, &w);
+  int mx = 0;
+  int rc = check_len_src(m, src, len, B, S, st, &mx, w.src);
+  if (rc) return rc;
+  return encode_compute(m, src, len, B, S, mx, w, st);
+}
+
+size_t onmt_state_bytes(const onmt_model* m, int N) {
+  if (!m || N < 1) return 0;
+  return state_layout(m->d, N, nullptr, nullptr);
+}
+
+size_t onmt_step_ws_bytes(const onmt_model* m, int B, int S, int K) {
+  if (!m || B < 1 || S < 1 || K < 1) return 0;
+  return step_layout(m->d, B, S, K, nullptr, nullptr);
+}
+
+int onmt_decode_init(onmt_model* m, const void* enc_ws, int B, int S, int K, void* state_out, void* stream) {
+  if (!m || !enc_ws || !state_out) return fail(ONMT_EINVAL, "NULL argument");
+  if (B < 1 || S < 1 || K < 1) return fail(ONMT_EINVAL, "B, S_max, K must be >= 1");
+  EncWs w;
+  enc_layout(m->d, B, S, (char*)enc_ws, &w);
+  State s;
+  state_layout(m->d, B * K, (char*)state_out, &s);
+  return decode_init_compute(m, w, B, K, s, (hipStream_t)stream);
+}
+
+int onmt_decode_step(onmt_model* m, const void* enc_ws, int B, int S, int K, const void* state_in, void* state_out,
+                     const int32_t* prev_tok, const int32_t* parent, int mode, float* logp, int32_t* ids, float* lse,
+                     float* attn, void* step_ws, size_t step_ws_bytes, void* stream) {
+  if (!m || !enc_ws || !state_in || !state_out || !prev_tok || !logp || !step_ws) return fail(ONMT_EINVAL, "NULL argument");
+  if (state_in == state_out) return fail(ONMT_EINVAL, "state_in and state_out must differ");
+  if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
+  int rc = check_beam(m, S, K);
+  if (rc) return rc;
+  if (mode != 0 && mode != 1) return fail(ONMT_EINVAL, "mode must be 0 (full) or 1 (top-K)");
+  if (mode == 1 && !ids) return fail(ONMT_EINVAL, "ids is NULL in top-K mode");
+  if (step_ws_bytes < step_layout(m->d, B, S, K, nullptr, nullptr)) return fail(ONMT_ESIZE, "step workspace too small");
+  hipStream_t st = (hipStream_t)stream;
+  const int N = B * K;
+  std::vector<int32_t> ht(N), hp(parent ? N : 0);
+  HIP_TRY(hipMemcpyAsync(ht.data(), prev_tok, sizeof(int32_t) * N, hipMemcpyDeviceToHost, st));
+  if (parent) HIP_TRY(hipMemcpyAsync(hp.data(), parent, sizeof(int32_t) * N, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  for (int r = 0; r < N; ++r) {
+    if (ht[r] < 0 || ht[r] >= m->cfg.tgt_vocab) return fail(ONMT_EINVAL, "prev_tok[%d] = %d out of range", r, ht[r]);
+    if (parent && (hp[r] < 0 || hp[r] >= N)) return fail(ONMT_EINVAL, "parent[%d] = %d out of range", r, hp[r]);
+  }
+  EncWs w;
+  enc_layout(m->d, B, S, (char*)enc_ws, &w);
+  State si, so;
+  state_layout(m->d, N, (char*)state_in, &si);
+  state_layout(m->d, N, (char*)state_out, &so);
+  StepWs sw;
+  step_layout(m->d, B, S, K, (char*)step_ws, &sw);
+  rc = decode_compute(m, w, B, S, K, si, so, prev_tok, parent, mode, logp, ids, lse, attn, sw, st);
+  if (m->prof) {
+    HIP_TRY(hipStreamSynchronize(st));
+    time_collect(m);
+  }
+  return rc;
+}
+
+size_t onmt_search_ws_bytes(const onmt_model* m, int B, int S, const onmt_search_params* p) {
+  if (!m || !p || B < 1 || S < 1 || p->beam < 1 || p->max_len < 1) return 0;
+  return search_layout(m->d, B, S, p->beam, p->max_len, nullptr, nullptr);
+}
+
+int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int B, int S,
+                     const onmt_search_params* prm, void* ws, size_t ws_bytes, int32_t* out_tok, int32_t* out_len,
+                     double* out_raw, double* out_norm, float* out_tok_logp, const onmt_trace* trace, void* stream) {
+  if (!m || !prm || !ws) return fail(ONMT_EINVAL, "NULL argument");
+  if (!out_tok || !out_len || !out_raw || !out_norm) return fail(ONMT_EINVAL, "NULL output pointer");
+  const int K = prm->beam, T = prm->max_len;
+  if (T < 1 || T > 100000) return fail(ONMT_EINVAL, "max_len %d outside [1, 100000]", T);
+  if (!(prm->alpha >= 0.0) || !std::isfinite(prm->alpha)) return fail(ONMT_EINVAL, "alpha must be finite and >= 0");
+  if (trace && (!trace->slot || !trace->tok || !trace->cand || !trace->steps))
+    return fail(ONMT_EINVAL, "trace given with a NULL array");
+  if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
+  int rc = check_beam(m, S, K);
+  if (rc) return rc;
+  if (ws_bytes < search_layout(m->d, B, S, K, T, nullptr, nullptr)) return fail(ONMT_ESIZE, "search workspace too small");
+  hipStream_t st = (hipStream_t)stream;
+  SearchWs w;
+  search_layout(m->d, B, S, K, T, (char*)ws, &w);
+  int mx = 0;
+  rc = check_len_src(m, src, len, B, S, st, &mx, w.enc.src);
+  if (rc) return rc;
+
+  BeamParams bp = w.bp;
+  bp.B = B;
+  bp.K = K;
+  bp.V = m->cfg.tgt_vocab;
+  bp.T_max = T;
+  bp.eos = m->cfg.eos_id;
+  bp.pad = m->cfg.pad_id;
+  bp.alpha = prm->alpha;
+  bp.lp_tmax = std::pow((5.0 + T) / 6.0, prm->alpha);
+  bp.tk_val = w.step.tk_val;
+  bp.tk_id = w.step.tk_id;
+  bp.tr_slot = trace ? trace->slot : nullptr;
+  bp.tr_tok = trace ? trace->tok : nullptr;
+  bp.tr_cand = trace ? trace->cand : nullptr;
+
+  rc = encode_compute(m, src, len, B, S, mx, w.enc, st);
+  if (rc) return rc;
+  rc = decode_init_compute(m, w.enc, B, K, w.st[0], st);
+  if (rc) return rc;
+  HIP_TRY(beam_init(bp, m->cfg.bos_id, st));
+  const int every = prm->check_every > 0 ? prm->check_every : (T <= 32 ? 1 : 8);
+  int cur = 0;
+  for (int t = 1; t <= T; ++t) {
+    rc = decode_compute(m, w.enc, B, S, K, w.st[cur], w.st[cur ^ 1], bp.tok, bp.parent, 1, w.step.tk_val,
+                        w.step.tk_id, nullptr, nullptr, w.step, st);
+    if (rc) return rc;
+    HIP_TRY(beam_step(bp, t, st));
+    cur ^= 1;
+    if (t < T && t % every == 0) {
+      int32_t done = 0;
+      HIP_TRY(hipMemcpyAsync(&done, bp.done_count, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+      HIP_TRY(hipStreamSynchronize(st));
+      if (done >= B) break;
+    }
+  }
+  HIP_TRY(backtrack(bp, out_tok, out_len, out_raw, out_norm, out_tok_logp, st));
+  if (trace) HIP_TRY(hipMemcpyAsync(trace->steps, bp.steps, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  if (m->prof) time_collect(m);
+  return ONMT_OK;
+}
+
+int onmt_profile_enable(onmt_model* m, int on) {
+  if (!m) return fail(ONMT_EINVAL, "model is NULL");
+  m->prof = on != 0;
+  return ONMT_OK;
+}
+
+int onmt_profile_read(onmt_model* m, int* n, double* ms, int reset) {
+  if (!m || !n || !ms) return fail(ONMT_EINVAL, "NULL argument");
+  *n = m->prof_n;
+  *ms = m->prof_ms;
+  if (reset) {
+    m->prof_n = 0;
+    m->prof_ms = 0.0;
+  }
+  return ONMT_OK;
+}
+
+}  // extern "C"

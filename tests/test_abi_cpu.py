@@ -1,0 +1,102 @@
+"""The C-ABI library loads, exports every declared symbol and validates configs (no GPU needed)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_1805_11462_amd import _lib
+from paper_1805_11462_amd.translator import make_config
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "onmt.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(onmt_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported_and_bound():
+    lib = _lib.load()
+    names = declared_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in _lib.SIGNATURES, f"{n} has no binding"
+    assert set(_lib.SIGNATURES) == set(names)
+
+
+def cfg_of(w):
+    return make_config(w.enc_layers, w.dec_layers, w.bidirectional, w.emb, w.hidden, w.src_vocab, w.tgt_vocab,
+                       w.wdtype)
+
+
+@pytest.mark.parametrize("name", list(W.WORKLOADS))
+def test_weight_order_matches_the_shared_generator(name):
+    w = W.get(name)
+    lib = _lib.load()
+    cfg = cfg_of(w)
+    specs = W.weight_specs(w)
+    assert lib.onmt_num_weights(ctypes.byref(cfg)) == len(specs)
+    for i, (_, shape) in enumerate(specs):
+        assert lib.onmt_weight_numel(ctypes.byref(cfg), i) == int(np.prod(shape))
+    assert lib.onmt_model_bytes(ctypes.byref(cfg)) > 0
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("dec_layers", 3, _lib.ONMT_EINVAL),        # encoder/decoder depth mismatch
+    ("enc_layers", 0, _lib.ONMT_EINVAL),
+    ("wdtype", 2, _lib.ONMT_EINVAL),
+    ("emb", 30, _lib.ONMT_EUNSUPPORTED),        # not a multiple of 4
+    ("eos_id", 50000, _lib.ONMT_EINVAL),
+    ("tgt_vocab", 3, _lib.ONMT_EINVAL),
+])
+def test_invalid_configs_are_rejected(field, value, code):
+    lib = _lib.load()
+    cfg = cfg_of(W.get("default"))
+    setattr(cfg, field, value)
+    assert lib.onmt_num_weights(ctypes.byref(cfg)) == code
+    assert lib.onmt_model_bytes(ctypes.byref(cfg)) == 0
+    assert len(lib.onmt_last_error()) > 0
+
+
+def test_bf16_needs_emb_multiple_of_8():
+    lib = _lib.load()
+    cfg = cfg_of(W.get("larger"))
+    cfg.emb = 1004
+    assert lib.onmt_num_weights(ctypes.byref(cfg)) == _lib.ONMT_EUNSUPPORTED
+
+
+def test_null_handles_are_rejected_without_a_device():
+    lib = _lib.load()
+    assert lib.onmt_encode_ws_bytes(None, 4, 10) == 0
+    assert lib.onmt_model_destroy(None) == _lib.ONMT_EINVAL
+    assert lib.onmt_encode(None, None, None, 1, 1, None, 0, None) == _lib.ONMT_EINVAL
+    assert lib.onmt_beam_search(None, None, None, 1, 1, None, None, 0, None, None, None, None, None, None,
+                                None) == _lib.ONMT_EINVAL
+    n = ctypes.c_int()
+    ms = ctypes.c_double()
+    assert lib.onmt_profile_read(None, ctypes.byref(n), ctypes.byref(ms), 0) == _lib.ONMT_EINVAL
+
+
+def test_model_create_rejects_bad_arguments_before_touching_memory():
+    lib = _lib.load()
+    cfg = cfg_of(W.get("tiny"))
+    out = ctypes.c_void_p()
+    n = lib.onmt_num_weights(ctypes.byref(cfg))
+    arr = (ctypes.c_void_p * n)()
+    # wrong count, NULL arrays, NULL buffer, too-small buffer: all rejected during validation
+    assert lib.onmt_model_create(ctypes.byref(cfg), arr, n - 1, None, 0, None, ctypes.byref(out)) == _lib.ONMT_EINVAL
+    assert lib.onmt_model_create(ctypes.byref(cfg), arr, n, None, 0, None, ctypes.byref(out)) == _lib.ONMT_EINVAL
+    keep = [np.zeros(lib.onmt_weight_numel(ctypes.byref(cfg), i), np.float32) for i in range(n)]
+    for i, a in enumerate(keep):
+        arr[i] = a.ctypes.data
+    assert lib.onmt_model_create(ctypes.byref(cfg), arr, n, None, 0, None, ctypes.byref(out)) == _lib.ONMT_EINVAL
+    assert lib.onmt_model_create(ctypes.byref(cfg), arr, n, ctypes.c_void_p(256), 16, None,
+                                 ctypes.byref(out)) == _lib.ONMT_ESIZE
+    assert lib.onmt_model_create(ctypes.byref(cfg), arr, n, ctypes.c_void_p(8), 1 << 40, None,
+                                 ctypes.byref(out)) == _lib.ONMT_EINVAL      # misaligned

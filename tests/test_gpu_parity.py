@@ -1,0 +1,225 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, element by element.
+
+Tolerances: per-step log-probs within 1e-4 absolute (fp32 workloads) or 2e-2 (bf16 weights, fp32
+accumulation); attention weights within 1e-5 / 1e-2. Token choices must be identical wherever the
+oracle's selection gaps exceed twice the tolerance; elsewhere the step-by-step replay of the GPU's
+decisions must pass (any choice within the tolerance is correct).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import onmt_oracle as O
+from tests._gpu import Setup, TAU, ATTN_TOL, with_workload
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return Setup(W.get("tiny"))
+
+
+@pytest.fixture(scope="module")
+def tiny_peaked():
+    return Setup(W.get("tiny"), peaked=True)
+
+
+@pytest.fixture(scope="module")
+def default():
+    return Setup(W.get("default"))
+
+
+def _print_case(name, **kw):
+    print(f"[case] {name} " + " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
+
+
+# ------------------------------------------------------------------ encoder
+@pytest.mark.parametrize("which", ["tiny", "tiny_peaked", "default"])
+def test_encoder_matches_oracle(which, request):
+    s = request.getfixturevalue(which)
+    _print_case("encoder", workload=s.w.name)
+    B, S = s.src.shape
+    ws = s.tr.encode(s.src_d, s.lens_d)
+    torch.cuda.synchronize()
+    mem, keys, fh, fc = s.tr.enc_views(ws, B, S)
+    enc = O.encode(s.model, s.src, s.lens)
+    np.testing.assert_allclose(mem.cpu().numpy(), enc.memory, atol=1e-5, rtol=0)
+    mask = enc.mask
+    assert (mem.cpu().numpy()[~mask] == 0).all()
+    ref_keys = enc.memory @ s.model.w["W_a"].T
+    np.testing.assert_allclose(keys.cpu().numpy()[mask], ref_keys[mask], atol=1e-5, rtol=0)
+    for l in range(s.w.dec_layers):
+        np.testing.assert_allclose(fh[l].cpu().numpy(), enc.final_h[l], atol=1e-5, rtol=0)
+        np.testing.assert_allclose(fc[l].cpu().numpy(), enc.final_c[l], atol=1e-5, rtol=0)
+
+
+# ------------------------------------------------------------------ decoder step
+def _oracle_state(s, st_views, N):
+    h, c, feed = st_views
+    return O.State([h[l].cpu().numpy().astype(np.float64) for l in range(s.w.dec_layers)],
+                   [c[l].cpu().numpy().astype(np.float64) for l in range(s.w.dec_layers)],
+                   feed.cpu().numpy().astype(np.float64))
+
+
+@pytest.mark.parametrize("which", ["tiny", "tiny_peaked", "default"])
+def test_decode_steps_full_and_topk(which, request):
+    s = request.getfixturevalue(which)
+    w = s.w
+    B, S = s.src.shape
+    K = w.beam
+    N = B * K
+    _print_case("decode_step", workload=w.name, N=N)
+    tr = s.tr
+    ws = tr.encode(s.src_d, s.lens_d)
+    st = tr.decode_init(ws, B, S, K)
+    enc = O.encode(s.model, s.src, s.lens)
+    ost = O.init_state(s.model, enc, K)
+    rows = np.repeat(np.arange(B), K)
+    rng = np.random.default_rng(7)
+    tok = np.full(N, W.BOS_ID, np.int32)
+    parent = None
+    for step in range(3):
+        tok_d = torch.from_numpy(tok).cuda()
+        par_d = torch.from_numpy(parent).cuda() if parent is not None else None
+        st_full, logp, _, lse, attn = tr.decode_step(ws, B, S, K, st, tok_d, par_d, mode=0, want_attn=True)
+        st_topk, tv, ti, lse2, _ = tr.decode_step(ws, B, S, K, st, tok_d, par_d, mode=1)
+        torch.cuda.synchronize()
+        o_in = ost if parent is None else ost.take(parent)
+        o_new, o_logp, o_attn = O.decode_step(s.model, enc, o_in, tok, rows)
+        g_logp = logp.cpu().numpy()
+        err = np.abs(g_logp - o_logp).max()
+        print(f"  step {step}: max |logp - oracle| = {err:.3g}", flush=True)
+        assert err <= s.tau
+        np.testing.assert_allclose(attn.cpu().numpy(), o_attn, atol=ATTN_TOL[w.wdtype], rtol=0)
+        # top-K mode: values within tau, ids exact where the oracle's sorted gaps exceed 2 tau
+        o_sorted = np.argsort(-o_logp, axis=1, kind="stable")[:, :K + 1]
+        g_ids = ti.cpu().numpy()
+        g_val = tv.cpu().numpy()
+        for r in range(N):
+            np.testing.assert_allclose(g_val[r], o_logp[r, g_ids[r]], atol=s.tau, rtol=0)
+            vals = o_logp[r, o_sorted[r]]
+            for j in range(K):
+                gap_ok = (j == 0 or vals[j - 1] - vals[j] > 2 * s.tau) and vals[j] - vals[j + 1] > 2 * s.tau
+                if gap_ok:
+                    assert g_ids[r, j] == o_sorted[r, j], (r, j)
+        # full and top-K runs wrote the same state
+        for a, b in zip(tr.state_views(st_full, N), tr.state_views(st_topk, N)):
+            assert torch.equal(a, b)
+        np.testing.assert_allclose(lse.cpu().numpy(), lse2.cpu().numpy(), atol=0, rtol=0)
+        h, c, feed = tr.state_views(st_full, N)
+        for l in range(w.dec_layers):
+            np.testing.assert_allclose(h[l].cpu().numpy(), o_new.h[l], atol=1e-5, rtol=0)
+            np.testing.assert_allclose(c[l].cpu().numpy(), o_new.c[l], atol=1e-5, rtol=0)
+        np.testing.assert_allclose(feed.cpu().numpy(), o_new.feed, atol=1e-5, rtol=0)
+        # next step: random in-sentence parents and random tokens
+        parent = (np.repeat(np.arange(B), K) * K + rng.integers(0, K, size=N)).astype(np.int32)
+        tok = rng.integers(0, w.tgt_vocab, size=N).astype(np.int32)
+        st = st_full
+        ost = o_new
+
+
+# ------------------------------------------------------------------ beam search
+def _check_search(s, buf, sentences, K, T, alpha):
+    tau = s.tau
+    g_tok = buf["tok"].cpu().numpy()
+    g_len = buf["len"].cpu().numpy()
+    g_raw = buf["raw"].cpu().numpy()
+    g_norm = buf["norm"].cpu().numpy()
+    g_lp = buf["tok_logp"].cpu().numpy()
+    trace = {k: [a for a in buf[f"trace_{k}"].cpu().numpy()] for k in ("slot", "tok", "cand")}
+    mismatched = []
+    for b in sentences:
+        res = O.beam_search(s.model, s.src[b:b + 1], s.lens[b:b + 1], K, T, alpha)
+        n = int(g_len[b])
+        toks = list(g_tok[b, :n])
+        assert (g_tok[b, n:] == W.PAD_ID).all()
+        # the GPU's own result is internally consistent: per-token log-probs sum to raw, norm = raw / lp
+        assert abs(g_lp[b, :n].astype(np.float64).sum() - g_raw[b]) < 1e-6 * max(1, n)
+        assert abs(g_norm[b] - g_raw[b] / O.length_penalty(n, alpha)) < 1e-9 * max(1.0, abs(g_raw[b]))
+        # teacher-forced oracle rescoring of the GPU's hypothesis
+        forced = O.score_forced(s.model, s.src[b], s.lens[b], toks)
+        assert np.abs(forced - g_lp[b, :n]).max() <= tau
+        assert abs(forced.sum() - g_raw[b]) <= n * tau
+        if toks == res.tokens[0]:
+            assert abs(res.raw[0] - g_raw[b]) <= n * tau
+        else:
+            mismatched.append(b)
+    # every sentence (matched or not) must pass the step-by-step replay of the GPU's decisions
+    bad = O.replay_verify(s.model, s.src, s.lens, K, T, alpha, trace, tau, sentences=sentences)
+    assert bad == [], bad[:10]
+    return mismatched
+
+
+@pytest.mark.parametrize("which,alpha", [("tiny", 0.0), ("tiny", 0.6), ("tiny_peaked", 0.0), ("tiny_peaked", 0.6)])
+def test_beam_search_tiny(which, alpha, request):
+    s = request.getfixturevalue(which)
+    w = s.w
+    B, S = s.src.shape
+    _print_case("beam_search", workload=w.name, alpha=alpha)
+    buf = s.tr.search_buffers(B, S, w.beam, w.max_len, alpha, trace=True)
+    s.tr.beam_search(s.src_d, s.lens_d, buf)
+    torch.cuda.synchronize()
+    mism = _check_search(s, buf, range(B), w.beam, w.max_len, alpha)
+    print(f"  free-run token mismatches (replay-verified): {mism}", flush=True)
+
+
+@pytest.mark.parametrize("K", [1, 3, 8, 16])
+def test_beam_widths_tiny_peaked(tiny_peaked, K):
+    s = tiny_peaked
+    B, S = s.src.shape
+    _print_case("beam_width", K=K)
+    buf = s.tr.search_buffers(B, S, K, 9, 0.6, trace=True)
+    s.tr.beam_search(s.src_d, s.lens_d, buf)
+    torch.cuda.synchronize()
+    _check_search(s, buf, range(B), K, 9, 0.6)
+
+
+def test_beam_search_default_sampled(default):
+    # full default workload (64 sentences, beam 5, max 100) on the GPU; oracle on sampled sentences
+    s = default
+    w = s.w
+    B, S = s.src.shape
+    _print_case("beam_search", workload=w.name, B=B)
+    buf = s.tr.search_buffers(B, S, w.beam, w.max_len, w.alpha, trace=True)
+    s.tr.beam_search(s.src_d, s.lens_d, buf)
+    torch.cuda.synchronize()
+    g_len = buf["len"].cpu().numpy()
+    assert (g_len >= 1).all() and (g_len <= w.max_len).all()
+    _check_search(s, buf, [0, 37, 63], w.beam, w.max_len, w.alpha)
+
+
+def test_search_is_deterministic(tiny_peaked):
+    s = tiny_peaked
+    B, S = s.src.shape
+    outs = []
+    for _ in range(2):
+        buf = s.tr.search_buffers(B, S, 4, 10, 0.6, trace=False)
+        s.tr.beam_search(s.src_d, s.lens_d, buf)
+        torch.cuda.synchronize()
+        outs.append({k: buf[k].cpu().numpy() for k in ("tok", "len", "raw", "norm", "tok_logp")})
+    for k in outs[0]:
+        np.testing.assert_array_equal(outs[0][k], outs[1][k])
+
+
+def test_all_zero_weights_tie_rules():
+    # every candidate ties: the tie-break to the smaller flat index and the stop rule on equality
+    w = with_workload(W.get("tiny"), tgt_vocab=50, src_vocab=50)
+    s = Setup(w)
+    s.weights = {k: np.zeros_like(v) for k, v in s.weights.items()}
+    from tests._gpu import translator_for
+    tr = translator_for(w, s.weights)
+    B, S = s.src.shape
+    for K, want in ((3, [W.PAD_ID] * 6), (4, [W.EOS_ID])):
+        buf = tr.search_buffers(B, S, K, 6, 0.0)
+        tr.beam_search(s.src_d, s.lens_d, buf)
+        torch.cuda.synchronize()
+        for b in range(B):
+            n = int(buf["len"][b])
+            assert list(buf["tok"][b, :n].cpu().numpy()) == want
+            assert abs(buf["raw"][b].item() + len(want) * np.log(50)) < 1e-5

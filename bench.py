@@ -1,0 +1,154 @@
+"""Throughput of batched beam-search translation on one MI355X, with roofline and CPU-oracle baselines.
+
+One step = one onmt_beam_search call over the paper-default workload (2-layer 500-unit LSTM encoder and
+input-feeding decoder, emb 500, general attention, vocab 50000, batch 64 with source lengths 10-50,
+beam 5, max decode 100, fp32), i.e. encoder + every decoder step + beam bookkeeping + backtrack, with
+the source batch and weights already resident in device memory.
+
+Prints one JSON line: target tokens/s over the timed steps, the generator kernel's achieved fraction of
+the fp32 MFMA peak (timed with HIP events on the library's stream inside the timed region), and the CPU
+oracle's throughput on a bounded sample of the same workload.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "target tokens/sec, beam-5 2×500 LSTM batch 64; MFMA util / HBM GB/s fraction"
+PEAK_FP32_TFLOPS = 157.3
+PEAK_BF16_TFLOPS = 2500.0
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "gen_gemm_default_counters.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="default")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sentences", type=int, default=4)
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "common.h", "kernels.h"):
+        h.update(open(os.path.join(ROOT, "paper_1805_11462_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_counters(per_launch_flops_key):
+    """HBM bytes per generator launch from committed rocprofv3 counters, if taken on the current kernel."""
+    try:
+        c = json.load(open(COUNTERS_FILE))
+    except (OSError, ValueError):
+        return None
+    if c.get("kernel_source_hash") != kernel_source_hash() or c.get("workload") != per_launch_flops_key:
+        return None
+    return c.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, weights, src, lens, n_sent):
+    """The oracle (fp64 NumPy) on the first n_sent sentences of the same batch, on this host's cores."""
+    import numpy as np
+    from oracle import onmt_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    m = O.model_from(w, weights)
+    t0 = time.perf_counter()
+    res = O.beam_search(m, src[:n_sent], lens[:n_sent], w.beam, w.max_len, w.alpha)
+    dt = time.perf_counter() - t0
+    toks = int(sum(len(t) for t in res.tokens))
+    return {"value": round(toks / dt, 3), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n_sent} of the {src.shape[0]} sentences (full beam search incl. encoder), "
+                      f"{toks} target tokens in {dt:.1f} s, fp64 NumPy"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU design shards "
+              f"sentences across GPUs and is not measured here", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_1805_11462_amd.translator import Translator, make_config
+
+    w = W.get(args.workload)
+    weights = W.make_weights(w)
+    src, lens = W.make_batch(w)
+    B, S = src.shape
+    cfg = make_config(w.enc_layers, w.dec_layers, w.bidirectional, w.emb, w.hidden, w.src_vocab, w.tgt_vocab,
+                      w.wdtype)
+    tr = Translator(cfg, [weights[n] for n, _ in W.weight_specs(w)], device="cuda:0")
+    src_d = torch.from_numpy(src).cuda()
+    lens_d = torch.from_numpy(lens).cuda()
+    buf = tr.search_buffers(B, S, w.beam, w.max_len, w.alpha)
+
+    for i in range(args.warmup):
+        tr.beam_search(src_d, lens_d, buf)
+        print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+
+    tr.profile(True)
+    tr.profile_read(reset=True)
+    tokens = 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        tr.beam_search(src_d, lens_d, buf)
+        tokens += int(buf["len"].sum().item())
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    n_gen, gen_ms = tr.profile_read(reset=True)
+    tr.profile(False)
+    print(f"[bench] timed {args.steps} steps in {dt:.3f} s", file=sys.stderr, flush=True)
+
+    N = B * w.beam
+    gen_flops = 2.0 * N * w.tgt_vocab * w.hidden          # per generator launch (vocabulary projection)
+    avg_gen_s = gen_ms / 1e3 / max(n_gen, 1)
+    achieved = gen_flops / avg_gen_s / 1e12 if n_gen else 0.0
+    peak = PEAK_BF16_TFLOPS if w.wdtype == "bf16" else PEAK_FP32_TFLOPS
+    out = {
+        "metric": METRIC,
+        "value": round(tokens / dt, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(dt / args.steps * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.wdtype == "fp32" else "bf16",
+        "data": "synthetic (seeded uniform(-0.1,0.1) weights, bounded-Zipf source tokens)",
+        "config": {"workload": f"{w.name}: {w.enc_layers}x{w.hidden} LSTM enc/dec, emb {w.emb}, vocab {w.tgt_vocab}, "
+                               f"batch {w.batch}, src len {w.len_lo}-{w.len_hi}, beam {w.beam}, "
+                               f"max decode {w.max_len}, alpha {w.alpha}, {w.wdtype}",
+                   "global_batch": B, "beam": w.beam, "max_decode": w.max_len,
+                   "target_tokens_per_step": tokens // max(args.steps, 1)},
+        "roofline": {"kernel": "k_gemm_gen (generator GEMM + fused log-softmax/top-K partials)",
+                     "bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": traffic_from_counters(w.name),
+                     "launches_timed": n_gen, "avg_launch_us": round(avg_gen_s * 1e6, 2),
+                     "flops_per_launch": gen_flops},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, weights, src, lens, args.cpu_sentences)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

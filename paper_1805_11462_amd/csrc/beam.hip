@@ -7,72 +7,133 @@
 namespace onmt {
 
 // ------------------------------------------------------------------ softmax merge
-// One wave per row: combine per-tile (max, sum exp) into logsumexp and per-tile top-K lists into the
-// row's top-K (larger logit first, smaller id on ties). Outputs log-probs z - lse.
-template <int KMAX>
-__global__ __launch_bounds__(256) void k_lse_topk(const float* __restrict__ pmax, const float* __restrict__ psum,
-                                                  const float* __restrict__ pval, const int32_t* __restrict__ pid,
-                                                  int M, int ntiles, int K, float* __restrict__ out_val,
-                                                  int32_t* __restrict__ out_id, float* __restrict__ out_lse) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (row >= M) return;
+// One workgroup per row: combine per-tile (max, sum exp) into the row's logsumexp, and select the row's
+// top-K (larger logit first, smaller id on ties) from the per-tile top-K lists by K rounds of a
+// workgroup-wide argmax. Candidates are processed in chunks of 256 * kMergeCap; the running top-K of
+// earlier chunks takes part in every later chunk's rounds. Outputs log-probs z - lse.
+constexpr int kMergeThreads = 256;
+constexpr int kMergeCap = 8;
+
+__device__ inline void block_best(float& v, int& id, float* sv, int* si) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ov = __shfl_xor(v, o, kWave);
+    const int oi = __shfl_xor(id, o, kWave);
+    if (better(ov, oi, v, id)) {
+      v = ov;
+      id = oi;
+    }
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sv[wave] = v;
+    si[wave] = id;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kMergeThreads / kWave; ++w)
+    if (better(sv[w], si[w], v, id)) {
+      v = sv[w];
+      id = si[w];
+    }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kMergeThreads) void k_lse_topk(const float* __restrict__ pmax,
+                                                           const float* __restrict__ psum,
+                                                           const float* __restrict__ pval,
+                                                           const int32_t* __restrict__ pid, int M, int ntiles,
+                                                           int K, float* __restrict__ out_val,
+                                                           int32_t* __restrict__ out_id, float* __restrict__ out_lse) {
+  __shared__ float sv[kMergeThreads / kWave];
+  __shared__ int si[kMergeThreads / kWave];
+  __shared__ float run_v[kMaxBeam];
+  __shared__ int run_i[kMaxBeam];
+  const int row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const float ninf = -__builtin_inff();
   const size_t base = (size_t)row * ntiles;
-  float mx = -__builtin_inff();
-  for (int t = lane; t < ntiles; t += kWave) mx = fmaxf(mx, pmax[base + t]);
-  const float gmx = wave_max(mx);
+  // logsumexp
+  float mx = ninf;
+  for (int t = tid; t < ntiles; t += kMergeThreads) mx = fmaxf(mx, pmax[base + t]);
+  int dummy = 0;
+  {
+    float v = mx;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    if ((tid & 63) == 0) sv[tid >> 6] = v;
+    __syncthreads();
+    mx = sv[0];
+#pragma unroll
+    for (int w = 1; w < kMergeThreads / kWave; ++w) mx = fmaxf(mx, sv[w]);
+    __syncthreads();
+  }
   float sm = 0.f;
-  float val[KMAX];
-  int ids[KMAX];
-  topk_clear<KMAX>(val, ids);
-  for (int t = lane; t < ntiles; t += kWave) {
-    sm += psum[base + t] * __expf(pmax[base + t] - gmx);
-    for (int i = 0; i < K; ++i) topk_insert<KMAX>(val, ids, pval[(base + t) * K + i], pid[(base + t) * K + i]);
-  }
-  sm = wave_sum(sm);
-  const float lse = gmx + __logf(sm);
-  if (out_lse && lane == 0) out_lse[row] = lse;
-  for (int k = 0; k < K; ++k) {
-    float bv = val[0];
-    int bi = ids[0];
+  for (int t = tid; t < ntiles; t += kMergeThreads) sm += psum[base + t] * __expf(pmax[base + t] - mx);
+  {
+    float v = wave_sum(sm);
+    if ((tid & 63) == 0) sv[tid >> 6] = v;
+    __syncthreads();
+    sm = 0.f;
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, kWave);
-      const int oi = __shfl_xor(bi, o, kWave);
-      if (better(ov, oi, bv, bi)) {
-        bv = ov;
-        bi = oi;
+    for (int w = 0; w < kMergeThreads / kWave; ++w) sm += sv[w];
+    __syncthreads();
+  }
+  const float lse = mx + __logf(sm);
+  (void)dummy;
+  // top-K
+  if (tid < kMaxBeam) {
+    run_v[tid] = ninf;
+    run_i[tid] = 0x7fffffff;
+  }
+  __syncthreads();
+  const int n = ntiles * K;
+  for (int c0 = 0; c0 < n; c0 += kMergeThreads * kMergeCap) {
+    float v[kMergeCap + 1];
+    int id[kMergeCap + 1];
+#pragma unroll
+    for (int i = 0; i < kMergeCap; ++i) {
+      const int c = c0 + tid + i * kMergeThreads;
+      v[i] = c < n ? pval[base * K + c] : ninf;
+      id[i] = c < n ? pid[base * K + c] : 0x7fffffff;
+    }
+    v[kMergeCap] = tid < K ? run_v[tid] : ninf;
+    id[kMergeCap] = tid < K ? run_i[tid] : 0x7fffffff;
+    __syncthreads();
+    uint32_t taken = 0;
+    for (int k = 0; k < K; ++k) {
+      float bv = ninf;
+      int bi = 0x7fffffff;
+      int bj = -1;
+#pragma unroll
+      for (int i = 0; i <= kMergeCap; ++i) {
+        if (!((taken >> i) & 1u) && better(v[i], id[i], bv, bi)) {
+          bv = v[i];
+          bi = id[i];
+          bj = i;
+        }
+      }
+      const int mine = bi;
+      block_best(bv, bi, sv, si);
+      if (bj >= 0 && mine == bi && bv > ninf) taken |= 1u << bj;
+      if (tid == 0) {
+        run_v[k] = bv;
+        run_i[k] = bi;
       }
     }
-    if (ids[0] == bi && val[0] == bv) {        // this lane owned the winner: pop it
-#pragma unroll
-      for (int i = 0; i + 1 < KMAX; ++i) {
-        val[i] = val[i + 1];
-        ids[i] = ids[i + 1];
-      }
-      val[KMAX - 1] = -__builtin_inff();
-      ids[KMAX - 1] = 0x7fffffff;
-    }
-    if (lane == 0) {
-      out_val[(size_t)row * K + k] = bv - lse;
-      if (out_id) out_id[(size_t)row * K + k] = bi;
-    }
+    __syncthreads();
   }
+  if (tid < K) {
+    out_val[(size_t)row * K + tid] = run_v[tid] - lse;
+    if (out_id) out_id[(size_t)row * K + tid] = run_i[tid];
+  }
+  if (tid == 0 && out_lse) out_lse[row] = lse;
 }
 
 hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pval, const int32_t* pid, int M,
                           int ntiles, int K, float* out_val, int32_t* out_id, float* out_lse, hipStream_t st) {
-  dim3 grid((M + 3) / 4), block(256);
-  if (K <= 1)
-    hipLaunchKernelGGL(k_lse_topk<1>, grid, block, 0, st, pmax, psum, pval, pid, M, ntiles, K, out_val, out_id, out_lse);
-  else if (K <= 2)
-    hipLaunchKernelGGL(k_lse_topk<2>, grid, block, 0, st, pmax, psum, pval, pid, M, ntiles, K, out_val, out_id, out_lse);
-  else if (K <= 4)
-    hipLaunchKernelGGL(k_lse_topk<4>, grid, block, 0, st, pmax, psum, pval, pid, M, ntiles, K, out_val, out_id, out_lse);
-  else if (K <= 8)
-    hipLaunchKernelGGL(k_lse_topk<8>, grid, block, 0, st, pmax, psum, pval, pid, M, ntiles, K, out_val, out_id, out_lse);
-  else
-    hipLaunchKernelGGL(k_lse_topk<16>, grid, block, 0, st, pmax, psum, pval, pid, M, ntiles, K, out_val, out_id, out_lse);
+  hipLaunchKernelGGL(k_lse_topk, dim3(M), dim3(kMergeThreads), 0, st, pmax, psum, pval, pid, M, ntiles, K, out_val,
+                     out_id, out_lse);
   return hipGetLastError();
 }
 

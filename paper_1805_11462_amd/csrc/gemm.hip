@@ -2,8 +2,9 @@
 //
 // Computes acc[r, n] = sum_k A[r, k] * W[n, k] where A is gathered on the fly from up to three
 // row-mapped segments (embedding rows by token id, state rows by beam parent, plain activations)
-// and W is a packed weight matrix. The tile is staged through LDS (two buffers, one barrier per
-// K stage) and multiplied with 16x16 MFMA tiles: v_mfma_f32_16x16x4_f32 for fp32 operands and
+// and W is a packed weight matrix. Tiles are staged through two LDS buffers; global loads run two
+// K stages ahead in registers so that a stage's loads have a full stage of MFMA work to hide behind.
+// Products use 16x16 MFMA tiles: v_mfma_f32_16x16x4_f32 for fp32 operands and
 // v_mfma_f32_16x16x32_bf16 for bf16 operands, always accumulating in fp32. Waves may split K
 // inside the workgroup (WK > 1); their partial tiles are summed in LDS before the epilogue.
 //
@@ -16,12 +17,13 @@
 
 namespace onmt {
 
-template <class T, int WM_, int WN_, int WK_, int TM_, int TN_>
+template <class T, int WM_, int WN_, int WK_, int TM_, int TN_, int KW_>
 struct Tile {
   static constexpr int WM = WM_, WN = WN_, WK = WK_, TM = TM_, TN = TN_;
   static constexpr bool kBf16 = sizeof(T) == 2;
   static constexpr int CH = 16 / sizeof(T);          // elements per 16-byte chunk
-  static constexpr int KW = kBf16 ? 32 : 16;         // K per wave per stage
+  static constexpr int KW = KW_;                     // K per wave per stage
+  static constexpr int KSUB = kBf16 ? 32 : 16;       // K consumed per MFMA round (one 16-byte read per lane)
   static constexpr int BM = WM * TM * 16;
   static constexpr int BN = WN * TN * 16;
   static constexpr int BK = WK * KW;
@@ -30,12 +32,14 @@ struct Tile {
   static constexpr int CPR = BK / CH;                // chunks per tile row
   static constexpr int A_CH = BM * CPR;
   static constexpr int B_CH = BN * CPR;
-  static constexpr int A_PT = (A_CH + NT - 1) / NT;
-  static constexpr int B_PT = (B_CH + NT - 1) / NT;
+  static constexpr int A_PT = A_CH / NT;
+  static constexpr int B_PT = B_CH / NT;
   static constexpr int STAGE = (BM + BN) * ROW * (int)sizeof(T);
   static constexpr int CROW = BN + 4;                // fp32 output tile row stride
   static constexpr int CT = WK * BM * CROW * 4;
   static constexpr int LDS = (2 * STAGE > CT) ? 2 * STAGE : CT;
+  static_assert(A_CH % NT == 0 && B_CH % NT == 0, "chunks must divide evenly among threads");
+  static_assert(KW % KSUB == 0 && kSegK % BK == 0, "stage must divide the segment padding");
 };
 
 // XCD-aware tile order: blocks are dealt round-robin to the 8 XCDs, so renumber them so that each
@@ -49,37 +53,13 @@ __device__ inline int xcd_remap(int bid, int nblocks) {
 
 __device__ inline uint4 zero4() { return make_uint4(0u, 0u, 0u, 0u); }
 
-// Load one 16-byte chunk of A (CH elements starting at padded column k) for GEMM row r.
-template <class T>
-__device__ inline uint4 load_a_chunk(const AOp& a, const char* const (&rowp)[3], int k) {
-  int off = 0;
-#pragma unroll
-  for (int s = 0; s < 3; ++s) {
-    if (s < a.nseg) {
-      const Seg& g = a.seg[s];
-      if (k < off + g.kpad) {
-        const int kk = k - off;
-        if (rowp[s] == nullptr || kk >= g.width) return zero4();
-        if constexpr (sizeof(T) == 4) {
-          return *(const uint4*)(rowp[s] + (size_t)kk * 4);
-        } else {
-          if (g.bf16) return *(const uint4*)(rowp[s] + (size_t)kk * 2);
-          // fp32 source feeding a bf16 product: round to nearest even
-          const float4 lo = *(const float4*)(rowp[s] + (size_t)kk * 4);
-          float4 hi = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (kk + 4 < g.width) hi = *(const float4*)(rowp[s] + (size_t)(kk + 4) * 4);
-          uint4 r;
-          r.x = f32_to_bf16_bits(lo.x) | ((uint32_t)f32_to_bf16_bits(lo.y) << 16);
-          r.y = f32_to_bf16_bits(lo.z) | ((uint32_t)f32_to_bf16_bits(lo.w) << 16);
-          r.z = f32_to_bf16_bits(hi.x) | ((uint32_t)f32_to_bf16_bits(hi.y) << 16);
-          r.w = f32_to_bf16_bits(hi.z) | ((uint32_t)f32_to_bf16_bits(hi.w) << 16);
-          return r;
-        }
-      }
-      off += g.kpad;
-    }
-  }
-  return zero4();
+__device__ inline uint4 f32x8_to_bf16x8(const float4& lo, const float4& hi) {
+  uint4 r;
+  r.x = f32_to_bf16_bits(lo.x) | ((uint32_t)f32_to_bf16_bits(lo.y) << 16);
+  r.y = f32_to_bf16_bits(lo.z) | ((uint32_t)f32_to_bf16_bits(lo.w) << 16);
+  r.z = f32_to_bf16_bits(hi.x) | ((uint32_t)f32_to_bf16_bits(hi.y) << 16);
+  r.w = f32_to_bf16_bits(hi.z) | ((uint32_t)f32_to_bf16_bits(hi.w) << 16);
+  return r;
 }
 
 // Main loop: leaves the (WK-way partial) fp32 output tile in LDS at smem, layout [WK][BM][CROW].
@@ -93,66 +73,54 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
   const int wm = wave / (C::WK * C::WN);
   const int i16 = lane & 15, g = lane >> 4;
 
-  // Per-thread A row pointers (rows fixed across K stages).
-  const char* arow[C::A_PT][3];
-  int acol[C::A_PT];
-  bool aok[C::A_PT];
+  // Segment table (uniform). Every field is read with a constant index into a scalar, so the argument
+  // struct is never indexed at run time (which would put it in private memory).
+  const int nseg = a.nseg;
+  const int kp0 = a.seg[0].kpad, kp1 = a.seg[1].kpad, kp2 = a.seg[2].kpad;
+  const int wd0 = a.seg[0].width, wd1 = a.seg[1].width, wd2 = a.seg[2].width;
+  const int bf0 = a.seg[0].bf16, bf1 = a.seg[1].bf16, bf2 = a.seg[2].bf16;
+
+  // Per-thread A row pointers, one per segment (rows are fixed across K stages).
+  // Thread chunk c = tid + i * NT covers tile row c / CPR, columns (c % CPR) * CH ...; NT is a multiple
+  // of CPR, so the column is the same for every i and the row advances by NT / CPR.
+  constexpr int RSTEP = C::NT / C::CPR;
+  static_assert(C::NT % C::CPR == 0, "threads must cover whole tile rows");
+  const int arow0 = tid / C::CPR;
+  const int acol = (tid % C::CPR) * C::CH;
+  const char* ar0[C::A_PT];
+  const char* ar1[C::A_PT];
+  const char* ar2[C::A_PT];
+#define ONMT_ROW_PTR(S, r)                                                                            \
+  ((const char*)a.seg[S].base +                                                                      \
+   (size_t)(a.seg[S].idx ? a.seg[S].idx[r] : (r)) * a.seg[S].ld * (a.seg[S].bf16 ? 2 : 4))
 #pragma unroll
   for (int i = 0; i < C::A_PT; ++i) {
-    const int c = tid + i * C::NT;
-    const int row = c / C::CPR;
-    acol[i] = (c % C::CPR) * C::CH;
-    aok[i] = c < C::A_CH;
-    const int r = m0 + row;
-#pragma unroll
-    for (int s = 0; s < 3; ++s) {
-      arow[i][s] = nullptr;
-      if (aok[i] && s < a.nseg && r < a.M) {
-        const Seg& sg = a.seg[s];
-        const int rr = sg.idx ? sg.idx[r] : r;
-        arow[i][s] = (const char*)sg.base + (size_t)rr * sg.ld * (sg.bf16 ? 2 : 4);
-      }
-    }
+    const int r = m0 + arow0 + i * RSTEP;
+    const bool rv = r < a.M;
+    ar0[i] = rv ? ONMT_ROW_PTR(0, r) : nullptr;
+    ar1[i] = (rv && nseg > 1) ? ONMT_ROW_PTR(1, r) : nullptr;
+    ar2[i] = (rv && nseg > 2) ? ONMT_ROW_PTR(2, r) : nullptr;
   }
-  const char* brow[C::B_PT];
-  int bcol[C::B_PT];
-  bool bok[C::B_PT];
-#pragma unroll
-  for (int i = 0; i < C::B_PT; ++i) {
-    const int c = tid + i * C::NT;
-    const int row = c / C::CPR;
-    bcol[i] = (c % C::CPR) * C::CH;
-    bok[i] = c < C::B_CH;
-    brow[i] = (const char*)b.W + (size_t)(n0 + row) * b.Kp * sizeof(T);
-  }
+#undef ONMT_ROW_PTR
+  const char* brow = (const char*)b.W + ((size_t)(n0 + arow0) * b.Kp + acol) * sizeof(T);
+  const size_t bstep = (size_t)RSTEP * b.Kp * sizeof(T);
 
   T* As[2] = {(T*)smem, (T*)(smem + C::STAGE)};
   T* Bs[2] = {As[0] + C::BM * C::ROW, As[1] + C::BM * C::ROW};
 
-  uint4 ra[C::A_PT], rb[C::B_PT];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < C::A_PT; ++i) {
-      const int k = k0 + acol[i];
-      ra[i] = (aok[i] && k < b.Kp) ? load_a_chunk<T>(a, arow[i], k) : zero4();
-    }
-#pragma unroll
-    for (int i = 0; i < C::B_PT; ++i) {
-      const int k = k0 + bcol[i];
-      rb[i] = (bok[i] && k < b.Kp) ? *(const uint4*)(brow[i] + (size_t)k * sizeof(T)) : zero4();
-    }
+  // One K stage of operands in flight: held in registers between its global load and its LDS store.
+  struct Regs {
+    uint4 a[C::A_PT];
+    uint4 b[C::B_PT];
   };
-  auto lstore = [&](int buf) {
+  // Loads are issued unconditionally (out-of-range chunks read a valid dummy address and are zeroed
+  // afterwards) so the loop stays straight-line and the compiler can keep both stages in flight.
+  const char* dummy = (const char*)b.W;
+  auto lstore = [&](int buf, const Regs& r) {
 #pragma unroll
-    for (int i = 0; i < C::A_PT; ++i) {
-      const int c = tid + i * C::NT;
-      if (aok[i]) *(uint4*)(As[buf] + (c / C::CPR) * C::ROW + acol[i]) = ra[i];
-    }
+    for (int i = 0; i < C::A_PT; ++i) *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + acol) = r.a[i];
 #pragma unroll
-    for (int i = 0; i < C::B_PT; ++i) {
-      const int c = tid + i * C::NT;
-      if (bok[i]) *(uint4*)(Bs[buf] + (c / C::CPR) * C::ROW + bcol[i]) = rb[i];
-    }
+    for (int i = 0; i < C::B_PT; ++i) *(uint4*)(Bs[buf] + (arow0 + i * RSTEP) * C::ROW + acol) = r.b[i];
   };
 
   f32x4 acc[C::TM][C::TN];
@@ -161,43 +129,97 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
 #pragma unroll
     for (int y = 0; y < C::TN; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nst = (b.Kp + C::BK - 1) / C::BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    const int buf = st & 1;
-    if (st + 1 < nst) gload((st + 1) * C::BK);
+  auto compute = [&](int buf) {
     const T* Ab = As[buf] + (wm * C::TM * 16 + i16) * C::ROW + wk * C::KW;
     const T* Bb = Bs[buf] + (wn * C::TN * 16 + i16) * C::ROW + wk * C::KW;
-    if constexpr (!C::kBf16) {
-      f32x4 av[C::TM], bv[C::TN];
 #pragma unroll
-      for (int x = 0; x < C::TM; ++x) av[x] = *(const f32x4*)(Ab + x * 16 * C::ROW + 4 * g);
+    for (int sub = 0; sub < C::KW / C::KSUB; ++sub) {
+      if constexpr (!C::kBf16) {
+        f32x4 av[C::TM], bv[C::TN];
 #pragma unroll
-      for (int y = 0; y < C::TN; ++y) bv[y] = *(const f32x4*)(Bb + y * 16 * C::ROW + 4 * g);
+        for (int x = 0; x < C::TM; ++x) av[x] = *(const f32x4*)(Ab + x * 16 * C::ROW + sub * 16 + 4 * g);
 #pragma unroll
-      for (int m = 0; m < 4; ++m)
+        for (int y = 0; y < C::TN; ++y) bv[y] = *(const f32x4*)(Bb + y * 16 * C::ROW + sub * 16 + 4 * g);
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+          for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+            for (int y = 0; y < C::TN; ++y)
+              acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x][m], bv[y][m], acc[x][y], 0, 0, 0);
+      } else {
+        bf16x8 av[C::TM], bv[C::TN];
+#pragma unroll
+        for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ab + x * 16 * C::ROW + sub * 32 + 8 * g);
+#pragma unroll
+        for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + sub * 32 + 8 * g);
 #pragma unroll
         for (int x = 0; x < C::TM; ++x)
 #pragma unroll
           for (int y = 0; y < C::TN; ++y)
-            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x][m], bv[y][m], acc[x][y], 0, 0, 0);
-    } else {
-      bf16x8 av[C::TM], bv[C::TN];
-#pragma unroll
-      for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ab + x * 16 * C::ROW + 8 * g);
-#pragma unroll
-      for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + 8 * g);
-#pragma unroll
-      for (int x = 0; x < C::TM; ++x)
-#pragma unroll
-        for (int y = 0; y < C::TN; ++y)
-          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+      }
     }
-    if (st + 1 < nst) lstore(buf ^ 1);
+  };
+
+  // K runs segment by segment, each with its own two-stage pipeline, so the row pointers a stage reads
+  // are known at compile time (selecting among them at run time would put them in private memory).
+  int kbase = 0;
+  auto run_segment = [&](const char* const (&arp)[C::A_PT], int width, int src_bf16, int kpad) {
+    const bool sbf = src_bf16 != 0;
+    auto gload = [&](int st) -> Regs {
+      Regs r;
+      const int kk = st * C::BK + acol;
+#pragma unroll
+      for (int i = 0; i < C::A_PT; ++i) {
+        const char* rp = arp[i];
+        const bool ok = rp != nullptr && kk < width;
+        if constexpr (!C::kBf16) {
+          const uint4 v = *(const uint4*)(ok ? rp + (size_t)kk * 4 : dummy);
+          r.a[i] = ok ? v : zero4();
+        } else {
+          // bf16 source: 8 elements in one 16-byte load; fp32 source: two 16-byte loads rounded to bf16
+          // (nearest, ties to even). Widths are multiples of 4, so the second half may be past the end.
+          const bool ok_hi = ok && !sbf && kk + 4 < width;
+          const uint4 lo = *(const uint4*)(ok ? rp + (size_t)kk * (sbf ? 2 : 4) : dummy);
+          const uint4 hi = *(const uint4*)(ok_hi ? rp + (size_t)(kk + 4) * 4 : dummy);
+          const float4 flo = __builtin_bit_cast(float4, lo);
+          const float4 fhi = ok_hi ? __builtin_bit_cast(float4, hi) : make_float4(0.f, 0.f, 0.f, 0.f);
+          const uint4 cv = f32x8_to_bf16x8(flo, fhi);
+          r.a[i] = !ok ? zero4() : (sbf ? lo : cv);
+        }
+      }
+      const size_t kb = (size_t)(kbase + st * C::BK) * sizeof(T);
+#pragma unroll
+      for (int i = 0; i < C::B_PT; ++i) r.b[i] = *(const uint4*)(brow + i * bstep + kb);
+      return r;
+    };
+    // Loads and LDS stores are unconditional: past the last stage they re-read the last stage and fill a
+    // buffer that is never multiplied, which keeps the loop free of data-dependent branches.
+    const int nst = kpad / C::BK;       // segment widths are padded to multiples of kSegK, hence of BK
+    const int last = nst - 1;
+    Regs r0 = gload(0);
+    Regs r1 = gload(min(1, last));
+    lstore(0, r0);
     __syncthreads();
-  }
+    for (int st = 0; st < nst; st += 2) {
+      // even stage: LDS buffer 0 holds stage st, r1 holds st + 1
+      r0 = gload(min(st + 2, last));
+      compute(0);
+      lstore(1, r1);
+      __syncthreads();
+      if (st + 1 >= nst) break;
+      // odd stage: LDS buffer 1 holds stage st + 1, r0 holds st + 2
+      r1 = gload(min(st + 3, last));
+      compute(1);
+      lstore(0, r0);
+      __syncthreads();
+    }
+    kbase += kpad;
+  };
+  run_segment(ar0, wd0, bf0, kp0);
+  if (nseg > 1) run_segment(ar1, wd1, bf1, kp1);
+  if (nseg > 2) run_segment(ar2, wd2, bf2, kp2);
 
   // Partial tiles to LDS: lane holds rows 4g..4g+3 of column i16 of each 16x16 block.
   float* Ct = (float*)smem + wk * C::BM * C::CROW;
@@ -282,8 +304,10 @@ __global__ __launch_bounds__(C::NT) void k_gemm_lstm(AOp a, BOp b, LstmParams p,
   }
 }
 
-// Generator: 4 threads per row, 32 contiguous columns each, merged with lane shuffles.
-template <class T, class C, int KMAX>
+// Generator: 4 threads per row, 32 contiguous columns each. Row max and sum of exponentials are
+// combined with lane shuffles; the tile's top-K is taken with K rounds of a 4-lane argmax (larger
+// logit first, smaller id on ties), each thread skipping the columns it already gave away.
+template <class T, class C>
 __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, int nm, int nblocks) {
   static_assert(C::NT / C::BM == 4 && C::BN == 128, "generator tile is 64 x 128 with 256 threads");
   __shared__ __attribute__((aligned(16))) char smem[C::LDS];
@@ -294,19 +318,20 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
   const float* Ct = (const float*)smem;
   const int r = threadIdx.x >> 2, part = threadIdx.x & 3;
   const int row = m0 + r;
-  const int c0 = part * 32;
+  const int c0 = n0 + part * 32;
+  const float ninf = -__builtin_inff();
   float z[32];
-  float mx = -__builtin_inff();
+  float mx = ninf;
 #pragma unroll
   for (int j = 0; j < 32; ++j) {
-    const int gc = n0 + c0 + j;
-    z[j] = (gc < p.V) ? ctile<C>(Ct, r, c0 + j) + p.bias[gc] : -__builtin_inff();
+    const int gc = c0 + j;
+    z[j] = gc < p.V ? ctile<C>(Ct, r, part * 32 + j) + p.bias[gc] : ninf;
     mx = fmaxf(mx, z[j]);
   }
   if (p.logits && row < a.M) {
 #pragma unroll
     for (int j = 0; j < 32; j += 4) {
-      const int gc = n0 + c0 + j;
+      const int gc = c0 + j;
       if (gc + 3 < p.V && (p.ld_logits & 3) == 0) {
         *(float4*)(p.logits + (size_t)row * p.ld_logits + gc) = make_float4(z[j], z[j + 1], z[j + 2], z[j + 3]);
       } else {
@@ -315,59 +340,56 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
       }
     }
   }
-  float val[KMAX];
-  int ids[KMAX];
-  topk_clear<KMAX>(val, ids);
+  float rmx = fmaxf(mx, __shfl_xor(mx, 1, kWave));
+  rmx = fmaxf(rmx, __shfl_xor(rmx, 2, kWave));
   float sm = 0.f;
-  if (mx > -__builtin_inff()) {
+#pragma unroll
+  for (int j = 0; j < 32; ++j) sm += __expf(z[j] - rmx);     // exp(-inf) = 0 for columns past V
+  sm += __shfl_xor(sm, 1, kWave);
+  sm += __shfl_xor(sm, 2, kWave);
+  const size_t o = (size_t)row * p.ntiles + nt;
+  if (part == 0 && row < a.M) {
+    p.pmax[o] = rmx;
+    p.psum[o] = sm;
+  }
+  uint32_t taken = 0;
+  for (int k = 0; k < p.K; ++k) {
+    float bv = ninf;
+    int bj = 0;
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
-      if (z[j] > -__builtin_inff()) {
-        sm += __expf(z[j] - mx);
-        topk_insert<KMAX>(val, ids, z[j], n0 + c0 + j);
+      const bool free = !((taken >> j) & 1u);
+      if (free && z[j] > bv) {                    // strict: the earlier (smaller id) column wins ties
+        bv = z[j];
+        bj = j;
       }
     }
-  }
-  // merge the 4 parts of the row (lanes 4q .. 4q+3 of one wave)
+    int bid = bv > ninf ? c0 + bj : 0x7fffffff;
 #pragma unroll
-  for (int o = 1; o < 4; o <<= 1) {
-    const float omx = __shfl_xor(mx, o, kWave);
-    const float osm = __shfl_xor(sm, o, kWave);
-    const float nmx = fmaxf(mx, omx);
-    sm = (mx > -__builtin_inff() ? sm * __expf(mx - nmx) : 0.f) + (omx > -__builtin_inff() ? osm * __expf(omx - nmx) : 0.f);
-    mx = nmx;
-    float ov[KMAX];
-    int oi[KMAX];
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) {
-      ov[i] = __shfl_xor(val[i], o, kWave);
-      oi[i] = __shfl_xor(ids[i], o, kWave);
-    }
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) topk_insert<KMAX>(val, ids, ov[i], oi[i]);
-  }
-  if (part == 0 && row < a.M) {
-    const size_t o = (size_t)row * p.ntiles + nt;
-    p.pmax[o] = mx;
-    p.psum[o] = sm;
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i) {
-      if (i < p.K) {
-        p.pval[o * p.K + i] = val[i];
-        p.pid[o * p.K + i] = ids[i];
+    for (int s = 1; s < 4; s <<= 1) {
+      const float ov = __shfl_xor(bv, s, kWave);
+      const int oi = __shfl_xor(bid, s, kWave);
+      if (better(ov, oi, bv, bid)) {
+        bv = ov;
+        bid = oi;
       }
+    }
+    if (bid == c0 + bj && bv > ninf) taken |= 1u << bj;
+    if (part == 0 && row < a.M) {
+      p.pval[o * p.K + k] = bv;
+      p.pid[o * p.K + k] = bid;
     }
   }
 }
 
 // ---------------------------------------------------------------- launchers
 
-using TileWide32 = Tile<float, 2, 2, 1, 2, 4>;
-using TileSplit32 = Tile<float, 1, 1, 4, 2, 4>;
-using TileThin32 = Tile<float, 1, 1, 4, 1, 4>;
-using TileWide16 = Tile<__bf16, 2, 2, 1, 2, 4>;
-using TileSplit16 = Tile<__bf16, 1, 1, 4, 2, 4>;
-using TileThin16 = Tile<__bf16, 1, 1, 4, 1, 4>;
+using TileWide32 = Tile<float, 2, 2, 1, 2, 4, 32>;
+using TileSplit32 = Tile<float, 1, 1, 4, 2, 4, 16>;
+using TileThin32 = Tile<float, 1, 1, 4, 1, 4, 16>;
+using TileWide16 = Tile<__bf16, 2, 2, 1, 2, 4, 64>;
+using TileSplit16 = Tile<__bf16, 1, 1, 4, 2, 4, 32>;
+using TileThin16 = Tile<__bf16, 1, 1, 4, 1, 4, 32>;
 
 template <class C>
 static inline void grid_of(const AOp& a, const BOp& b, int& nm, int& nblocks) {
@@ -396,12 +418,12 @@ static hipError_t launch_lstm(const AOp& a, const BOp& b, const LstmParams& p, h
   return hipGetLastError();
 }
 
-template <class T, class C, int KMAX>
+template <class T, class C>
 static hipError_t launch_gen(const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
   int nm, nb;
   grid_of<C>(a, b, nm, nb);
   if (nb == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_gen<T, C, KMAX>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+  hipLaunchKernelGGL((k_gemm_gen<T, C>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
   return hipGetLastError();
 }
 
@@ -428,11 +450,7 @@ hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const Lstm
 }
 
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
-  if (p.K <= 1) return bf16 ? launch_gen<__bf16, TileWide16, 1>(a, b, p, st) : launch_gen<float, TileWide32, 1>(a, b, p, st);
-  if (p.K <= 2) return bf16 ? launch_gen<__bf16, TileWide16, 2>(a, b, p, st) : launch_gen<float, TileWide32, 2>(a, b, p, st);
-  if (p.K <= 4) return bf16 ? launch_gen<__bf16, TileWide16, 4>(a, b, p, st) : launch_gen<float, TileWide32, 4>(a, b, p, st);
-  if (p.K <= 8) return bf16 ? launch_gen<__bf16, TileWide16, 8>(a, b, p, st) : launch_gen<float, TileWide32, 8>(a, b, p, st);
-  return bf16 ? launch_gen<__bf16, TileWide16, 16>(a, b, p, st) : launch_gen<float, TileWide32, 16>(a, b, p, st);
+  return bf16 ? launch_gen<__bf16, TileWide16>(a, b, p, st) : launch_gen<float, TileWide32>(a, b, p, st);
 }
 
 }  // namespace onmt

@@ -6,6 +6,10 @@
 
 namespace onmt {
 
+// K segments of GEMM operands are padded to multiples of this many elements; every tile's K stage
+// (32, 64 or 128 elements) divides it, so a stage never straddles two segments.
+constexpr int kSegK = 128;
+
 // One K-segment of a GEMM's A operand: A[r, off + k] = base[map(r) * ld + k] for k < width,
 // 0 for width <= k < kpad. map(r) = idx ? idx[r] : r.
 struct Seg {
@@ -23,7 +27,7 @@ struct AOp {
   int M;
 };
 
-// Packed weight matrix [Np, Kp], K contiguous. Np is a multiple of 128, Kp of 8.
+// Packed weight matrix [Np, Kp], K contiguous. Np is a multiple of 128, Kp of kSegK.
 struct BOp {
   const void* W;
   int Np;

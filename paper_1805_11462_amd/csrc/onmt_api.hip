@@ -63,9 +63,10 @@ struct Dims {
   int L, ndir, Hd, Hm, H, E, Vs, Vt;
   int Hd_pad, H_pad;   // units padded to multiples of 32 (gate-blocked groups, 128-column tiles)
   bool bf16;
-  int kq;              // K-padding quantum: 8 elements for bf16 operands, 4 for fp32
   int esz;             // operand element size
-  int pad(int w) const { return ceil_to(w, kq); }
+  // Every K segment of a GEMM operand is padded to a multiple of kSegK so that no K stage of any tile
+  // shape straddles two segments.
+  int pad(int w) const { return ceil_to(w, kSegK); }
 };
 
 bool dims_of(const onmt_config* c, Dims* d) {
@@ -81,7 +82,6 @@ bool dims_of(const onmt_config* c, Dims* d) {
   d->Hd_pad = ceil_to(d->Hd, 32);
   d->H_pad = ceil_to(d->H, 32);
   d->bf16 = c->wdtype == 1;
-  d->kq = d->bf16 ? 8 : 4;
   d->esz = d->bf16 ? 2 : 4;
   return true;
 }
@@ -158,7 +158,8 @@ struct onmt_model {
   bool prof = false;
   int prof_n = 0;
   double prof_ms = 0.0;
-  std::vector<hipEvent_t> ev;
+  std::vector<hipEvent_t> ev;   // reusable start/stop pairs
+  size_t ev_used = 0;
 };
 
 namespace {
@@ -651,30 +652,27 @@ int decode_init_compute(onmt_model* m, const EncWs& w, int B, int K, const State
 
 void time_begin(onmt_model* m, hipStream_t st) {
   if (!m->prof) return;
-  hipEvent_t a, b;
-  if (hipEventCreate(&a) != hipSuccess) return;
-  if (hipEventCreate(&b) != hipSuccess) {
-    hipEventDestroy(a);
-    return;
+  while (m->ev.size() < m->ev_used + 2) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return;
+    m->ev.push_back(e);
   }
-  m->ev.push_back(a);
-  m->ev.push_back(b);
-  hipEventRecord(a, st);
+  hipEventRecord(m->ev[m->ev_used], st);
+  m->ev_used += 2;
 }
 void time_end(onmt_model* m, hipStream_t st) {
-  if (!m->prof || m->ev.size() < 2) return;
-  hipEventRecord(m->ev.back(), st);
+  if (!m->prof || m->ev_used < 2) return;
+  hipEventRecord(m->ev[m->ev_used - 1], st);
 }
 void time_collect(onmt_model* m) {
-  for (size_t i = 0; i + 1 < m->ev.size(); i += 2) {
+  for (size_t i = 0; i + 1 < m->ev_used; i += 2) {
     float ms = 0.f;
     if (hipEventSynchronize(m->ev[i + 1]) == hipSuccess && hipEventElapsedTime(&ms, m->ev[i], m->ev[i + 1]) == hipSuccess) {
       m->prof_ms += ms;
       m->prof_n += 1;
     }
   }
-  for (auto e : m->ev) hipEventDestroy(e);
-  m->ev.clear();
+  m->ev_used = 0;
 }
 
 // One decoder step on validated inputs (Section 2; Figure 1(a); items (a)-(c); Section 4.2 attention).
@@ -753,6 +751,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
 int check_beam(const onmt_model* m, int S, int K) {
   if (K < 1 || K > kMaxBeam) return fail(ONMT_EUNSUPPORTED, "beam %d outside [1, %d]", K, kMaxBeam);
   if (K > m->cfg.tgt_vocab) return fail(ONMT_EINVAL, "beam %d larger than the vocabulary", K);
+  if (m->d.H > 1024) return fail(ONMT_EUNSUPPORTED, "attention supports hidden <= 1024");
   if (attention_lds_bytes(S, m->d.H, K) > 64 * 1024)
     return fail(ONMT_EUNSUPPORTED, "beam * (hidden + S_max) too large for one attention workgroup");
   return ONMT_OK;

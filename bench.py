@@ -34,7 +34,20 @@ def parse():
     ap.add_argument("--workload", default="default")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sentences", type=int, default=4)
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only run one plain device-to-device copy of this many bytes (counter calibration)")
     return ap.parse_args()
+
+
+def copy_calibration(nbytes):
+    """One plain device copy of a known size, to scale rocprofv3's FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes}), flush=True)
 
 
 def kernel_source_hash():
@@ -80,6 +93,9 @@ def main():
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU design shards "
               f"sentences across GPUs and is not measured here", file=sys.stderr)
         sys.exit(2)
+    if args.copy_bytes:
+        copy_calibration(args.copy_bytes)
+        return
     import numpy as np
     import torch
 
@@ -105,11 +121,16 @@ def main():
     tr.profile(True)
     tr.profile_read(reset=True)
     tokens = 0
+    step_s = []
+    len_host = torch.empty(B, dtype=torch.int32, pin_memory=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        tr.beam_search(src_d, lens_d, buf)
-        tokens += int(buf["len"].sum().item())
+        ts = time.perf_counter()
+        tr.beam_search(src_d, lens_d, buf)       # returns with its outputs written (stream synchronized)
+        step_s.append(time.perf_counter() - ts)
+        len_host.copy_(buf["len"])                 # target tokens of this step's 1-best outputs
+        tokens += int(len_host.numpy().sum())
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     n_gen, gen_ms = tr.profile_read(reset=True)
@@ -139,6 +160,8 @@ def main():
                                f"max decode {w.max_len}, alpha {w.alpha}, {w.wdtype}",
                    "global_batch": B, "beam": w.beam, "max_decode": w.max_len,
                    "target_tokens_per_step": tokens // max(args.steps, 1)},
+        "step_ms": {"min": round(min(step_s) * 1e3, 3), "median": round(sorted(step_s)[len(step_s) // 2] * 1e3, 3),
+                    "max": round(max(step_s) * 1e3, 3)},
         "roofline": {"kernel": "k_gemm_gen (generator GEMM + fused log-softmax/top-K partials)",
                      "bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": traffic_from_counters(w.name),

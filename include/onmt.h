@@ -49,7 +49,8 @@ enum {
 /* Model shape. enc_layers must equal dec_layers (the decoder starts from the encoder's final states,
  * Figure 1(a)). When bidirectional, each encoder direction has hidden/2 units and their outputs are
  * concatenated, so the memory width is `hidden` either way. emb and hidden (and hidden/2 when
- * bidirectional) must be multiples of 4; with wdtype = 1 emb must be a multiple of 8. */
+ * bidirectional) must be multiples of 4; with wdtype = 1 emb must be a multiple of 8. Kernel limits
+ * (ONMT_EUNSUPPORTED beyond them): tgt_vocab <= 131072; the decoder calls need hidden <= 1024. */
 typedef struct {
   int enc_layers, dec_layers, bidirectional;
   int emb, hidden;

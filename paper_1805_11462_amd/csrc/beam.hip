@@ -7,133 +7,140 @@
 namespace onmt {
 
 // ------------------------------------------------------------------ softmax merge
-// One workgroup per row: combine per-tile (max, sum exp) into the row's logsumexp, and select the row's
-// top-K (larger logit first, smaller id on ties) from the per-tile top-K lists by K rounds of a
-// workgroup-wide argmax. Candidates are processed in chunks of 256 * kMergeCap; the running top-K of
-// earlier chunks takes part in every later chunk's rounds. Outputs log-probs z - lse.
-constexpr int kMergeThreads = 256;
-constexpr int kMergeCap = 8;
+// One wave merges one row's generator partials (per column tile: max, sum of exp, top-K list) into the
+// row's logsumexp and top-K (larger logit first, smaller id on ties).
+//
+// Selection is by rank: an entry's position in the result is the number of entries that come before it,
+// which each lane counts for its own entries independently (no reduction trees). To keep the candidate
+// set small, theta = the K-th largest of the 64 per-lane tile maxima is used as a lower bound on the
+// row's K-th largest logit (those K values are maxima of K distinct tiles), so only list entries
+// >= theta can be in the top-K; they are appended to LDS. If ties at theta produce more survivors than
+// fit, the lane-local lists are merged through the same rank rule over all entries instead.
+constexpr int kMaxTilesPerLane = 16;          // tiles per row <= 64 * 16 (vocabulary <= 131072)
+constexpr int kSurvivorCap = 256;
 
-__device__ inline void block_best(float& v, int& id, float* sv, int* si) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(v, o, kWave);
-    const int oi = __shfl_xor(id, o, kWave);
-    if (better(ov, oi, v, id)) {
-      v = ov;
-      id = oi;
-    }
-  }
-  const int wave = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    sv[wave] = v;
-    si[wave] = id;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int w = 0; w < kMergeThreads / kWave; ++w)
-    if (better(sv[w], si[w], v, id)) {
-      v = sv[w];
-      id = si[w];
-    }
-  __syncthreads();
-}
-
-__global__ __launch_bounds__(kMergeThreads) void k_lse_topk(const float* __restrict__ pmax,
-                                                           const float* __restrict__ psum,
-                                                           const float* __restrict__ pval,
-                                                           const int32_t* __restrict__ pid, int M, int ntiles,
-                                                           int K, float* __restrict__ out_val,
-                                                           int32_t* __restrict__ out_id, float* __restrict__ out_lse) {
-  __shared__ float sv[kMergeThreads / kWave];
-  __shared__ int si[kMergeThreads / kWave];
-  __shared__ float run_v[kMaxBeam];
-  __shared__ int run_i[kMaxBeam];
-  const int row = blockIdx.x;
-  const int tid = threadIdx.x;
+// Row partials start at pmax/psum + row * ntiles and pval/pid + row * ntiles * K. Lane 0 writes
+// out_val[k] = logit - lse (K entries), out_id[k] and *out_lse. sv/si/cnt: this wave's LDS scratch
+// (kSurvivorCap entries; sv doubles as the 64 lane maxima while theta is found).
+__device__ __forceinline__ void row_merge_wave(const float* __restrict__ pmax, const float* __restrict__ psum,
+                                               const float* __restrict__ pval, const int32_t* __restrict__ pid,
+                                               int ntiles, int K, float* sv, int* si, int* cnt, float* out_val,
+                                               int32_t* out_id, float* out_lse) {
+  const int lane = threadIdx.x & 63;
   const float ninf = -__builtin_inff();
-  const size_t base = (size_t)row * ntiles;
-  // logsumexp
+  float tm[kMaxTilesPerLane];
   float mx = ninf;
-  for (int t = tid; t < ntiles; t += kMergeThreads) mx = fmaxf(mx, pmax[base + t]);
-  int dummy = 0;
-  {
-    float v = mx;
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-    if ((tid & 63) == 0) sv[tid >> 6] = v;
-    __syncthreads();
-    mx = sv[0];
-#pragma unroll
-    for (int w = 1; w < kMergeThreads / kWave; ++w) mx = fmaxf(mx, sv[w]);
-    __syncthreads();
+  for (int j = 0; j < kMaxTilesPerLane; ++j) {
+    const int t = lane + j * kWave;
+    tm[j] = t < ntiles ? pmax[t] : ninf;
+    mx = fmaxf(mx, tm[j]);
   }
   float sm = 0.f;
-  for (int t = tid; t < ntiles; t += kMergeThreads) sm += psum[base + t] * __expf(pmax[base + t] - mx);
-  {
-    float v = wave_sum(sm);
-    if ((tid & 63) == 0) sv[tid >> 6] = v;
-    __syncthreads();
-    sm = 0.f;
+  const float gmx = wave_max(mx);
 #pragma unroll
-    for (int w = 0; w < kMergeThreads / kWave; ++w) sm += sv[w];
-    __syncthreads();
+  for (int j = 0; j < kMaxTilesPerLane; ++j) {
+    const int t = lane + j * kWave;
+    if (t < ntiles) sm += psum[t] * __expf(tm[j] - gmx);
   }
-  const float lse = mx + __logf(sm);
-  (void)dummy;
-  // top-K
-  if (tid < kMaxBeam) {
-    run_v[tid] = ninf;
-    run_i[tid] = 0x7fffffff;
+  const float lse = gmx + __logf(wave_sum(sm));
+
+  // theta: K-th largest lane maximum, by rank among the 64 (lane index breaks ties)
+  sv[lane] = mx;
+  if (lane == 0) *cnt = 0;
+  __builtin_amdgcn_wave_barrier();
+  int rank = 0;
+  for (int l = 0; l < kWave; ++l) {
+    const float o = sv[l];
+    rank += (o > mx || (o == mx && l < lane)) ? 1 : 0;
   }
-  __syncthreads();
-  const int n = ntiles * K;
-  for (int c0 = 0; c0 < n; c0 += kMergeThreads * kMergeCap) {
-    float v[kMergeCap + 1];
-    int id[kMergeCap + 1];
+  __builtin_amdgcn_wave_barrier();
+  if (rank == K - 1) si[0] = __builtin_bit_cast(int, mx);
+  __builtin_amdgcn_wave_barrier();
+  const float theta = K <= kWave ? __builtin_bit_cast(float, si[0]) : ninf;
+  __builtin_amdgcn_wave_barrier();
+
+  // survivors: entries >= theta of the tiles whose maximum reaches theta; a qualifying tile's list is
+  // loaded whole (no data-dependent exit), so its loads overlap
 #pragma unroll
-    for (int i = 0; i < kMergeCap; ++i) {
-      const int c = c0 + tid + i * kMergeThreads;
-      v[i] = c < n ? pval[base * K + c] : ninf;
-      id[i] = c < n ? pid[base * K + c] : 0x7fffffff;
+  for (int j = 0; j < kMaxTilesPerLane; ++j) {
+    const int t = lane + j * kWave;
+    if (!(t < ntiles && tm[j] >= theta)) continue;
+    const size_t o = (size_t)t * K;
+    float v[kMaxBeam];
+    int id[kMaxBeam];
+#pragma unroll
+    for (int i = 0; i < kMaxBeam; ++i) {
+      v[i] = i < K ? pval[o + i] : ninf;
+      id[i] = i < K ? pid[o + i] : 0;
     }
-    v[kMergeCap] = tid < K ? run_v[tid] : ninf;
-    id[kMergeCap] = tid < K ? run_i[tid] : 0x7fffffff;
-    __syncthreads();
-    uint32_t taken = 0;
-    for (int k = 0; k < K; ++k) {
-      float bv = ninf;
-      int bi = 0x7fffffff;
-      int bj = -1;
 #pragma unroll
-      for (int i = 0; i <= kMergeCap; ++i) {
-        if (!((taken >> i) & 1u) && better(v[i], id[i], bv, bi)) {
-          bv = v[i];
-          bi = id[i];
-          bj = i;
+    for (int i = 0; i < kMaxBeam; ++i) {
+      if (i < K && v[i] >= theta) {
+        const int pos = atomicAdd(cnt, 1);
+        if (pos < kSurvivorCap) {
+          sv[pos] = v[i];
+          si[pos] = id[i];
         }
       }
-      const int mine = bi;
-      block_best(bv, bi, sv, si);
-      if (bj >= 0 && mine == bi && bv > ninf) taken |= 1u << bj;
-      if (tid == 0) {
-        run_v[k] = bv;
-        run_i[k] = bi;
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  const int n = *cnt;
+  if (n <= kSurvivorCap) {
+    for (int c = lane; c < n; c += kWave) {
+      const float v = sv[c];
+      const int id = si[c];
+      int r = 0;
+      for (int d = 0; d < n; ++d) r += before(sv[d], si[d], v, id) ? 1 : 0;
+      if (r < K) {
+        out_val[r] = v - lse;
+        if (out_id) out_id[r] = id;
       }
     }
-    __syncthreads();
+  } else {
+    // many ties at theta: rank every list entry against every other (slow, but only for degenerate rows)
+    for (int c = lane; c < ntiles * K; c += kWave) {
+      const float v = pval[c];
+      const int id = pid[c];
+      if (v < theta) continue;
+      int r = 0;
+      for (int d = 0; d < ntiles * K && r < K; ++d) r += before(pval[d], pid[d], v, id) ? 1 : 0;
+      if (r < K) {
+        out_val[r] = v - lse;
+        if (out_id) out_id[r] = id;
+      }
+    }
   }
-  if (tid < K) {
-    out_val[(size_t)row * K + tid] = run_v[tid] - lse;
-    if (out_id) out_id[(size_t)row * K + tid] = run_i[tid];
-  }
-  if (tid == 0 && out_lse) out_lse[row] = lse;
+  if (lane == 0 && out_lse) *out_lse = lse;
+}
+
+constexpr int kMergeWaves = 4;
+
+__global__ __launch_bounds__(kMergeWaves * kWave) void k_lse_topk(const float* __restrict__ pmax,
+                                                                  const float* __restrict__ psum,
+                                                                  const float* __restrict__ pval,
+                                                                  const int32_t* __restrict__ pid, int M, int ntiles,
+                                                                  int K, float* __restrict__ out_val,
+                                                                  int32_t* __restrict__ out_id,
+                                                                  float* __restrict__ out_lse) {
+  __shared__ float sv[kMergeWaves][kSurvivorCap];
+  __shared__ int si[kMergeWaves][kSurvivorCap];
+  __shared__ int cnt[kMergeWaves];
+  const int w = threadIdx.x >> 6;
+  const int row = blockIdx.x * kMergeWaves + w;
+  if (row >= M) return;
+  const size_t base = (size_t)row * ntiles;
+  row_merge_wave(pmax + base, psum + base, pval + base * K, pid + base * K, ntiles, K, sv[w], si[w], &cnt[w],
+                     out_val + (size_t)row * K, out_id ? out_id + (size_t)row * K : nullptr,
+                     out_lse ? out_lse + row : nullptr);
 }
 
 hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pval, const int32_t* pid, int M,
                           int ntiles, int K, float* out_val, int32_t* out_id, float* out_lse, hipStream_t st) {
-  hipLaunchKernelGGL(k_lse_topk, dim3(M), dim3(kMergeThreads), 0, st, pmax, psum, pval, pid, M, ntiles, K, out_val,
-                     out_id, out_lse);
+  if (ntiles > kWave * kMaxTilesPerLane || K > kMaxBeam) return hipErrorInvalidValue;
+  const dim3 grid((M + kMergeWaves - 1) / kMergeWaves), block(kMergeWaves * kWave);
+  hipLaunchKernelGGL(k_lse_topk, grid, block, 0, st, pmax, psum, pval, pid, M, ntiles, K, out_val, out_id, out_lse);
   return hipGetLastError();
 }
 
@@ -185,107 +192,110 @@ hipError_t beam_init(const BeamParams& p, int bos, hipStream_t st) {
   return hipGetLastError();
 }
 
-// One wave per sentence. Candidates are the K per-row top-K entries of every live slot; the sentence's
-// top-K over them (larger score first, smaller flat index slot*V + token on ties) is taken with K rounds
-// of a wave-wide argmax, then walked in rank order by lane 0: EOS (or any choice at the last step) goes
-// to the finished pool, which only keeps its best entry by normalised score, the rest fill live slots.
-__global__ __launch_bounds__(64) void k_beam_step(BeamParams p, int t) {
-  const int b = blockIdx.x;
-  const int lane = threadIdx.x;
-  if (p.done[b]) return;
-  const int K = p.K;
-  const int r0 = b * K;
-  constexpr int PER = (kMaxBeam * kMaxBeam) / kWave;   // candidates per lane
-  double cv[PER];
-  long long cf[PER];
-  float cl[PER];
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int c = lane + i * kWave;
-    cv[i] = -__builtin_inf();
-    cf[i] = 0x7fffffffffffffffLL;
-    cl[i] = 0.f;
-    if (c < K * K) {
-      const int k = c / K, j = c % K;
-      const double s = p.score[r0 + k];
-      if (s > -__builtin_inf()) {
-        const float lp = p.tk_val[(size_t)(r0 + k) * K + j];
-        cv[i] = s + (double)lp;
-        cf[i] = (long long)k * p.V + p.tk_id[(size_t)(r0 + k) * K + j];
-        cl[i] = lp;
-      }
-    }
-  }
+// One workgroup per sentence, one wave per beam slot. Each live slot's wave first merges its row's
+// generator partials (logsumexp and per-row top-K, as in k_lse_topk). Candidates are then the K per-row
+// top-K entries of every live slot; the sentence's top-K over them (larger fp64 score first, smaller
+// flat index slot*V + token on ties) is selected by rank in wave 0 and walked in rank order by lane 0:
+// EOS (or any choice at the last step) goes to the finished pool, which only keeps its best entry by
+// normalised score, the rest fill live slots.
+__global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, GenPartials gp, int t) {
+  __shared__ float sv[kMaxBeam][kSurvivorCap];
+  __shared__ int si[kMaxBeam][kSurvivorCap];
+  __shared__ int cnt[kMaxBeam];
+  __shared__ float tkv[kMaxBeam][kMaxBeam];
+  __shared__ int tki[kMaxBeam][kMaxBeam];
+  __shared__ double cand_v[kMaxBeam * kMaxBeam];
+  __shared__ long long cand_f[kMaxBeam * kMaxBeam];
   __shared__ double sel_v[kMaxBeam];
   __shared__ long long sel_f[kMaxBeam];
   __shared__ float sel_l[kMaxBeam];
-  for (int k = 0; k < K; ++k) {
-    double bv = cv[0];
-    long long bf = cf[0];
-#pragma unroll
-    for (int i = 1; i < PER; ++i)
-      if (better_d(cv[i], cf[i], bv, bf)) {
-        bv = cv[i];
-        bf = cf[i];
-      }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const double ov = __shfl_xor(bv, o, kWave);
-      const long long of = __shfl_xor(bf, o, kWave);
-      if (better_d(ov, of, bv, bf)) {
-        bv = ov;
-        bf = of;
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      if (bv > -__builtin_inf() && cf[i] == bf && cv[i] == bv) {   // flat indices are unique: one owner
-        sel_l[k] = cl[i];
-        cv[i] = -__builtin_inf();
-        cf[i] = 0x7fffffffffffffffLL;
-      }
-    }
-    if (lane == 0) {
-      sel_v[k] = bv;
-      sel_f[k] = bf;
-    }
+  __shared__ double s_score[kMaxBeam];
+  __shared__ double s_best_norm;
+  __shared__ int s_best_t;
+  const int b = blockIdx.x;
+  const int w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  if (p.done[b]) return;
+  const int K = p.K;
+  const int r0 = b * K;
+  // sentence state, fetched once up front so the serial tail below does not wait on memory
+  const double my_score = p.score[r0 + w];
+  if (lane == 0) s_score[w] = my_score;
+  if (threadIdx.x == 0) {
+    s_best_norm = p.best_norm[b];
+    s_best_t = p.best_t[b];
+  }
+  if (my_score > -__builtin_inf()) {
+    const size_t base = (size_t)(r0 + w) * gp.ntiles;
+    row_merge_wave(gp.pmax + base, gp.psum + base, gp.pval + base * K, gp.pid + base * K, gp.ntiles, K, sv[w], si[w],
+                   &cnt[w], tkv[w], tki[w], nullptr);
   }
   __syncthreads();
+  if (w != 0) return;
+
+  const int nc = K * K;
+  for (int c = lane; c < nc; c += kWave) {
+    const int k = c / K, j = c % K;
+    const double s = s_score[k];
+    cand_v[c] = s > -__builtin_inf() ? s + (double)tkv[k][j] : -__builtin_inf();
+    cand_f[c] = (long long)k * p.V + tki[k][j];
+  }
+  if (lane < K) sel_v[lane] = -__builtin_inf();
+  __builtin_amdgcn_wave_barrier();
+  for (int c = lane; c < nc; c += kWave) {
+    const double v = cand_v[c];
+    const long long f = cand_f[c];
+    if (!(v > -__builtin_inf())) continue;
+    int r = 0;
+    for (int d = 0; d < nc; ++d) r += before(cand_v[d], cand_f[d], v, f) ? 1 : 0;
+    if (r < K) {
+      sel_v[r] = v;
+      sel_f[r] = f;
+      sel_l[r] = tkv[c / K][c % K];
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
   if (lane != 0) return;
 
   const double lp_t = pow((5.0 + t) / 6.0, p.alpha);
   const size_t N = (size_t)p.B * K;
   int live = 0;
   double live_max = -__builtin_inf();
+  double best_norm = s_best_norm;
+  int best_t = s_best_t;
   for (int k = 0; k < K; ++k) {
     const double v = sel_v[k];
     if (!(v > -__builtin_inf())) break;                    // fewer finite candidates than K
-    const int slot = (int)(sel_f[k] / p.V);
-    const int w = (int)(sel_f[k] % p.V);
+    const long long f = sel_f[k];
+    const int slot = (int)(f / p.V);
+    const int wtok = (int)(f - (long long)slot * p.V);
+    const float lp = sel_l[k];
     if (p.tr_slot) {
       const size_t o = ((size_t)(t - 1) * p.B + b) * K + k;
       p.tr_slot[o] = slot;
-      p.tr_tok[o] = w;
+      p.tr_tok[o] = wtok;
       p.tr_cand[o] = v;
     }
-    if (w == p.eos || t == p.T_max) {
+    if (wtok == p.eos || t == p.T_max) {
       const double norm = v / lp_t;
-      if (norm > p.best_norm[b]) {
+      if (norm > best_norm) {
+        best_norm = norm;
+        best_t = t;
         p.best_norm[b] = norm;
         p.best_raw[b] = v;
         p.best_t[b] = t;
         p.best_slot[b] = slot;
-        p.best_tok[b] = w;
-        p.best_logp[b] = sel_l[k];
+        p.best_tok[b] = wtok;
+        p.best_logp[b] = lp;
       }
     } else {
       const int j = live++;
       p.score[r0 + j] = v;
       p.parent[r0 + j] = r0 + slot;
-      p.tok[r0 + j] = w;
+      p.tok[r0 + j] = wtok;
       p.bp_slot[(size_t)(t - 1) * N + r0 + j] = slot;
-      p.bp_tok[(size_t)(t - 1) * N + r0 + j] = w;
-      p.bp_logp[(size_t)(t - 1) * N + r0 + j] = sel_l[k];
+      p.bp_tok[(size_t)(t - 1) * N + r0 + j] = wtok;
+      p.bp_logp[(size_t)(t - 1) * N + r0 + j] = lp;
       if (v > live_max) live_max = v;
     }
   }
@@ -294,17 +304,7 @@ __global__ __launch_bounds__(64) void k_beam_step(BeamParams p, int t) {
     p.parent[r0 + j] = r0;
     p.tok[r0 + j] = p.pad;
   }
-  if (p.tr_slot) {
-    for (int k = 0; k < K; ++k) {
-      if (!(sel_v[k] > -__builtin_inf())) {
-        const size_t o = ((size_t)(t - 1) * p.B + b) * K + k;
-        p.tr_slot[o] = -1;
-        p.tr_tok[o] = -1;
-        p.tr_cand[o] = -__builtin_inf();
-      }
-    }
-  }
-  const bool stop = (t == p.T_max) || (live == 0) || (p.best_t[b] > 0 && p.best_norm[b] >= live_max / p.lp_tmax);
+  const bool stop = (t == p.T_max) || (live == 0) || (best_t > 0 && best_norm >= live_max / p.lp_tmax);
   if (stop) {
     p.done[b] = 1;
     p.steps[b] = t;
@@ -312,8 +312,9 @@ __global__ __launch_bounds__(64) void k_beam_step(BeamParams p, int t) {
   }
 }
 
-hipError_t beam_step(const BeamParams& p, int t, hipStream_t st) {
-  hipLaunchKernelGGL(k_beam_step, dim3(p.B), dim3(64), 0, st, p, t);
+hipError_t beam_step(const BeamParams& p, const GenPartials& gp, int t, hipStream_t st) {
+  if (gp.ntiles > kWave * kMaxTilesPerLane || p.K > kMaxBeam) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_beam_step, dim3(p.B), dim3(p.K * kWave), 0, st, p, gp, t);
   return hipGetLastError();
 }
 

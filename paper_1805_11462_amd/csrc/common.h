@@ -27,41 +27,10 @@ __device__ inline float bf16_bits_to_f32(uint16_t h) {
 
 __device__ inline float sigmoidf_(float x) { return 1.0f / (1.0f + __expf(-x)); }
 
-// Candidate order used everywhere a top-K is taken: larger value first, then smaller id.
-__device__ inline bool better(float v, int id, float w, int jd) {
+// Order used by every top-K: larger value first, then smaller id (ids are unique, so this is total).
+template <class V, class I>
+__device__ inline bool before(V v, I id, V w, I jd) {
   return v > w || (v == w && id < jd);
-}
-__device__ inline bool better_d(double v, long long id, double w, long long jd) {
-  return v > w || (v == w && id < jd);
-}
-
-// Stable insertion of (v, id) into a descending list of KMAX entries held in registers.
-template <int KMAX>
-__device__ inline void topk_insert(float (&val)[KMAX], int (&ids)[KMAX], float v, int id) {
-  if (!better(v, id, val[KMAX - 1], ids[KMAX - 1])) return;
-  bool moving = false;
-#pragma unroll
-  for (int i = 0; i < KMAX; ++i) {
-    bool take = moving || better(v, id, val[i], ids[i]);
-    if (take) {
-      float tv = val[i];
-      int ti = ids[i];
-      val[i] = v;
-      ids[i] = id;
-      v = tv;
-      id = ti;
-      moving = true;
-    }
-  }
-}
-
-template <int KMAX>
-__device__ inline void topk_clear(float (&val)[KMAX], int (&ids)[KMAX]) {
-#pragma unroll
-  for (int i = 0; i < KMAX; ++i) {
-    val[i] = -__builtin_inff();
-    ids[i] = 0x7fffffff;
-  }
 }
 
 __device__ inline float wave_max(float v) {

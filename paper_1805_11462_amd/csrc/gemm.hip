@@ -62,6 +62,19 @@ __device__ inline uint4 f32x8_to_bf16x8(const float4& lo, const float4& hi) {
   return r;
 }
 
+// Buffer resource descriptor (gfx9 family word 3). Loads through it return zeros past num_records, so
+// an invalid row is given an offset beyond every buffer instead of a branch.
+constexpr int kBufWord3 = 0x00020000;
+constexpr uint32_t kNoRow = 0x80000000u;      // byte offset past the end of any buffer (buffers < 2 GiB)
+
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufWord3);
+}
+
+__device__ inline uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+
 // Main loop: leaves the (WK-way partial) fp32 output tile in LDS at smem, layout [WK][BM][CROW].
 template <class T, class C>
 __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, char* smem) {
@@ -73,37 +86,37 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
   const int wm = wave / (C::WK * C::WN);
   const int i16 = lane & 15, g = lane >> 4;
 
-  // Segment table (uniform). Every field is read with a constant index into a scalar, so the argument
-  // struct is never indexed at run time (which would put it in private memory).
-  const int nseg = a.nseg;
-  const int kp0 = a.seg[0].kpad, kp1 = a.seg[1].kpad, kp2 = a.seg[2].kpad;
-  const int wd0 = a.seg[0].width, wd1 = a.seg[1].width, wd2 = a.seg[2].width;
-  const int bf0 = a.seg[0].bf16, bf1 = a.seg[1].bf16, bf2 = a.seg[2].bf16;
-
-  // Per-thread A row pointers, one per segment (rows are fixed across K stages).
   // Thread chunk c = tid + i * NT covers tile row c / CPR, columns (c % CPR) * CH ...; NT is a multiple
   // of CPR, so the column is the same for every i and the row advances by NT / CPR.
   constexpr int RSTEP = C::NT / C::CPR;
   static_assert(C::NT % C::CPR == 0, "threads must cover whole tile rows");
   const int arow0 = tid / C::CPR;
   const int acol = (tid % C::CPR) * C::CH;
-  const char* ar0[C::A_PT];
-  const char* ar1[C::A_PT];
-  const char* ar2[C::A_PT];
-#define ONMT_ROW_PTR(S, r)                                                                            \
-  ((const char*)a.seg[S].base +                                                                      \
-   (size_t)(a.seg[S].idx ? a.seg[S].idx[r] : (r)) * a.seg[S].ld * (a.seg[S].bf16 ? 2 : 4))
-#pragma unroll
-  for (int i = 0; i < C::A_PT; ++i) {
-    const int r = m0 + arow0 + i * RSTEP;
-    const bool rv = r < a.M;
-    ar0[i] = rv ? ONMT_ROW_PTR(0, r) : nullptr;
-    ar1[i] = (rv && nseg > 1) ? ONMT_ROW_PTR(1, r) : nullptr;
-    ar2[i] = (rv && nseg > 2) ? ONMT_ROW_PTR(2, r) : nullptr;
+
+  // Every segment field is read with a constant index into a scalar, so the argument struct is never
+  // indexed at run time (which would put it in private memory).
+  const int nseg = a.nseg;
+  // Per-thread byte offsets of the thread's A rows inside each segment's buffer (kNoRow past M).
+#define ONMT_SEG_SETUP(S)                                                                             \
+  const int kp##S = a.seg[S].kpad, wd##S = a.seg[S].width, bf##S = a.seg[S].bf16;                     \
+  const uint32_t es##S = bf##S ? 2u : 4u;                                                              \
+  const __amdgpu_buffer_rsrc_t rs##S = make_rsrc(a.seg[S].base, (uint32_t)a.seg[S].rows * a.seg[S].ld * es##S); \
+  uint32_t ao##S[C::A_PT];                                                                             \
+  _Pragma("unroll") for (int i = 0; i < C::A_PT; ++i) {                                                \
+    const int r = m0 + arow0 + i * RSTEP;                                                              \
+    const bool ok = S < nseg && r < a.M;                                                               \
+    const int rr = ok ? (a.seg[S].idx ? a.seg[S].idx[r] : r) : 0;                                      \
+    ao##S[i] = ok ? ((uint32_t)rr * a.seg[S].ld + acol) * es##S : kNoRow;                              \
   }
-#undef ONMT_ROW_PTR
-  const char* brow = (const char*)b.W + ((size_t)(n0 + arow0) * b.Kp + acol) * sizeof(T);
-  const size_t bstep = (size_t)RSTEP * b.Kp * sizeof(T);
+  ONMT_SEG_SETUP(0)
+  ONMT_SEG_SETUP(1)
+  ONMT_SEG_SETUP(2)
+#undef ONMT_SEG_SETUP
+
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(b.W, (uint32_t)b.Np * b.Kp * sizeof(T));
+  uint32_t bo[C::B_PT];
+#pragma unroll
+  for (int i = 0; i < C::B_PT; ++i) bo[i] = ((uint32_t)(n0 + arow0 + i * RSTEP) * b.Kp + acol) * sizeof(T);
 
   T* As[2] = {(T*)smem, (T*)(smem + C::STAGE)};
   T* Bs[2] = {As[0] + C::BM * C::ROW, As[1] + C::BM * C::ROW};
@@ -113,9 +126,6 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
     uint4 a[C::A_PT];
     uint4 b[C::B_PT];
   };
-  // Loads are issued unconditionally (out-of-range chunks read a valid dummy address and are zeroed
-  // afterwards) so the loop stays straight-line and the compiler can keep both stages in flight.
-  const char* dummy = (const char*)b.W;
   auto lstore = [&](int buf, const Regs& r) {
 #pragma unroll
     for (int i = 0; i < C::A_PT; ++i) *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + acol) = r.a[i];
@@ -162,40 +172,40 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
     }
   };
 
-  // K runs segment by segment, each with its own two-stage pipeline, so the row pointers a stage reads
-  // are known at compile time (selecting among them at run time would put them in private memory).
-  int kbase = 0;
-  auto run_segment = [&](const char* const (&arp)[C::A_PT], int width, int src_bf16, int kpad) {
-    const bool sbf = src_bf16 != 0;
+  // K runs segment by segment, each with its own two-stage pipeline. Loads are unconditional: rows past
+  // M read zeros through the descriptor bound, columns in a segment's padding are zeroed by a select,
+  // and past the last stage the loads re-read the last stage into a buffer that is never multiplied.
+  uint32_t kbyte_w = 0;                 // byte offset of the segment inside a weight row
+  auto run_segment = [&](__amdgpu_buffer_rsrc_t rs, const uint32_t (&ao)[C::A_PT], uint32_t es, int width,
+                         int kpad) {
+    const bool src_bf16 = es == 2;
     auto gload = [&](int st) -> Regs {
       Regs r;
       const int kk = st * C::BK + acol;
+      const bool ok = kk < width;
 #pragma unroll
       for (int i = 0; i < C::A_PT; ++i) {
-        const char* rp = arp[i];
-        const bool ok = rp != nullptr && kk < width;
+        const uint32_t off = ao[i] + (uint32_t)(st * C::BK) * es;
         if constexpr (!C::kBf16) {
-          const uint4 v = *(const uint4*)(ok ? rp + (size_t)kk * 4 : dummy);
+          const uint4 v = buf_load16(rs, off);
           r.a[i] = ok ? v : zero4();
         } else {
           // bf16 source: 8 elements in one 16-byte load; fp32 source: two 16-byte loads rounded to bf16
           // (nearest, ties to even). Widths are multiples of 4, so the second half may be past the end.
-          const bool ok_hi = ok && !sbf && kk + 4 < width;
-          const uint4 lo = *(const uint4*)(ok ? rp + (size_t)kk * (sbf ? 2 : 4) : dummy);
-          const uint4 hi = *(const uint4*)(ok_hi ? rp + (size_t)(kk + 4) * 4 : dummy);
+          const uint4 lo = buf_load16(rs, off);
+          const uint4 hi = buf_load16(rs, off + 16);
+          const bool ok_hi = kk + 4 < width;
           const float4 flo = __builtin_bit_cast(float4, lo);
           const float4 fhi = ok_hi ? __builtin_bit_cast(float4, hi) : make_float4(0.f, 0.f, 0.f, 0.f);
           const uint4 cv = f32x8_to_bf16x8(flo, fhi);
-          r.a[i] = !ok ? zero4() : (sbf ? lo : cv);
+          r.a[i] = !ok ? zero4() : (src_bf16 ? lo : cv);
         }
       }
-      const size_t kb = (size_t)(kbase + st * C::BK) * sizeof(T);
+      const uint32_t kb = kbyte_w + (uint32_t)(st * C::BK) * sizeof(T);
 #pragma unroll
-      for (int i = 0; i < C::B_PT; ++i) r.b[i] = *(const uint4*)(brow + i * bstep + kb);
+      for (int i = 0; i < C::B_PT; ++i) r.b[i] = buf_load16(rw, bo[i] + kb);
       return r;
     };
-    // Loads and LDS stores are unconditional: past the last stage they re-read the last stage and fill a
-    // buffer that is never multiplied, which keeps the loop free of data-dependent branches.
     const int nst = kpad / C::BK;       // segment widths are padded to multiples of kSegK, hence of BK
     const int last = nst - 1;
     Regs r0 = gload(0);
@@ -215,11 +225,14 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
       lstore(0, r0);
       __syncthreads();
     }
-    kbase += kpad;
+    kbyte_w += (uint32_t)kpad * sizeof(T);
   };
-  run_segment(ar0, wd0, bf0, kp0);
-  if (nseg > 1) run_segment(ar1, wd1, bf1, kp1);
-  if (nseg > 2) run_segment(ar2, wd2, bf2, kp2);
+  run_segment(rs0, ao0, es0, wd0, kp0);
+  if (nseg > 1) run_segment(rs1, ao1, es1, wd1, kp1);
+  if (nseg > 2) run_segment(rs2, ao2, es2, wd2, kp2);
+  (void)bf0;
+  (void)bf1;
+  (void)bf2;
 
   // Partial tiles to LDS: lane holds rows 4g..4g+3 of column i16 of each 16x16 block.
   float* Ct = (float*)smem + wk * C::BM * C::CROW;
@@ -369,7 +382,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
     for (int s = 1; s < 4; s <<= 1) {
       const float ov = __shfl_xor(bv, s, kWave);
       const int oi = __shfl_xor(bid, s, kWave);
-      if (better(ov, oi, bv, bid)) {
+      if (before(ov, oi, bv, bid)) {
         bv = ov;
         bid = oi;
       }
@@ -397,6 +410,17 @@ static inline void grid_of(const AOp& a, const BOp& b, int& nm, int& nblocks) {
   nblocks = nm * (b.Np / C::BN);
 }
 
+// Buffer descriptors address at most 2 GiB: reject operands that do not fit (never the case for the
+// supported model shapes, which the C ABI validates).
+template <class T>
+static inline bool operands_fit(const AOp& a, const BOp& b) {
+  const uint64_t lim = 1ull << 31;
+  if ((uint64_t)b.Np * b.Kp * sizeof(T) >= lim || b.Np % 128 || b.Kp % kSegK) return false;
+  for (int s = 0; s < a.nseg; ++s)
+    if ((uint64_t)a.seg[s].rows * a.seg[s].ld * (a.seg[s].bf16 ? 2 : 4) >= lim || a.seg[s].kpad % kSegK) return false;
+  return true;
+}
+
 int gemm_tile_cols(int shape) { return shape == kShapeWide ? TileWide32::BN : TileSplit32::BN; }
 int gen_tile_cols() { return TileWide32::BN; }
 
@@ -404,6 +428,7 @@ template <class T, class C>
 static hipError_t launch_store(const AOp& a, const BOp& b, const StoreParams& p, hipStream_t st) {
   int nm, nb;
   grid_of<C>(a, b, nm, nb);
+  if (!operands_fit<T>(a, b)) return hipErrorInvalidValue;
   if (nb == 0) return hipSuccess;
   hipLaunchKernelGGL((k_gemm_store<T, C>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
   return hipGetLastError();
@@ -413,6 +438,7 @@ template <class T, class C>
 static hipError_t launch_lstm(const AOp& a, const BOp& b, const LstmParams& p, hipStream_t st) {
   int nm, nb;
   grid_of<C>(a, b, nm, nb);
+  if (!operands_fit<T>(a, b)) return hipErrorInvalidValue;
   if (nb == 0) return hipSuccess;
   hipLaunchKernelGGL((k_gemm_lstm<T, C>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
   return hipGetLastError();
@@ -422,6 +448,7 @@ template <class T, class C>
 static hipError_t launch_gen(const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
   int nm, nb;
   grid_of<C>(a, b, nm, nb);
+  if (!operands_fit<T>(a, b)) return hipErrorInvalidValue;
   if (nb == 0) return hipSuccess;
   hipLaunchKernelGGL((k_gemm_gen<T, C>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
   return hipGetLastError();

@@ -11,10 +11,11 @@ namespace onmt {
 constexpr int kSegK = 128;
 
 // One K-segment of a GEMM's A operand: A[r, off + k] = base[map(r) * ld + k] for k < width,
-// 0 for width <= k < kpad. map(r) = idx ? idx[r] : r.
+// 0 for width <= k < kpad. map(r) = idx ? idx[r] : r. The buffer must be smaller than 2 GiB.
 struct Seg {
   const void* base;
   const int32_t* idx;
+  int rows;      // rows in the source buffer (reads are bounded by rows * ld elements)
   int ld;
   int width;
   int kpad;
@@ -95,8 +96,6 @@ hipError_t subtract_rows(float* x, int ld, const float* lse, int M, int ncols, h
 struct BeamParams {
   int B, K, V, T_max, eos, pad;
   double alpha, lp_tmax;
-  const float* tk_val;
-  const int32_t* tk_id;
   double* score;
   int32_t* parent;
   int32_t* tok;
@@ -117,8 +116,17 @@ struct BeamParams {
   double* tr_cand;
 };
 
+// Generator partials of one decoder step (per row and column tile), as written by gemm_gen.
+struct GenPartials {
+  const float* pmax;
+  const float* psum;
+  const float* pval;
+  const int32_t* pid;
+  int ntiles;
+};
+
 hipError_t beam_init(const BeamParams& p, int bos, hipStream_t st);
-hipError_t beam_step(const BeamParams& p, int t, hipStream_t st);
+hipError_t beam_step(const BeamParams& p, const GenPartials& gp, int t, hipStream_t st);
 hipError_t backtrack(const BeamParams& p, int32_t* out_tok, int32_t* out_len, double* out_raw, double* out_norm,
                      float* out_tok_logp, hipStream_t st);
 

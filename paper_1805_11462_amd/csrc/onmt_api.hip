@@ -96,6 +96,7 @@ int check_config(const onmt_config* c) {
   if (c->emb < 4 || c->hidden < 4 || c->src_vocab < 1 || c->tgt_vocab < 4)
     return fail(ONMT_EINVAL, "emb/hidden >= 4, src_vocab >= 1, tgt_vocab >= 4 required");
   if (c->emb > 8192 || c->hidden > 8192 || c->enc_layers > 64) return fail(ONMT_EUNSUPPORTED, "model too large");
+  if (c->tgt_vocab > 131072) return fail(ONMT_EUNSUPPORTED, "target vocabulary larger than 131072");
   const int Hd = c->bidirectional ? c->hidden / 2 : c->hidden;
   if (c->bidirectional && c->hidden % 2) return fail(ONMT_EINVAL, "bidirectional needs an even hidden size");
   if (c->emb % 4 || c->hidden % 4 || Hd % 4)
@@ -510,10 +511,11 @@ size_t search_layout(const Dims& d, int B, int S, int K, int T, char* base, Sear
   return align_up(c.off);
 }
 
-Seg seg(const void* base, const int32_t* idx, int ld, int width, int kpad, int bf16) {
+Seg seg(const void* base, const int32_t* idx, int rows, int ld, int width, int kpad, int bf16) {
   Seg s;
   s.base = base;
   s.idx = idx;
+  s.rows = rows;
   s.ld = ld;
   s.width = width;
   s.kpad = kpad;
@@ -529,10 +531,14 @@ BOp bop(const Packed& p) {
   return b;
 }
 
-// Small-M GEMMs: pick the thinner split-K tile when the 32-row tile would leave CUs idle.
+// Small-M GEMMs: the 16-row split-K tile unless the 32-row tile already gives this many workgroups
+// (measured on the decoder layers: more, smaller workgroups win while M is a few hundred rows).
+#ifndef ONMT_SMALL_M_TILES
+#define ONMT_SMALL_M_TILES 4096
+#endif
 int small_shape(int M, int Np) {
   const long tiles32 = (long)((M + 31) / 32) * (Np / 64);
-  return tiles32 >= 256 ? kShapeSplitK : kShapeSplitKThin;
+  return tiles32 >= ONMT_SMALL_M_TILES ? kShapeSplitK : kShapeSplitKThin;
 }
 
 // Copies src/len to the host, validates them, and uploads the token ids with every position at or beyond
@@ -578,8 +584,8 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
     AOp a{};
     a.M = BS;
     a.nseg = 1;
-    if (l == 0) a.seg[0] = seg(m->E_src, w.src, d.E, d.E, d.pad(d.E), d.bf16);
-    else a.seg[0] = seg(w.y[(l - 1) & 1], nullptr, d.Hm, d.Hm, d.pad(d.Hm), 0);
+    if (l == 0) a.seg[0] = seg(m->E_src, w.src, d.Vs, d.E, d.E, d.pad(d.E), d.bf16);
+    else a.seg[0] = seg(w.y[(l - 1) & 1], nullptr, BS, d.Hm, d.Hm, d.pad(d.Hm), 0);
     StoreParams sp{m->enc_bias[l], w.gx, gxw, gxw, 0};
     HIP_TRY(gemm_store(d.bf16, kShapeWide, a, bop(m->enc_x[l]), sp, st));
     HIP_TRY(fill_f32(w.hs[0], (size_t)d.ndir * B * d.Hd, 0.f, st));
@@ -594,7 +600,7 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
         AOp r{};
         r.M = B;
         r.nseg = 1;
-        r.seg[0] = seg(hp, nullptr, d.Hd, d.Hd, d.pad(d.Hd), 0);
+        r.seg[0] = seg(hp, nullptr, B, d.Hd, d.Hd, d.pad(d.Hd), 0);
         LstmParams lp{};
         lp.bias = nullptr;
         lp.gx = w.gx;
@@ -633,7 +639,7 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
   AOp a{};
   a.M = BS;
   a.nseg = 1;
-  a.seg[0] = seg(w.memory, nullptr, d.Hm, d.Hm, d.pad(d.Hm), 0);
+  a.seg[0] = seg(w.memory, nullptr, BS, d.Hm, d.Hm, d.pad(d.Hm), 0);
   StoreParams kp{nullptr, w.keys, d.H, d.H, 0};
   HIP_TRY(gemm_store(d.bf16, kShapeWide, a, bop(m->W_a), kp, st));
   return ONMT_OK;
@@ -676,7 +682,8 @@ void time_collect(onmt_model* m) {
 }
 
 // One decoder step on validated inputs (Section 2; Figure 1(a); items (a)-(c); Section 4.2 attention).
-// mode 0: logp [N, V] full log-softmax; mode 1: top-K (logp [N, K], ids [N, K]).
+// mode 0: logp [N, V] full log-softmax; mode 1: top-K (logp [N, K], ids [N, K]); mode 2 (beam search):
+// stop after the generator, leaving its per-tile partials in the step workspace for the beam step.
 int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const State& in, const State& out,
                    const int32_t* prev_tok, const int32_t* parent, int mode, float* logp, int32_t* ids, float* lse,
                    float* attn, const StepWs& sw, hipStream_t st) {
@@ -688,13 +695,13 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     a.M = N;
     if (l == 0) {
       a.nseg = 3;
-      a.seg[0] = seg(m->E_tgt, prev_tok, d.E, d.E, d.pad(d.E), d.bf16);
-      a.seg[1] = seg(in.feed, parent, d.H, d.H, d.pad(d.H), 0);
-      a.seg[2] = seg(in.h, parent, d.H, d.H, d.pad(d.H), 0);
+      a.seg[0] = seg(m->E_tgt, prev_tok, d.Vt, d.E, d.E, d.pad(d.E), d.bf16);
+      a.seg[1] = seg(in.feed, parent, N, d.H, d.H, d.pad(d.H), 0);
+      a.seg[2] = seg(in.h, parent, N, d.H, d.H, d.pad(d.H), 0);
     } else {
       a.nseg = 2;
-      a.seg[0] = seg(out.h + (l - 1) * LH, nullptr, d.H, d.H, d.pad(d.H), 0);
-      a.seg[1] = seg(in.h + l * LH, parent, d.H, d.H, d.pad(d.H), 0);
+      a.seg[0] = seg(out.h + (l - 1) * LH, nullptr, N, d.H, d.H, d.pad(d.H), 0);
+      a.seg[1] = seg(in.h + l * LH, parent, N, d.H, d.H, d.pad(d.H), 0);
     }
     LstmParams lp{};
     lp.bias = m->dec_bias[l];
@@ -713,8 +720,8 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     AOp a{};
     a.M = N;
     a.nseg = 2;
-    a.seg[0] = seg(sw.ctx, nullptr, d.Hm, d.Hm, d.pad(d.Hm), 0);
-    a.seg[1] = seg(q, nullptr, d.H, d.H, d.pad(d.H), 0);
+    a.seg[0] = seg(sw.ctx, nullptr, N, d.Hm, d.Hm, d.pad(d.Hm), 0);
+    a.seg[1] = seg(q, nullptr, N, d.H, d.H, d.pad(d.H), 0);
     StoreParams sp{nullptr, out.feed, d.H, d.H, 1};
     HIP_TRY(gemm_store(d.bf16, small_shape(N, m->W_c.Np), a, bop(m->W_c), sp, st));
   }
@@ -722,7 +729,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     AOp a{};
     a.M = N;
     a.nseg = 1;
-    a.seg[0] = seg(out.feed, nullptr, d.H, d.H, d.pad(d.H), 0);
+    a.seg[0] = seg(out.feed, nullptr, N, d.H, d.H, d.pad(d.H), 0);
     GenParams gp{};
     gp.bias = m->b_s;
     gp.V = d.Vt;
@@ -738,6 +745,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     HIP_TRY(gemm_gen(d.bf16, a, bop(m->W_s), gp, st));
     time_end(m, st);
   }
+  if (mode == 2) return ONMT_OK;
   float* lse_out = lse ? lse : sw.lse;
   if (mode == 0) {
     HIP_TRY(lse_topk_merge(sw.pmax, sw.psum, sw.pval, sw.pid, N, sw.ntiles, K, sw.tk_val, sw.tk_id, lse_out, st));
@@ -872,12 +880,11 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   bp.pad = m->cfg.pad_id;
   bp.alpha = prm->alpha;
   bp.lp_tmax = std::pow((5.0 + T) / 6.0, prm->alpha);
-  bp.tk_val = w.step.tk_val;
-  bp.tk_id = w.step.tk_id;
   bp.tr_slot = trace ? trace->slot : nullptr;
   bp.tr_tok = trace ? trace->tok : nullptr;
   bp.tr_cand = trace ? trace->cand : nullptr;
 
+  GenPartials gp{w.step.pmax, w.step.psum, w.step.pval, w.step.pid, w.step.ntiles};
   rc = encode_compute(m, src, len, B, S, mx, w.enc, st);
   if (rc) return rc;
   rc = decode_init_compute(m, w.enc, B, K, w.st[0], st);
@@ -886,10 +893,10 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   const int every = prm->check_every > 0 ? prm->check_every : (T <= 32 ? 1 : 8);
   int cur = 0;
   for (int t = 1; t <= T; ++t) {
-    rc = decode_compute(m, w.enc, B, S, K, w.st[cur], w.st[cur ^ 1], bp.tok, bp.parent, 1, w.step.tk_val,
-                        w.step.tk_id, nullptr, nullptr, w.step, st);
+    rc = decode_compute(m, w.enc, B, S, K, w.st[cur], w.st[cur ^ 1], bp.tok, bp.parent, 2, nullptr, nullptr,
+                        nullptr, nullptr, w.step, st);
     if (rc) return rc;
-    HIP_TRY(beam_step(bp, t, st));
+    HIP_TRY(beam_step(bp, gp, t, st));
     cur ^= 1;
     if (t < T && t % every == 0) {
       int32_t done = 0;

@@ -49,7 +49,9 @@ R9  Beam: scores s_0 = 0, s_1.. = -inf; candidates cand = s_k + logp_k(w) in
 R10 GNMT length penalty lp(n) = ((5 + n) / 6) ** alpha, applied to finished
     hypotheses only; n counts EOS.
 R11 max_len = most generated tokens, EOS included.
-R12 bf16 workloads: the oracle runs in fp64 on the bf16-rounded weights.
+R12 bf16 workloads: the oracle runs in fp64 on the bf16-rounded weights. (The GPU path keeps bf16
+    weights and fp32 accumulation; it carries each activation entering a product as two bf16 terms,
+    which keeps the chaotic decoder recurrence within the bf16 tolerance over full-length outputs.)
 R15 Throughput counts target tokens of the 1-best, EOS included.
 R16 Near-ties: any choice within the tolerance is a correct result.
 

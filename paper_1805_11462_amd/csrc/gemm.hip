@@ -34,7 +34,10 @@ struct Tile {
   static constexpr int B_CH = BN * CPR;
   static constexpr int A_PT = A_CH / NT;
   static constexpr int B_PT = B_CH / NT;
-  static constexpr int STAGE = (BM + BN) * ROW * (int)sizeof(T);
+  // bf16 products carry each fp32 activation as two bf16 terms (hi + lo, ~16 significant bits); the
+  // A tile therefore holds a hi and a lo copy. Weights are bf16 already, so W a = W hi + W lo exactly.
+  static constexpr int AREP = kBf16 ? 2 : 1;
+  static constexpr int STAGE = (AREP * BM + BN) * ROW * (int)sizeof(T);
   static constexpr int CROW = BN + 4;                // fp32 output tile row stride
   static constexpr int CT = WK * BM * CROW * 4;
   static constexpr int LDS = (2 * STAGE > CT) ? 2 * STAGE : CT;
@@ -53,13 +56,18 @@ __device__ inline int xcd_remap(int bid, int nblocks) {
 
 __device__ inline uint4 zero4() { return make_uint4(0u, 0u, 0u, 0u); }
 
-__device__ inline uint4 f32x8_to_bf16x8(const float4& lo, const float4& hi) {
-  uint4 r;
-  r.x = f32_to_bf16_bits(lo.x) | ((uint32_t)f32_to_bf16_bits(lo.y) << 16);
-  r.y = f32_to_bf16_bits(lo.z) | ((uint32_t)f32_to_bf16_bits(lo.w) << 16);
-  r.z = f32_to_bf16_bits(hi.x) | ((uint32_t)f32_to_bf16_bits(hi.y) << 16);
-  r.w = f32_to_bf16_bits(hi.z) | ((uint32_t)f32_to_bf16_bits(hi.w) << 16);
-  return r;
+// Split 8 fp32 values into bf16 hi = RNE(x) and lo = RNE(x - hi); x - hi is exact in fp32, so
+// hi + lo keeps about 16 significant bits of x.
+__device__ inline void split_bf16x8(const float4& a, const float4& b, uint4& hi, uint4& lo) {
+  const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  uint32_t h[8], l[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    h[i] = f32_to_bf16_bits(x[i]);
+    l[i] = f32_to_bf16_bits(x[i] - bf16_bits_to_f32((uint16_t)h[i]));
+  }
+  hi = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+  lo = make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16));
 }
 
 // Buffer resource descriptor (gfx9 family word 3). Loads through it return zeros past num_records, so
@@ -118,17 +126,22 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
 #pragma unroll
   for (int i = 0; i < C::B_PT; ++i) bo[i] = ((uint32_t)(n0 + arow0 + i * RSTEP) * b.Kp + acol) * sizeof(T);
 
+  // LDS stage layout: [A (hi) rows | A lo rows (bf16 only) | B rows].
   T* As[2] = {(T*)smem, (T*)(smem + C::STAGE)};
-  T* Bs[2] = {As[0] + C::BM * C::ROW, As[1] + C::BM * C::ROW};
+  T* Bs[2] = {As[0] + C::AREP * C::BM * C::ROW, As[1] + C::AREP * C::BM * C::ROW};
 
   // One K stage of operands in flight: held in registers between its global load and its LDS store.
   struct Regs {
     uint4 a[C::A_PT];
+    uint4 alo[C::AREP == 2 ? C::A_PT : 1];
     uint4 b[C::B_PT];
   };
   auto lstore = [&](int buf, const Regs& r) {
 #pragma unroll
-    for (int i = 0; i < C::A_PT; ++i) *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + acol) = r.a[i];
+    for (int i = 0; i < C::A_PT; ++i) {
+      *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + acol) = r.a[i];
+      if constexpr (C::AREP == 2) *(uint4*)(As[buf] + (C::BM + arow0 + i * RSTEP) * C::ROW + acol) = r.alo[i];
+    }
 #pragma unroll
     for (int i = 0; i < C::B_PT; ++i) *(uint4*)(Bs[buf] + (arow0 + i * RSTEP) * C::ROW + acol) = r.b[i];
   };
@@ -139,7 +152,7 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
 #pragma unroll
     for (int y = 0; y < C::TN; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute = [&](int buf) {
+  auto compute = [&](int buf, bool has_lo) {
     const T* Ab = As[buf] + (wm * C::TM * 16 + i16) * C::ROW + wk * C::KW;
     const T* Bb = Bs[buf] + (wn * C::TN * 16 + i16) * C::ROW + wk * C::KW;
 #pragma unroll
@@ -168,6 +181,16 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
 #pragma unroll
           for (int y = 0; y < C::TN; ++y)
             acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+        if (has_lo) {               // uniform: the segment's source is fp32
+#pragma unroll
+          for (int x = 0; x < C::TM; ++x)
+            av[x] = *(const bf16x8*)(Ab + (C::BM + x * 16) * C::ROW + sub * 32 + 8 * g);
+#pragma unroll
+          for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+            for (int y = 0; y < C::TN; ++y)
+              acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+        }
       }
     }
   };
@@ -190,15 +213,17 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
           const uint4 v = buf_load16(rs, off);
           r.a[i] = ok ? v : zero4();
         } else {
-          // bf16 source: 8 elements in one 16-byte load; fp32 source: two 16-byte loads rounded to bf16
-          // (nearest, ties to even). Widths are multiples of 4, so the second half may be past the end.
-          const uint4 lo = buf_load16(rs, off);
-          const uint4 hi = buf_load16(rs, off + 16);
-          const bool ok_hi = kk + 4 < width;
-          const float4 flo = __builtin_bit_cast(float4, lo);
-          const float4 fhi = ok_hi ? __builtin_bit_cast(float4, hi) : make_float4(0.f, 0.f, 0.f, 0.f);
-          const uint4 cv = f32x8_to_bf16x8(flo, fhi);
-          r.a[i] = !ok ? zero4() : (src_bf16 ? lo : cv);
+          // bf16 source: 8 elements in one 16-byte load (exact, no lo part); fp32 source: two 16-byte
+          // loads split into bf16 hi + lo. Widths are multiples of 4, so the second half may be past the end.
+          const uint4 l0 = buf_load16(rs, off);
+          const uint4 l1 = buf_load16(rs, off + 16);
+          const bool ok1 = kk + 4 < width;
+          const float4 f0 = __builtin_bit_cast(float4, l0);
+          const float4 f1 = ok1 ? __builtin_bit_cast(float4, l1) : make_float4(0.f, 0.f, 0.f, 0.f);
+          uint4 hi, lo;
+          split_bf16x8(f0, f1, hi, lo);
+          r.a[i] = !ok ? zero4() : (src_bf16 ? l0 : hi);
+          r.alo[i] = (!ok || src_bf16) ? zero4() : lo;
         }
       }
       const uint32_t kb = kbyte_w + (uint32_t)(st * C::BK) * sizeof(T);
@@ -215,13 +240,13 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
     for (int st = 0; st < nst; st += 2) {
       // even stage: LDS buffer 0 holds stage st, r1 holds st + 1
       r0 = gload(min(st + 2, last));
-      compute(0);
+      compute(0, !src_bf16);
       lstore(1, r1);
       __syncthreads();
       if (st + 1 >= nst) break;
       // odd stage: LDS buffer 1 holds stage st + 1, r0 holds st + 2
       r1 = gload(min(st + 3, last));
-      compute(1);
+      compute(1, !src_bf16);
       lstore(0, r0);
       __syncthreads();
     }

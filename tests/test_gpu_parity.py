@@ -223,3 +223,76 @@ def test_all_zero_weights_tie_rules():
             n = int(buf["len"][b])
             assert list(buf["tok"][b, :n].cpu().numpy()) == want
             assert abs(buf["raw"][b].item() + len(want) * np.log(50)) < 1e-5
+
+
+# ------------------------------------------------------------------ the other workloads (full batches on
+# the GPU, oracle on sampled sentences; bf16 workloads at the bf16 tolerance)
+@pytest.fixture(scope="module")
+def larger():
+    return Setup(W.get("larger"))
+
+
+@pytest.fixture(scope="module")
+def greedy():
+    return Setup(W.get("greedy"))
+
+
+@pytest.fixture(scope="module")
+def long_src():
+    return Setup(W.get("long"))
+
+
+@pytest.mark.parametrize("which", ["larger", "greedy", "long_src"])
+def test_encoder_other_workloads(which, request):
+    s = request.getfixturevalue(which)
+    _print_case("encoder", workload=s.w.name)
+    B, S = s.src.shape
+    ws = s.tr.encode(s.src_d, s.lens_d)
+    torch.cuda.synchronize()
+    mem, keys, fh, fc = s.tr.enc_views(ws, B, S)
+    pick = [0, B // 2, B - 1]
+    enc = O.encode(s.model, s.src[pick], s.lens[pick])
+    tol = 1e-4 if s.w.wdtype == "fp32" else 2e-2
+    np.testing.assert_allclose(mem.cpu().numpy()[pick], enc.memory, atol=tol, rtol=0)
+    for l in range(s.w.dec_layers):
+        np.testing.assert_allclose(fh[l].cpu().numpy()[pick], enc.final_h[l], atol=tol, rtol=0)
+
+
+@pytest.mark.parametrize("which", ["larger", "greedy"])
+def test_decode_step_bf16(which, request):
+    # one full-vocabulary step from the encoder state, sampled rows, bf16 tolerance
+    s = request.getfixturevalue(which)
+    w = s.w
+    B, S = s.src.shape
+    K = w.beam
+    _print_case("decode_step", workload=w.name)
+    ws = s.tr.encode(s.src_d, s.lens_d)
+    st = s.tr.decode_init(ws, B, S, K)
+    tok = torch.full((B * K,), W.BOS_ID, dtype=torch.int32, device="cuda")
+    _, logp, _, _, attn = s.tr.decode_step(ws, B, S, K, st, tok, None, mode=0, want_attn=True)
+    torch.cuda.synchronize()
+    sent = [0, B // 2, B - 1]
+    enc = O.encode(s.model, s.src[sent], s.lens[sent])
+    ost = O.init_state(s.model, enc, K)
+    rows = np.repeat(np.arange(len(sent)), K)
+    _, o_logp, o_attn = O.decode_step(s.model, enc, ost, np.full(len(rows), W.BOS_ID), rows)
+    g_rows = np.concatenate([np.arange(b * K, (b + 1) * K) for b in sent])
+    err = np.abs(logp.cpu().numpy()[g_rows] - o_logp).max()
+    print(f"  max |logp - oracle| = {err:.3g}", flush=True)
+    assert err <= s.tau
+    np.testing.assert_allclose(attn.cpu().numpy()[g_rows], o_attn, atol=ATTN_TOL[w.wdtype], rtol=0)
+
+
+@pytest.mark.parametrize("which,sample", [("larger", [5]), ("greedy", [3, 300]), ("long_src", [7])])
+def test_beam_search_other_workloads(which, sample, request):
+    s = request.getfixturevalue(which)
+    w = s.w
+    B, S = s.src.shape
+    _print_case("beam_search", workload=w.name, B=B)
+    buf = s.tr.search_buffers(B, S, w.beam, w.max_len, w.alpha, trace=True)
+    s.tr.beam_search(s.src_d, s.lens_d, buf)
+    torch.cuda.synchronize()
+    g_len = buf["len"].cpu().numpy()
+    assert (g_len >= 1).all() and (g_len <= w.max_len).all()
+    mism = _check_search(s, buf, sample, w.beam, w.max_len, w.alpha)
+    print(f"  free-run token mismatches (replay-verified): {mism}", flush=True)

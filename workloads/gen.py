@@ -53,9 +53,10 @@ def weight_specs(w: Workload):
 def round_bf16(a: np.ndarray) -> np.ndarray:
     """float32 -> nearest bfloat16 (ties to even), returned as float32 (finite inputs)."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32)
+    u = a.view(np.uint32)
+    # no uint32 overflow for finite inputs: the largest finite pattern plus 0x8000 stays below 2^32
+    u = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)
+    return u.view(np.float32)
 
 
 def make_weights(w: Workload, seed: int = WEIGHT_SEED, peaked: bool = False):

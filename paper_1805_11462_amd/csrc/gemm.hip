@@ -28,8 +28,13 @@ struct Tile {
   static constexpr int BN = WN * TN * 16;
   static constexpr int BK = WK * KW;
   static constexpr int NT = 64 * WM * WN * WK;
-  static constexpr int ROW = BK + CH;                // LDS row stride in elements (16-byte pad)
-  static constexpr int CPR = BK / CH;                // chunks per tile row
+  static constexpr int ROW = BK;                     // LDS row stride in elements (rows are swizzled)
+  static constexpr int CPR = BK / CH;                // 16-byte chunks per tile row
+  // Chunk c of tile row r is stored in slot c ^ swz(r), with swz taking distinct values on the rows that
+  // share a 256-byte bank window, so the 16 rows one 16-byte read touches (and a row's 16-byte writes)
+  // spread over all 64 banks.
+  static constexpr int RSH = CPR >= 16 ? 0 : (CPR == 8 ? 1 : 2);
+  static constexpr int SMASK = (CPR >= 16 ? 16 : CPR) - 1;
   static constexpr int A_CH = BM * CPR;
   static constexpr int B_CH = BN * CPR;
   static constexpr int A_PT = A_CH / NT;
@@ -43,6 +48,8 @@ struct Tile {
   static constexpr int LDS = (2 * STAGE > CT) ? 2 * STAGE : CT;
   static_assert(A_CH % NT == 0 && B_CH % NT == 0, "chunks must divide evenly among threads");
   static_assert(KW % KSUB == 0 && kSegK % BK == 0, "stage must divide the segment padding");
+  static_assert(CPR == 4 || CPR == 8 || CPR >= 16, "swizzle covers 64-, 128- and >=256-byte rows");
+  __device__ static int swz(int row) { return (row >> RSH) & SMASK; }
 };
 
 // XCD-aware tile order: blocks are dealt round-robin to the 8 XCDs, so renumber them so that each
@@ -136,14 +143,17 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
     uint4 alo[C::AREP == 2 ? C::A_PT : 1];
     uint4 b[C::B_PT];
   };
+  // RSTEP and BM are multiples of 16, so every row this thread stores has the swizzle of arow0.
+  static_assert(RSTEP % 16 == 0 && C::BM % 16 == 0, "row steps must keep the swizzle");
+  const int scol = ((acol / C::CH) ^ C::swz(arow0)) * C::CH;
   auto lstore = [&](int buf, const Regs& r) {
 #pragma unroll
     for (int i = 0; i < C::A_PT; ++i) {
-      *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + acol) = r.a[i];
-      if constexpr (C::AREP == 2) *(uint4*)(As[buf] + (C::BM + arow0 + i * RSTEP) * C::ROW + acol) = r.alo[i];
+      *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + scol) = r.a[i];
+      if constexpr (C::AREP == 2) *(uint4*)(As[buf] + (C::BM + arow0 + i * RSTEP) * C::ROW + scol) = r.alo[i];
     }
 #pragma unroll
-    for (int i = 0; i < C::B_PT; ++i) *(uint4*)(Bs[buf] + (arow0 + i * RSTEP) * C::ROW + acol) = r.b[i];
+    for (int i = 0; i < C::B_PT; ++i) *(uint4*)(Bs[buf] + (arow0 + i * RSTEP) * C::ROW + scol) = r.b[i];
   };
 
   f32x4 acc[C::TM][C::TN];
@@ -152,17 +162,21 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
 #pragma unroll
     for (int y = 0; y < C::TN; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // MFMA operand reads: lane (i16, g) reads chunk (first chunk of the sub-step) + g of rows i16 + 16 x; the
+  // swizzle depends only on i16.
+  const int lsw = C::swz(i16);
   auto compute = [&](int buf, bool has_lo) {
-    const T* Ab = As[buf] + (wm * C::TM * 16 + i16) * C::ROW + wk * C::KW;
-    const T* Bb = Bs[buf] + (wn * C::TN * 16 + i16) * C::ROW + wk * C::KW;
+    const T* Ab = As[buf] + (wm * C::TM * 16 + i16) * C::ROW;
+    const T* Bb = Bs[buf] + (wn * C::TN * 16 + i16) * C::ROW;
 #pragma unroll
     for (int sub = 0; sub < C::KW / C::KSUB; ++sub) {
+      const int col = (((wk * C::KW + sub * C::KSUB) / C::CH + g) ^ lsw) * C::CH;
       if constexpr (!C::kBf16) {
         f32x4 av[C::TM], bv[C::TN];
 #pragma unroll
-        for (int x = 0; x < C::TM; ++x) av[x] = *(const f32x4*)(Ab + x * 16 * C::ROW + sub * 16 + 4 * g);
+        for (int x = 0; x < C::TM; ++x) av[x] = *(const f32x4*)(Ab + x * 16 * C::ROW + col);
 #pragma unroll
-        for (int y = 0; y < C::TN; ++y) bv[y] = *(const f32x4*)(Bb + y * 16 * C::ROW + sub * 16 + 4 * g);
+        for (int y = 0; y < C::TN; ++y) bv[y] = *(const f32x4*)(Bb + y * 16 * C::ROW + col);
 #pragma unroll
         for (int m = 0; m < 4; ++m)
 #pragma unroll
@@ -173,9 +187,9 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
       } else {
         bf16x8 av[C::TM], bv[C::TN];
 #pragma unroll
-        for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ab + x * 16 * C::ROW + sub * 32 + 8 * g);
+        for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ab + x * 16 * C::ROW + col);
 #pragma unroll
-        for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + sub * 32 + 8 * g);
+        for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + col);
 #pragma unroll
         for (int x = 0; x < C::TM; ++x)
 #pragma unroll
@@ -184,7 +198,7 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
         if (has_lo) {               // uniform: the segment's source is fp32
 #pragma unroll
           for (int x = 0; x < C::TM; ++x)
-            av[x] = *(const bf16x8*)(Ab + (C::BM + x * 16) * C::ROW + sub * 32 + 8 * g);
+            av[x] = *(const bf16x8*)(Ab + (C::BM + x * 16) * C::ROW + col);
 #pragma unroll
           for (int x = 0; x < C::TM; ++x)
 #pragma unroll
@@ -342,7 +356,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_lstm(AOp a, BOp b, LstmParams p,
   }
 }
 
-// Generator: 4 threads per row, 32 contiguous columns each. Row max and sum of exponentials are
+// Generator: 4 threads per row, 32 interleaved columns each. Row max and sum of exponentials are
 // combined with lane shuffles; the tile's top-K is taken with K rounds of a 4-lane argmax (larger
 // logit first, smaller id on ties), each thread skipping the columns it already gave away.
 template <class T, class C>
@@ -354,28 +368,24 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
   const int m0 = mt * C::BM, n0 = nt * C::BN;
   gemm_tile<T, C>(a, b, m0, n0, smem);
   const float* Ct = (const float*)smem;
+  // thread (row r, part p) owns columns 4 j + p, j < 32: the 64 lanes of a wave then read 64 different
+  // banks of the output tile for every j
   const int r = threadIdx.x >> 2, part = threadIdx.x & 3;
   const int row = m0 + r;
-  const int c0 = n0 + part * 32;
   const float ninf = -__builtin_inff();
   float z[32];
   float mx = ninf;
 #pragma unroll
   for (int j = 0; j < 32; ++j) {
-    const int gc = c0 + j;
-    z[j] = gc < p.V ? ctile<C>(Ct, r, part * 32 + j) + p.bias[gc] : ninf;
+    const int gc = n0 + 4 * j + part;
+    z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) + p.bias[gc] : ninf;
     mx = fmaxf(mx, z[j]);
   }
   if (p.logits && row < a.M) {
 #pragma unroll
-    for (int j = 0; j < 32; j += 4) {
-      const int gc = c0 + j;
-      if (gc + 3 < p.V && (p.ld_logits & 3) == 0) {
-        *(float4*)(p.logits + (size_t)row * p.ld_logits + gc) = make_float4(z[j], z[j + 1], z[j + 2], z[j + 3]);
-      } else {
-        for (int q = 0; q < 4; ++q)
-          if (gc + q < p.V) p.logits[(size_t)row * p.ld_logits + gc + q] = z[j + q];
-      }
+    for (int j = 0; j < 32; ++j) {
+      const int gc = n0 + 4 * j + part;
+      if (gc < p.V) p.logits[(size_t)row * p.ld_logits + gc] = z[j];
     }
   }
   float rmx = fmaxf(mx, __shfl_xor(mx, 1, kWave));
@@ -402,17 +412,18 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
         bj = j;
       }
     }
-    int bid = bv > ninf ? c0 + bj : 0x7fffffff;
+    int bid = bv > ninf ? n0 + 4 * bj + part : 0x7fffffff;
+    const int mine = bid;
 #pragma unroll
-    for (int s = 1; s < 4; s <<= 1) {
-      const float ov = __shfl_xor(bv, s, kWave);
-      const int oi = __shfl_xor(bid, s, kWave);
+    for (int sft = 1; sft < 4; sft <<= 1) {
+      const float ov = __shfl_xor(bv, sft, kWave);
+      const int oi = __shfl_xor(bid, sft, kWave);
       if (before(ov, oi, bv, bid)) {
         bv = ov;
         bid = oi;
       }
     }
-    if (bid == c0 + bj && bv > ninf) taken |= 1u << bj;
+    if (bid == mine && bv > ninf) taken |= 1u << bj;
     if (part == 0 && row < a.M) {
       p.pval[o * p.K + k] = bv;
       p.pid[o * p.K + k] = bid;

@@ -1,6 +1,8 @@
 // Softmax merge, beam step and backtrack kernels (Section 2: softmax layer and item (d) beam search;
 // Section 4.2: length normalisation), plus small layout helpers.
 
+#include <cmath>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -45,19 +47,16 @@ __device__ __forceinline__ void row_merge_wave(const float* __restrict__ pmax, c
   }
   const float lse = gmx + __logf(wave_sum(sm));
 
-  // theta: K-th largest lane maximum, by rank among the 64 (lane index breaks ties)
-  sv[lane] = mx;
-  if (lane == 0) *cnt = 0;
-  __builtin_amdgcn_wave_barrier();
+  // theta: K-th largest lane maximum, by rank among the 64 (lane index breaks ties), broadcast through
+  // the scalar unit
   int rank = 0;
   for (int l = 0; l < kWave; ++l) {
-    const float o = sv[l];
+    const float o = readlane_f(mx, l);
     rank += (o > mx || (o == mx && l < lane)) ? 1 : 0;
   }
-  __builtin_amdgcn_wave_barrier();
-  if (rank == K - 1) si[0] = __builtin_bit_cast(int, mx);
-  __builtin_amdgcn_wave_barrier();
-  const float theta = K <= kWave ? __builtin_bit_cast(float, si[0]) : ninf;
+  const unsigned long long sel = __ballot(rank == K - 1);
+  const float theta = sel ? readlane_f(mx, __builtin_ctzll(sel)) : ninf;
+  if (lane == 0) *cnt = 0;
   __builtin_amdgcn_wave_barrier();
 
   // survivors: entries >= theta of the tiles whose maximum reaches theta; a qualifying tile's list is
@@ -87,7 +86,17 @@ __device__ __forceinline__ void row_merge_wave(const float* __restrict__ pmax, c
   }
   __builtin_amdgcn_wave_barrier();
   const int n = *cnt;
-  if (n <= kSurvivorCap) {
+  if (n <= kWave) {
+    // one survivor per lane, ranked against the others through the scalar unit
+    const float v = lane < n ? sv[lane] : ninf;
+    const int id = lane < n ? si[lane] : 0x7fffffff;
+    int r = 0;
+    for (int d = 0; d < n; ++d) r += before(readlane_f(v, d), readlane_i(id, d), v, id) ? 1 : 0;
+    if (lane < n && r < K) {
+      out_val[r] = v - lse;
+      if (out_id) out_id[r] = id;
+    }
+  } else if (n <= kSurvivorCap) {
     for (int c = lane; c < n; c += kWave) {
       const float v = sv[c];
       const int id = si[c];
@@ -198,16 +207,15 @@ hipError_t beam_init(const BeamParams& p, int bos, hipStream_t st) {
 // flat index slot*V + token on ties) is selected by rank in wave 0 and walked in rank order by lane 0:
 // EOS (or any choice at the last step) goes to the finished pool, which only keeps its best entry by
 // normalised score, the rest fill live slots.
-__global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, GenPartials gp, int t) {
+__global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, GenPartials gp, int t, double lp_t) {
   __shared__ float sv[kMaxBeam][kSurvivorCap];
   __shared__ int si[kMaxBeam][kSurvivorCap];
   __shared__ int cnt[kMaxBeam];
   __shared__ float tkv[kMaxBeam][kMaxBeam];
   __shared__ int tki[kMaxBeam][kMaxBeam];
-  __shared__ double cand_v[kMaxBeam * kMaxBeam];
-  __shared__ long long cand_f[kMaxBeam * kMaxBeam];
   __shared__ double sel_v[kMaxBeam];
-  __shared__ long long sel_f[kMaxBeam];
+  __shared__ int sel_slot[kMaxBeam];
+  __shared__ int sel_tok[kMaxBeam];
   __shared__ float sel_l[kMaxBeam];
   __shared__ double s_score[kMaxBeam];
   __shared__ double s_best_norm;
@@ -233,31 +241,56 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
   __syncthreads();
   if (w != 0) return;
 
+  // the sentence's top K of the K x K candidates, by rank: lane c holds candidates c + 64 i and counts
+  // the candidates before each of them (broadcast through the scalar unit)
   const int nc = K * K;
-  for (int c = lane; c < nc; c += kWave) {
-    const int k = c / K, j = c % K;
-    const double s = s_score[k];
-    cand_v[c] = s > -__builtin_inf() ? s + (double)tkv[k][j] : -__builtin_inf();
-    cand_f[c] = (long long)k * p.V + tki[k][j];
+  constexpr int PER = (kMaxBeam * kMaxBeam) / kWave;
+  double cv[PER];
+  long long cf[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int c = lane + i * kWave;
+    cv[i] = -__builtin_inf();
+    cf[i] = 0x7fffffffffffffffLL;
+    if (c < nc) {
+      const int k = c / K, j = c % K;
+      const double sc = s_score[k];
+      if (sc > -__builtin_inf()) {
+        cv[i] = sc + (double)tkv[k][j];
+        cf[i] = (long long)k * p.V + tki[k][j];
+      }
+    }
+  }
+  int rk[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) rk[i] = 0;
+#pragma unroll
+  for (int i2 = 0; i2 < PER; ++i2) {
+    const int nd = nc - i2 * kWave < kWave ? nc - i2 * kWave : kWave;    // <= 0: nothing in this set
+    const double mv = cv[i2];
+    const long long mf = cf[i2];
+    for (int d = 0; d < nd; ++d) {
+      const double ov = readlane_d(mv, d);
+      const long long of = readlane_ll(mf, d);
+#pragma unroll
+      for (int i = 0; i < PER; ++i) rk[i] += before(ov, of, cv[i], cf[i]) ? 1 : 0;
+    }
   }
   if (lane < K) sel_v[lane] = -__builtin_inf();
   __builtin_amdgcn_wave_barrier();
-  for (int c = lane; c < nc; c += kWave) {
-    const double v = cand_v[c];
-    const long long f = cand_f[c];
-    if (!(v > -__builtin_inf())) continue;
-    int r = 0;
-    for (int d = 0; d < nc; ++d) r += before(cand_v[d], cand_f[d], v, f) ? 1 : 0;
-    if (r < K) {
-      sel_v[r] = v;
-      sel_f[r] = f;
-      sel_l[r] = tkv[c / K][c % K];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int c = lane + i * kWave;
+    if (c < nc && cv[i] > -__builtin_inf() && rk[i] < K) {
+      sel_v[rk[i]] = cv[i];
+      sel_slot[rk[i]] = c / K;
+      sel_tok[rk[i]] = tki[c / K][c % K];
+      sel_l[rk[i]] = tkv[c / K][c % K];
     }
   }
   __builtin_amdgcn_wave_barrier();
   if (lane != 0) return;
 
-  const double lp_t = pow((5.0 + t) / 6.0, p.alpha);
   const size_t N = (size_t)p.B * K;
   int live = 0;
   double live_max = -__builtin_inf();
@@ -266,11 +299,10 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
   for (int k = 0; k < K; ++k) {
     const double v = sel_v[k];
     if (!(v > -__builtin_inf())) break;                    // fewer finite candidates than K
-    const long long f = sel_f[k];
-    const int slot = (int)(f / p.V);
-    const int wtok = (int)(f - (long long)slot * p.V);
+    const int slot = sel_slot[k];
+    const int wtok = sel_tok[k];
     const float lp = sel_l[k];
-    if (p.tr_slot) {
+  if (p.tr_slot) {
       const size_t o = ((size_t)(t - 1) * p.B + b) * K + k;
       p.tr_slot[o] = slot;
       p.tr_tok[o] = wtok;
@@ -314,7 +346,8 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
 
 hipError_t beam_step(const BeamParams& p, const GenPartials& gp, int t, hipStream_t st) {
   if (gp.ntiles > kWave * kMaxTilesPerLane || p.K > kMaxBeam) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_beam_step, dim3(p.B), dim3(p.K * kWave), 0, st, p, gp, t);
+  const double lp_t = std::pow((5.0 + t) / 6.0, p.alpha);     // GNMT length penalty of this step
+  hipLaunchKernelGGL(k_beam_step, dim3(p.B), dim3(p.K * kWave), 0, st, p, gp, t, lp_t);
   return hipGetLastError();
 }
 

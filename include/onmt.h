@@ -161,11 +161,12 @@ int onmt_beam_search(onmt_model* model, const int32_t* src, const int32_t* len, 
                      const onmt_trace* trace, void* stream);
 
 /* ---- Kernel timing -----------------------------------------------------------------------------------
- * When enabled, onmt_beam_search records HIP events around every launch of the decoder's generator
- * kernel (the vocabulary projection with its fused log-softmax/top-K epilogue) on `stream`, and
- * onmt_profile_read returns how many launches were timed and their summed duration in milliseconds since
- * the last reset. Timing adds two event records per step. */
-int onmt_profile_enable(onmt_model* model, int on);
+ * onmt_profile_enable(model, every): every >= 1 makes onmt_beam_search record HIP events on `stream`
+ * around every `every`-th launch of the decoder's generator kernel (the vocabulary projection with its
+ * fused log-softmax/top-K epilogue), counting launches from this call; 0 switches timing off; < 0 is
+ * ONMT_EINVAL. onmt_profile_read returns how many launches were timed and their summed duration in
+ * milliseconds since the last reset. Each timed launch adds two event records to the stream. */
+int onmt_profile_enable(onmt_model* model, int every);
 int onmt_profile_read(onmt_model* model, int* n_launches, double* total_ms, int reset);
 
 #ifdef __cplusplus

@@ -1,207 +1,271 @@
 // Global "general" attention over the source memory (Section 2 attention pooling; Section 4.2 attention
-// types; Figure 1(a) caption) for all beam rows of one sentence per workgroup.
+// types; Figure 1(a) caption).
 //
 // score e[k, s] = q_k . keys[s] with keys = W_a m_s precomputed once per batch; pads (s >= n_b) are
 // excluded, so their weight is exactly zero; a[k, :] = softmax over the real positions;
-// ctx_k = sum_s a[k, s] m_s. The sentence's keys and memory are read once per step and shared by its
-// K beam rows. The step is latency-bound (a few hundred KB per sentence), so every phase issues its
-// loads in unrolled batches to keep many of them in flight.
+// ctx_k = sum_s a[k, s] m_s.
+//
+// The step moves a few hundred KB per sentence, so it is bound by how many loads are in flight, not by
+// arithmetic. It runs as two launches that each issue all of their loads up front:
+//   k_attn_scores  one workgroup per (sentence, 8 source positions): the positions' key rows are read
+//                  once and dotted with the sentence's K query rows;
+//   k_attn_context one workgroup per (sentence, group of memory columns): every group repeats the
+//                  (cheap) softmax over the sentence's K x n scores, then reduces its columns of the
+//                  memory rows, which it started loading before the softmax.
+// Keys and memory are each read once per step, and all reductions run in a fixed order.
 
 #include "common.h"
 #include "kernels.h"
 
 namespace onmt {
 
-constexpr int kAttnThreads = 512;
-constexpr int kLanesPerPos = 16;     // lanes cooperating on one source position's dot products
-constexpr int kKeyChunks = 16;       // float4 chunks of one key row held per lane (H <= 1024)
-constexpr int kCtxUnroll = 4;
+constexpr int kScoreThreads = 256;
+constexpr int kScoreLanes = 32;                             // lanes per source position
+constexpr int kScorePos = kScoreThreads / kScoreLanes;      // source positions per workgroup
+constexpr int kScoreChunks = 8;                             // float4 chunks of a key row per lane (H <= 1024)
+constexpr int kCtxThreads = 512;
+constexpr int kCtxBatch = 4;                                // memory rows in flight per thread
+constexpr int kCtxTargetBlocks = 256;                       // at least one workgroup per CU when B allows
+constexpr size_t kAttnLdsLimit = 64 * 1024;
 
+// e [B*K, S_max]: raw scores of the real positions (pads are never written).
 template <int KMAX>
-__global__ __launch_bounds__(kAttnThreads) void k_attention(const float* __restrict__ q, int ld_q,
-                                                            const float* __restrict__ keys,
-                                                            const float* __restrict__ mem,
-                                                            const int32_t* __restrict__ lens, int S_max, int H,
-                                                            int Hm, int K, int G, float* __restrict__ ctx,
-                                                            float* __restrict__ attn) {
-  extern __shared__ __attribute__((aligned(16))) float lds[];
-  float* qs = lds;                       // [K][H]
-  float* es = lds + K * H;               // [K][S_max]
-  float* red = es + K * S_max;           // [groups - 1][K][Hm] partial contexts
-  const int b = blockIdx.x;
-  const int tid = threadIdx.x;
+__global__ __launch_bounds__(kScoreThreads) void k_attn_scores(const float* __restrict__ q, int ld_q,
+                                                               const float* __restrict__ keys,
+                                                               const int32_t* __restrict__ lens, int S_max, int H,
+                                                               int K, int nchunk, float* __restrict__ e) {
+  extern __shared__ __attribute__((aligned(16))) float qs[];      // [K][H]
+  const int b = blockIdx.x / nchunk, p = blockIdx.x % nchunk;
   const int n = lens[b];
+  const int s0 = p * kScorePos;
+  if (s0 >= n) return;
+  const int tid = threadIdx.x;
+  const int sub = tid % kScoreLanes;
+  const int s = s0 + tid / kScoreLanes;
+  const int H4 = H / 4;
+  // the key row first: its loads depend on nothing (rows past n re-read row s0, results unused)
+  const float* kr = keys + ((size_t)b * S_max + (s < n ? s : s0)) * H;
+  float4 kv[kScoreChunks];
+#pragma unroll
+  for (int j = 0; j < kScoreChunks; ++j) {
+    const int c = sub + j * kScoreLanes;
+    kv[j] = c < H4 ? *(const float4*)(kr + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  // the sentence's K query rows to LDS, all loads issued before the first store
   const int r0 = b * K;
-  const int H4 = H / 4, Hm4 = Hm / 4;
-
-  for (int e = tid; e < K * H4; e += kAttnThreads) {
-    const int k = e / H4, c = e % H4;
-    *(float4*)(qs + k * H + 4 * c) = *(const float4*)(q + (size_t)(r0 + k) * ld_q + 4 * c);
+  constexpr int QPT = KMAX * kScoreChunks * kScoreLanes / kScoreThreads;   // >= K * H4 / threads
+  float4 qv[QPT];
+#pragma unroll
+  for (int u = 0; u < QPT; ++u) {
+    const int i = tid + u * kScoreThreads;
+    qv[u] = i < K * H4 ? *(const float4*)(q + (size_t)(r0 + i / H4) * ld_q + 4 * (i % H4))
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+#pragma unroll
+  for (int u = 0; u < QPT; ++u) {
+    const int i = tid + u * kScoreThreads;
+    if (i < K * H4) *(float4*)(qs + (i / H4) * H + 4 * (i % H4)) = qv[u];
   }
   __syncthreads();
-
-  // scores: 16 lanes per source position, the position's key row loaded in one batch
-  const int grp = tid / kLanesPerPos, sub = tid % kLanesPerPos;
-  constexpr int kGroups = kAttnThreads / kLanesPerPos;
-  const float* kb = keys + (size_t)b * S_max * H;
-  for (int s0 = 0; s0 < n; s0 += kGroups) {
-    const int s = s0 + grp;
-    float4 kv[kKeyChunks];
+  float acc[KMAX];
 #pragma unroll
-    for (int j = 0; j < kKeyChunks; ++j) {
-      const int c = sub + j * kLanesPerPos;
-      kv[j] = (s < n && c < H4) ? *(const float4*)(kb + (size_t)s * H + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    float acc[KMAX];
+  for (int k = 0; k < KMAX; ++k) {
+    acc[k] = 0.f;
+    if (k < K) {
 #pragma unroll
-    for (int k = 0; k < KMAX; ++k) {
-      acc[k] = 0.f;
-      if (k < K) {
-#pragma unroll
-        for (int j = 0; j < kKeyChunks; ++j) {
-          const int c = sub + j * kLanesPerPos;
-          if (c < H4) {
-            const float4 qv = *(const float4*)(qs + k * H + 4 * c);
-            acc[k] += kv[j].x * qv.x + kv[j].y * qv.y + kv[j].z * qv.z + kv[j].w * qv.w;
-          }
+      for (int j = 0; j < kScoreChunks; ++j) {
+        const int c = sub + j * kScoreLanes;
+        if (c < H4) {
+          const float4 qv = *(const float4*)(qs + k * H + 4 * c);
+          acc[k] += kv[j].x * qv.x + kv[j].y * qv.y + kv[j].z * qv.z + kv[j].w * qv.w;
         }
       }
     }
+  }
 #pragma unroll
-    for (int k = 0; k < KMAX; ++k) {
+  for (int k = 0; k < KMAX; ++k) {
 #pragma unroll
-      for (int o = kLanesPerPos / 2; o > 0; o >>= 1) acc[k] += __shfl_xor(acc[k], o, kWave);
+    for (int o = kScoreLanes / 2; o > 0; o >>= 1) acc[k] += __shfl_xor(acc[k], o, kWave);
+  }
+  if (sub == 0 && s < n) {
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k)
+      if (k < K) e[(size_t)(r0 + k) * S_max + s] = acc[k];
+  }
+}
+
+// Thread (pl, c): pl = one of PL position lanes (adjacent lanes of a wave), c = one float4 column of the
+// group's CW = kCtxThreads / PL columns. Positions pl, pl + PL, ... are summed per thread, then across
+// the PL lanes by butterfly shuffles.
+template <int KMAX, int PL>
+__global__ __launch_bounds__(kCtxThreads) void k_attn_context(const float* __restrict__ e,
+                                                              const float* __restrict__ mem,
+                                                              const int32_t* __restrict__ lens, int S_max, int Hm,
+                                                              int K, int G, float* __restrict__ ctx,
+                                                              float* __restrict__ attn) {
+  extern __shared__ __attribute__((aligned(16))) float as[];      // [K][S_max] attention weights
+  constexpr int CW = kCtxThreads / PL;
+  const int b = blockIdx.x / G, g = blockIdx.x % G;
+  const int n = lens[b];
+  const int tid = threadIdx.x;
+  const int pl = tid % PL;
+  const int c = g * CW + tid / PL;
+  const int Hm4 = Hm / 4;
+  const bool col_ok = c < Hm4;
+  const float* mb = mem + (size_t)b * S_max * Hm + 4 * (col_ok ? c : 0);
+  // first batch of memory rows, issued before the softmax, which it does not depend on
+  float4 mv[kCtxBatch];
+#pragma unroll
+  for (int u = 0; u < kCtxBatch; ++u) {
+    const int s = pl + u * PL;
+    mv[u] = (col_ok && s < n) ? *(const float4*)(mb + (size_t)s * Hm) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  // the sentence's K x n scores to LDS, kCtxBatch loads in flight per thread
+  const int r0 = b * K;
+  for (int i0 = 0; i0 < K * n; i0 += kCtxBatch * kCtxThreads) {
+    float ev[kCtxBatch];
+#pragma unroll
+    for (int u = 0; u < kCtxBatch; ++u) {
+      const int i = i0 + tid + u * kCtxThreads;
+      ev[u] = i < K * n ? e[(size_t)(r0 + i / n) * S_max + i % n] : 0.f;
     }
-    if (s < n && sub == 0) {
 #pragma unroll
-      for (int k = 0; k < KMAX; ++k)
-        if (k < K) es[k * S_max + s] = acc[k];
+    for (int u = 0; u < kCtxBatch; ++u) {
+      const int i = i0 + tid + u * kCtxThreads;
+      if (i < K * n) as[(i / n) * S_max + i % n] = ev[u];
     }
   }
   __syncthreads();
 
-  // softmax over real positions, one wave per row
+  // softmax over the real positions, one wave per row
   const int wave = tid / kWave, lane = tid % kWave;
-  for (int k = wave; k < K; k += kAttnThreads / kWave) {
+  for (int k = wave; k < K; k += kCtxThreads / kWave) {
+    float* row = as + k * S_max;
     float mx = -__builtin_inff();
-    for (int s = lane; s < n; s += kWave) mx = fmaxf(mx, es[k * S_max + s]);
+    for (int s = lane; s < n; s += kWave) mx = fmaxf(mx, row[s]);
     mx = wave_max(mx);
     float sm = 0.f;
     for (int s = lane; s < n; s += kWave) {
-      const float p = __expf(es[k * S_max + s] - mx);
-      es[k * S_max + s] = p;
-      sm += p;
+      const float pv = __expf(row[s] - mx);
+      row[s] = pv;
+      sm += pv;
     }
     sm = wave_sum(sm);
     const float inv = 1.0f / sm;
-    for (int s = lane; s < S_max; s += kWave) {
-      const float a = s < n ? es[k * S_max + s] * inv : 0.f;
-      if (s < n) es[k * S_max + s] = a;
-      if (attn) attn[(size_t)(r0 + k) * S_max + s] = a;
+    for (int s = lane; s < n; s += kWave) row[s] *= inv;
+    if (attn && g == 0) {
+      for (int s = lane; s < S_max; s += kWave) attn[(size_t)(r0 + k) * S_max + s] = s < n ? row[s] : 0.f;
     }
   }
   __syncthreads();
 
-  // context: thread (group gi, column chunk c) sums positions gi, gi + G, ...; groups are then
-  // combined in a fixed order through LDS (deterministic).
-  const float* mb = mem + (size_t)b * S_max * Hm;
-  for (int c0 = 0; c0 < Hm4; c0 += kAttnThreads / G) {
-    const int c = c0 + tid % (kAttnThreads / G);
-    const int gi = tid / (kAttnThreads / G);
-    const bool act = c < Hm4 && gi < G;
-    float4 acc[KMAX];
+  float4 acc[KMAX];
 #pragma unroll
-    for (int k = 0; k < KMAX; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (act) {
-      for (int s = gi; s < n; s += G * kCtxUnroll) {
-        float4 mv[kCtxUnroll];
+  for (int k = 0; k < KMAX; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+  // batches of kCtxBatch rows per thread; the next batch is loaded while the current one is reduced
+  for (int sb = 0; sb < n; sb += PL * kCtxBatch) {
+    float4 nv[kCtxBatch];
+    const int sn = sb + PL * kCtxBatch;
 #pragma unroll
-        for (int u = 0; u < kCtxUnroll; ++u) {
-          const int ss = s + u * G;
-          mv[u] = ss < n ? *(const float4*)(mb + (size_t)ss * Hm + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+    for (int u = 0; u < kCtxBatch; ++u) {
+      const int s = sn + pl + u * PL;
+      nv[u] = (col_ok && s < n) ? *(const float4*)(mb + (size_t)s * Hm) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
 #pragma unroll
-        for (int u = 0; u < kCtxUnroll; ++u) {
-          const int ss = s + u * G;
-          if (ss < n) {
+    for (int u = 0; u < kCtxBatch; ++u) {
+      const int s = sb + pl + u * PL;
+      if (s < n) {
 #pragma unroll
-            for (int k = 0; k < KMAX; ++k) {
-              if (k < K) {
-                const float a = es[k * S_max + ss];
-                acc[k].x += a * mv[u].x;
-                acc[k].y += a * mv[u].y;
-                acc[k].z += a * mv[u].z;
-                acc[k].w += a * mv[u].w;
-              }
-            }
+        for (int k = 0; k < KMAX; ++k) {
+          if (k < K) {
+            const float a = as[k * S_max + s];
+            acc[k].x += a * mv[u].x;
+            acc[k].y += a * mv[u].y;
+            acc[k].z += a * mv[u].z;
+            acc[k].w += a * mv[u].w;
           }
         }
       }
     }
-    if (G > 1) {
-      if (act && gi > 0) {
 #pragma unroll
-        for (int k = 0; k < KMAX; ++k)
-          if (k < K) *(float4*)(red + ((size_t)(gi - 1) * K + k) * Hm + 4 * c) = acc[k];
-      }
-      __syncthreads();
-      if (act && gi == 0) {
-        for (int j = 1; j < G; ++j) {
+    for (int u = 0; u < kCtxBatch; ++u) mv[u] = nv[u];
+  }
 #pragma unroll
-          for (int k = 0; k < KMAX; ++k) {
-            if (k < K) {
-              const float4 o = *(const float4*)(red + ((size_t)(j - 1) * K + k) * Hm + 4 * c);
-              acc[k].x += o.x;
-              acc[k].y += o.y;
-              acc[k].z += o.z;
-              acc[k].w += o.w;
-            }
-          }
-        }
-      }
-      __syncthreads();
+  for (int k = 0; k < KMAX; ++k) {
+#pragma unroll
+    for (int o = PL / 2; o > 0; o >>= 1) {
+      acc[k].x += __shfl_xor(acc[k].x, o, kWave);
+      acc[k].y += __shfl_xor(acc[k].y, o, kWave);
+      acc[k].z += __shfl_xor(acc[k].z, o, kWave);
+      acc[k].w += __shfl_xor(acc[k].w, o, kWave);
     }
-    if (act && gi == 0) {
+  }
+  if (pl == 0 && col_ok) {
 #pragma unroll
-      for (int k = 0; k < KMAX; ++k)
-        if (k < K) *(float4*)(ctx + (size_t)(r0 + k) * Hm + 4 * c) = acc[k];
-    }
+    for (int k = 0; k < KMAX; ++k)
+      if (k < K) *(float4*)(ctx + (size_t)(r0 + k) * Hm + 4 * c) = acc[k];
   }
 }
 
-constexpr size_t kAttnLdsLimit = 64 * 1024;
-
-static size_t lds_for(int S_max, int H, int K, int G) {
-  return (size_t)K * (H + S_max) * sizeof(float) + (size_t)(G - 1) * K * H * sizeof(float);
+size_t attention_lds_bytes(int S_max, int H, int K) {
+  const size_t a = (size_t)K * H * sizeof(float), c = (size_t)K * S_max * sizeof(float);
+  return a > c ? a : c;
 }
 
-// Position groups for the context phase: as many as the threads allow (at most 4) within the LDS limit.
-static int ctx_groups(int S_max, int H, int K) {
-  int g = kAttnThreads / (H / 4);
-  g = g < 1 ? 1 : (g > 4 ? 4 : g);
-  while (g > 1 && lds_for(S_max, H, K, g) > kAttnLdsLimit) --g;
-  return g;
+// Position lanes for the context launch: the fewest (widest column groups) that still give every CU a
+// workgroup, else 64.
+static int ctx_lanes(int B, int Hm4) {
+  for (int pl = 4; pl < 64; pl *= 2) {
+    const int cw = kCtxThreads / pl;
+    if ((long long)B * ((Hm4 + cw - 1) / cw) >= kCtxTargetBlocks) return pl;
+  }
+  return 64;
 }
 
-size_t attention_lds_bytes(int S_max, int H, int K) { return lds_for(S_max, H, K, 1); }
+template <int KMAX>
+static void launch_context(int pl, dim3 grid, size_t lds, hipStream_t st, const float* e, const float* mem,
+                           const int32_t* lens, int S_max, int Hm, int K, int G, float* ctx, float* attn) {
+  const dim3 block(kCtxThreads);
+  switch (pl) {
+    case 4: hipLaunchKernelGGL((k_attn_context<KMAX, 4>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
+    case 8: hipLaunchKernelGGL((k_attn_context<KMAX, 8>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
+    case 16: hipLaunchKernelGGL((k_attn_context<KMAX, 16>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
+    case 32: hipLaunchKernelGGL((k_attn_context<KMAX, 32>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
+    default: hipLaunchKernelGGL((k_attn_context<KMAX, 64>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
+  }
+}
 
 hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens, int B,
-                     int S_max, int H, int Hm, int K, float* ctx, float* attn, hipStream_t st) {
-  if (H / 4 > kLanesPerPos * kKeyChunks || Hm != H) return hipErrorInvalidValue;
-  const int G = ctx_groups(S_max, H, K);
-  const size_t lds = lds_for(S_max, H, K, G);
-  if (lds > kAttnLdsLimit) return hipErrorInvalidValue;
-  dim3 grid(B), block(kAttnThreads);
+                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, hipStream_t st) {
+  if (H / 4 > kScoreLanes * kScoreChunks || H % 4 || Hm % 4 || K < 1 || K > kMaxBeam) return hipErrorInvalidValue;
+  if (attention_lds_bytes(S_max, H, K) > kAttnLdsLimit) return hipErrorInvalidValue;
+  const int nchunk = (S_max + kScorePos - 1) / kScorePos;
+  const dim3 sgrid(B * nchunk), sblock(kScoreThreads);
+  const size_t slds = (size_t)K * H * sizeof(float);
   if (K <= 1)
-    hipLaunchKernelGGL(k_attention<1>, grid, block, lds, st, q, ld_q, keys, mem, lens, S_max, H, Hm, K, G, ctx, attn);
+    hipLaunchKernelGGL(k_attn_scores<1>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
   else if (K <= 2)
-    hipLaunchKernelGGL(k_attention<2>, grid, block, lds, st, q, ld_q, keys, mem, lens, S_max, H, Hm, K, G, ctx, attn);
+    hipLaunchKernelGGL(k_attn_scores<2>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
   else if (K <= 4)
-    hipLaunchKernelGGL(k_attention<4>, grid, block, lds, st, q, ld_q, keys, mem, lens, S_max, H, Hm, K, G, ctx, attn);
+    hipLaunchKernelGGL(k_attn_scores<4>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
   else if (K <= 8)
-    hipLaunchKernelGGL(k_attention<8>, grid, block, lds, st, q, ld_q, keys, mem, lens, S_max, H, Hm, K, G, ctx, attn);
+    hipLaunchKernelGGL(k_attn_scores<8>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
   else
-    hipLaunchKernelGGL(k_attention<16>, grid, block, lds, st, q, ld_q, keys, mem, lens, S_max, H, Hm, K, G, ctx, attn);
+    hipLaunchKernelGGL(k_attn_scores<16>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+
+  const int Hm4 = Hm / 4;
+  const int pl = ctx_lanes(B, Hm4);
+  const int cw = kCtxThreads / pl;
+  const int G = (Hm4 + cw - 1) / cw;
+  const dim3 cgrid(B * G);
+  const size_t clds = (size_t)K * S_max * sizeof(float);
+  if (K <= 1) launch_context<1>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
+  else if (K <= 2) launch_context<2>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
+  else if (K <= 4) launch_context<4>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
+  else if (K <= 8) launch_context<8>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
+  else launch_context<16>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
   return hipGetLastError();
 }
 

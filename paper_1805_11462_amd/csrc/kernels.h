@@ -85,8 +85,8 @@ hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hi
 int gen_tile_cols();
 int gemm_tile_cols(int shape);
 
-hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens,
-                     int B, int S_max, int H, int Hm, int K, float* ctx, float* attn, hipStream_t st);
+hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens, int B,
+                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, hipStream_t st);
 size_t attention_lds_bytes(int S_max, int H, int K);
 
 hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pval, const int32_t* pid, int M,

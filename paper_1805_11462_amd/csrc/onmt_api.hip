@@ -156,7 +156,9 @@ struct onmt_model {
   Packed W_a, W_c, W_s;
   const float* b_s = nullptr;
   // kernel timing
-  bool prof = false;
+  int prof = 0;              // time every prof-th generator launch (0: off)
+  long long prof_seq = 0;    // generator launches seen while timing is on
+  bool prof_open = false;    // the current launch has a start event recorded
   int prof_n = 0;
   double prof_ms = 0.0;
   std::vector<hipEvent_t> ev;   // reusable start/stop pairs
@@ -439,6 +441,7 @@ size_t state_layout(const Dims& d, int N, char* base, State* s) {
 
 struct StepWs {
   float* ctx;      // [N, Hm]
+  float* scores;   // [N, S_max] raw attention scores
   float* pmax;     // [N, ntiles]
   float* psum;
   float* pval;     // [N, ntiles, K]
@@ -450,13 +453,13 @@ struct StepWs {
 };
 
 size_t step_layout(const Dims& d, int B, int S, int K, char* base, StepWs* w) {
-  (void)S;
   Carver c;
   c.base = base;
   StepWs t;
   const size_t N = (size_t)B * K;
   t.ntiles = (d.Vt + gen_tile_cols() - 1) / gen_tile_cols();
   t.ctx = c.take<float>(N * d.Hm);
+  t.scores = c.take<float>(N * S);
   t.pmax = c.take<float>(N * t.ntiles);
   t.psum = c.take<float>(N * t.ntiles);
   t.pval = c.take<float>(N * t.ntiles * K);
@@ -657,17 +660,21 @@ int decode_init_compute(onmt_model* m, const EncWs& w, int B, int K, const State
 }
 
 void time_begin(onmt_model* m, hipStream_t st) {
-  if (!m->prof) return;
+  m->prof_open = false;
+  if (!m->prof || (m->prof_seq++ % m->prof) != 0) return;
   while (m->ev.size() < m->ev_used + 2) {
     hipEvent_t e;
-    if (hipEventCreate(&e) != hipSuccess) return;
+    // timing-only events: no system-scope fence, so recording them does not stall the next kernel
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return;
     m->ev.push_back(e);
   }
   hipEventRecord(m->ev[m->ev_used], st);
   m->ev_used += 2;
+  m->prof_open = true;
 }
 void time_end(onmt_model* m, hipStream_t st) {
-  if (!m->prof || m->ev_used < 2) return;
+  if (!m->prof_open || m->ev_used < 2) return;
+  m->prof_open = false;
   hipEventRecord(m->ev[m->ev_used - 1], st);
 }
 void time_collect(onmt_model* m) {
@@ -715,7 +722,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     HIP_TRY(gemm_lstm(d.bf16, small_shape(N, m->dec_w[l].Np), a, bop(m->dec_w[l]), lp, st));
   }
   const float* q = out.h + (d.L - 1) * LH;
-  HIP_TRY(attention(q, d.H, w.keys, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.ctx, attn, st));
+  HIP_TRY(attention(q, d.H, w.keys, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.scores, sw.ctx, attn, st));
   {
     AOp a{};
     a.M = N;
@@ -761,7 +768,7 @@ int check_beam(const onmt_model* m, int S, int K) {
   if (K > m->cfg.tgt_vocab) return fail(ONMT_EINVAL, "beam %d larger than the vocabulary", K);
   if (m->d.H > 1024) return fail(ONMT_EUNSUPPORTED, "attention supports hidden <= 1024");
   if (attention_lds_bytes(S, m->d.H, K) > 64 * 1024)
-    return fail(ONMT_EUNSUPPORTED, "beam * (hidden + S_max) too large for one attention workgroup");
+    return fail(ONMT_EUNSUPPORTED, "beam * max(hidden, S_max) too large for the attention workgroups");
   return ONMT_OK;
 }
 
@@ -912,9 +919,11 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   return ONMT_OK;
 }
 
-int onmt_profile_enable(onmt_model* m, int on) {
+int onmt_profile_enable(onmt_model* m, int every) {
   if (!m) return fail(ONMT_EINVAL, "model is NULL");
-  m->prof = on != 0;
+  if (every < 0) return fail(ONMT_EINVAL, "timing period must be >= 0");
+  m->prof = every;
+  m->prof_seq = 0;
   return ONMT_OK;
 }
 

@@ -170,8 +170,9 @@ class Translator:
         return buf
 
     # ---------------------------------------------------------------- timing
-    def profile(self, on):
-        check(self.lib.onmt_profile_enable(self.handle, 1 if on else 0))
+    def profile(self, every):
+        """Time every ``every``-th generator launch of later searches (0 or False: off)."""
+        check(self.lib.onmt_profile_enable(self.handle, int(every)))
 
     def profile_read(self, reset=True):
         n = ctypes.c_int()

@@ -91,7 +91,7 @@ __device__ inline uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 }
 
 // Main loop: leaves the (WK-way partial) fp32 output tile in LDS at smem, layout [WK][BM][CROW].
-template <class T, class C>
+template <class T, class C, int NSEG>
 __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, char* smem) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -110,7 +110,7 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
 
   // Every segment field is read with a constant index into a scalar, so the argument struct is never
   // indexed at run time (which would put it in private memory).
-  const int nseg = a.nseg;
+  constexpr int nseg = NSEG;             // segments in use (a.nseg, checked by the launcher)
   // Per-thread byte offsets of the thread's A rows inside each segment's buffer (kNoRow past M).
 #define ONMT_SEG_SETUP(S)                                                                             \
   const int kp##S = a.seg[S].kpad, wd##S = a.seg[S].width, bf##S = a.seg[S].bf16;                     \
@@ -257,7 +257,11 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
       compute(0, !src_bf16);
       lstore(1, r1);
       __syncthreads();
-      if (st + 1 >= nst) break;
+      // whole pairs of stages when the stage count is even by construction: a single loop exit keeps
+      // the accumulators in place (no copies between the two exits' register assignments)
+      if constexpr ((kSegK / C::BK) % 2 != 0) {
+        if (st + 1 >= nst) break;
+      }
       // odd stage: LDS buffer 1 holds stage st + 1, r0 holds st + 2
       r1 = gload(min(st + 3, last));
       compute(1, !src_bf16);
@@ -267,8 +271,8 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
     kbyte_w += (uint32_t)kpad * sizeof(T);
   };
   run_segment(rs0, ao0, es0, wd0, kp0);
-  if (nseg > 1) run_segment(rs1, ao1, es1, wd1, kp1);
-  if (nseg > 2) run_segment(rs2, ao2, es2, wd2, kp2);
+  if constexpr (nseg > 1) run_segment(rs1, ao1, es1, wd1, kp1);
+  if constexpr (nseg > 2) run_segment(rs2, ao2, es2, wd2, kp2);
   (void)bf0;
   (void)bf1;
   (void)bf2;
@@ -295,12 +299,12 @@ __device__ inline float ctile(const float* smem, int r, int c) {
 
 // ---------------------------------------------------------------- kernels
 
-template <class T, class C>
+template <class T, class C, int NSEG>
 __global__ __launch_bounds__(C::NT) void k_gemm_store(AOp a, BOp b, StoreParams p, int nm, int nblocks) {
   __shared__ __attribute__((aligned(16))) char smem[C::LDS];
   const int L = xcd_remap(blockIdx.x, nblocks);
   const int m0 = (L % nm) * C::BM, n0 = (L / nm) * C::BN;
-  gemm_tile<T, C>(a, b, m0, n0, smem);
+  gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
   const float* Ct = (const float*)smem;
   for (int e = threadIdx.x; e < C::BM * (C::BN / 4); e += C::NT) {
     const int r = e / (C::BN / 4), c = (e % (C::BN / 4)) * 4;
@@ -316,12 +320,12 @@ __global__ __launch_bounds__(C::NT) void k_gemm_store(AOp a, BOp b, StoreParams 
   }
 }
 
-template <class T, class C>
+template <class T, class C, int NSEG>
 __global__ __launch_bounds__(C::NT) void k_gemm_lstm(AOp a, BOp b, LstmParams p, int nm, int nblocks) {
   __shared__ __attribute__((aligned(16))) char smem[C::LDS];
   const int L = xcd_remap(blockIdx.x, nblocks);
   const int m0 = (L % nm) * C::BM, n0 = (L / nm) * C::BN;
-  gemm_tile<T, C>(a, b, m0, n0, smem);
+  gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
   const float* Ct = (const float*)smem;
   constexpr int UPT = C::BN / 4;                      // units per tile
   for (int e = threadIdx.x; e < C::BM * UPT; e += C::NT) {
@@ -359,14 +363,14 @@ __global__ __launch_bounds__(C::NT) void k_gemm_lstm(AOp a, BOp b, LstmParams p,
 // Generator: 4 threads per row, 32 interleaved columns each. Row max and sum of exponentials are
 // combined with lane shuffles; the tile's top-K is taken with K rounds of a 4-lane argmax (larger
 // logit first, smaller id on ties), each thread skipping the columns it already gave away.
-template <class T, class C>
+template <class T, class C, int NSEG>
 __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, int nm, int nblocks) {
   static_assert(C::NT / C::BM == 4 && C::BN == 128, "generator tile is 64 x 128 with 256 threads");
   __shared__ __attribute__((aligned(16))) char smem[C::LDS];
   const int L = xcd_remap(blockIdx.x, nblocks);
   const int mt = L % nm, nt = L / nm;
   const int m0 = mt * C::BM, n0 = nt * C::BN;
-  gemm_tile<T, C>(a, b, m0, n0, smem);
+  gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
   const float* Ct = (const float*)smem;
   // thread (row r, part p) owns columns 4 j + p, j < 32: the 64 lanes of a wave then read 64 different
   // banks of the output tile for every j
@@ -439,6 +443,11 @@ using TileThin32 = Tile<float, 1, 1, 4, 1, 4, 16>;
 using TileWide16 = Tile<__bf16, 2, 2, 1, 2, 4, 64>;
 using TileSplit16 = Tile<__bf16, 1, 1, 4, 2, 4, 32>;
 using TileThin16 = Tile<__bf16, 1, 1, 4, 1, 4, 32>;
+// Generator: the 64 x 128 tile of the wide shapes with a 16 (fp32) / 32 (bf16) element K stage, which
+// halves the LDS stage buffers so that four workgroups fit on a CU.
+using TileGen32 = Tile<float, 2, 2, 1, 2, 4, 16>;
+using TileGen16 = Tile<__bf16, 2, 2, 1, 2, 4, 32>;
+static_assert(TileGen32::BN == TileGen16::BN, "both generator tiles give the same column tiles");
 
 template <class C>
 static inline void grid_of(const AOp& a, const BOp& b, int& nm, int& nblocks) {
@@ -458,15 +467,19 @@ static inline bool operands_fit(const AOp& a, const BOp& b) {
 }
 
 int gemm_tile_cols(int shape) { return shape == kShapeWide ? TileWide32::BN : TileSplit32::BN; }
-int gen_tile_cols() { return TileWide32::BN; }
+int gen_tile_cols() { return TileGen32::BN; }
 
+// Kernels are specialised on the number of A segments, so that a stage's segment is known at compile
+// time wherever there is only one.
 template <class T, class C>
 static hipError_t launch_store(const AOp& a, const BOp& b, const StoreParams& p, hipStream_t st) {
   int nm, nb;
   grid_of<C>(a, b, nm, nb);
-  if (!operands_fit<T>(a, b)) return hipErrorInvalidValue;
+  if (!operands_fit<T>(a, b) || a.nseg < 1 || a.nseg > 3) return hipErrorInvalidValue;
   if (nb == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_store<T, C>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+  if (a.nseg == 1) hipLaunchKernelGGL((k_gemm_store<T, C, 1>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+  else if (a.nseg == 2) hipLaunchKernelGGL((k_gemm_store<T, C, 2>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+  else hipLaunchKernelGGL((k_gemm_store<T, C, 3>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
   return hipGetLastError();
 }
 
@@ -474,19 +487,22 @@ template <class T, class C>
 static hipError_t launch_lstm(const AOp& a, const BOp& b, const LstmParams& p, hipStream_t st) {
   int nm, nb;
   grid_of<C>(a, b, nm, nb);
-  if (!operands_fit<T>(a, b)) return hipErrorInvalidValue;
+  if (!operands_fit<T>(a, b) || a.nseg < 1 || a.nseg > 3) return hipErrorInvalidValue;
   if (nb == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_lstm<T, C>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+  if (a.nseg == 1) hipLaunchKernelGGL((k_gemm_lstm<T, C, 1>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+  else if (a.nseg == 2) hipLaunchKernelGGL((k_gemm_lstm<T, C, 2>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+  else hipLaunchKernelGGL((k_gemm_lstm<T, C, 3>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
   return hipGetLastError();
 }
 
+// The generator's A operand is the attentional vector alone (one segment).
 template <class T, class C>
 static hipError_t launch_gen(const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
   int nm, nb;
   grid_of<C>(a, b, nm, nb);
-  if (!operands_fit<T>(a, b)) return hipErrorInvalidValue;
+  if (!operands_fit<T>(a, b) || a.nseg != 1) return hipErrorInvalidValue;
   if (nb == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_gen<T, C>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+  hipLaunchKernelGGL((k_gemm_gen<T, C, 1>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
   return hipGetLastError();
 }
 
@@ -513,7 +529,7 @@ hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const Lstm
 }
 
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
-  return bf16 ? launch_gen<__bf16, TileWide16>(a, b, p, st) : launch_gen<float, TileWide32>(a, b, p, st);
+  return bf16 ? launch_gen<__bf16, TileGen16>(a, b, p, st) : launch_gen<float, TileGen32>(a, b, p, st);
 }
 
 }  // namespace onmt

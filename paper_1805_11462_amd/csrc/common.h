@@ -12,7 +12,7 @@ typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kWave = 64;
 constexpr int kMaxBeam = 16;        // largest beam the register top-K lists support
-constexpr int kUnitGroup = 16;      // LSTM units per gate block in packed weights (one MFMA tile width)
+constexpr int kUnitGroup = 8;       // LSTM units per gate block in packed weights (4 gates x 8 units = 32 columns)
 
 // Round-to-nearest-even float -> bfloat16 bits (finite inputs).
 __device__ __host__ inline uint16_t f32_to_bf16_bits(float f) {

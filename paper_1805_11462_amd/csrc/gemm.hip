@@ -333,7 +333,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_lstm(AOp a, BOp b, LstmParams p,
     const int row = m0 + r;
     const int unit = n0 / 4 + uu;
     if (row >= a.M || unit >= p.H) continue;
-    const int cbase = (uu / kUnitGroup) * 64 + (uu % kUnitGroup);
+    const int cbase = (uu / kUnitGroup) * (4 * kUnitGroup) + (uu % kUnitGroup);
     float z[4];
 #pragma unroll
     for (int gt = 0; gt < 4; ++gt) {
@@ -439,7 +439,9 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
 
 using TileWide32 = Tile<float, 2, 2, 1, 2, 4, 32>;
 using TileSplit32 = Tile<float, 1, 1, 4, 2, 4, 16>;
-using TileThin32 = Tile<float, 1, 1, 4, 1, 4, 16>;
+// 16 x 32 tiles for GEMMs with few rows: twice the workgroups of a 16 x 64 tiling, which keeps more
+// loads in flight per CU (the decoder GEMMs at a few hundred rows are bound by that, not by MFMA).
+using TileThin32 = Tile<float, 1, 1, 4, 1, 2, 16>;
 using TileWide16 = Tile<__bf16, 2, 2, 1, 2, 4, 64>;
 using TileSplit16 = Tile<__bf16, 1, 1, 4, 2, 4, 32>;
 using TileThin16 = Tile<__bf16, 1, 1, 4, 1, 4, 32>;
@@ -466,7 +468,6 @@ static inline bool operands_fit(const AOp& a, const BOp& b) {
   return true;
 }
 
-int gemm_tile_cols(int shape) { return shape == kShapeWide ? TileWide32::BN : TileSplit32::BN; }
 int gen_tile_cols() { return TileGen32::BN; }
 
 // Kernels are specialised on the number of A segments, so that a stage's segment is known at compile

@@ -44,7 +44,7 @@ struct StoreParams {
   int act;
 };
 
-// LSTM cell epilogue over gate-blocked columns (groups of 64 = 4 gates x 16 units).
+// LSTM cell epilogue over gate-blocked columns (groups of 32 = 4 gates x kUnitGroup = 8 units).
 struct LstmParams {
   const float* bias;            // packed [Np]
   const float* gx;              // optional precomputed input projection (packed columns)
@@ -83,7 +83,6 @@ hipError_t gemm_store(int bf16, int shape, const AOp& a, const BOp& b, const Sto
 hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const LstmParams& p, hipStream_t st);
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st);
 int gen_tile_cols();
-int gemm_tile_cols(int shape);
 
 hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens, int B,
                      int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, hipStream_t st);

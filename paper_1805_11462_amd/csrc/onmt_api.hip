@@ -137,8 +137,10 @@ std::vector<WeightSpec> weight_specs(const onmt_config* c) {
   return v;
 }
 
-// Row of packed gate-blocked matrices for (gate, unit): groups of 16 units hold 4 gates x 16 rows.
-inline int gate_row(int gate, int unit) { return (unit / kUnitGroup) * 64 + gate * kUnitGroup + unit % kUnitGroup; }
+// Row of packed gate-blocked matrices for (gate, unit): groups of kUnitGroup units hold 4 gates x kUnitGroup rows.
+inline int gate_row(int gate, int unit) {
+  return (unit / kUnitGroup) * (4 * kUnitGroup) + gate * kUnitGroup + unit % kUnitGroup;
+}
 
 }  // namespace
 

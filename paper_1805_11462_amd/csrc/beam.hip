@@ -12,81 +12,100 @@ namespace onmt {
 // One wave merges one row's generator partials (per column tile: max, sum of exp, top-K list) into the
 // row's logsumexp and top-K (larger logit first, smaller id on ties).
 //
-// Selection is by rank: an entry's position in the result is the number of entries that come before it,
-// which each lane counts for its own entries independently (no reduction trees). To keep the candidate
-// set small, theta = the K-th largest of the 64 per-lane tile maxima is used as a lower bound on the
-// row's K-th largest logit (those K values are maxima of K distinct tiles), so only list entries
-// >= theta can be in the top-K; they are appended to LDS. If ties at theta produce more survivors than
-// fit, the lane-local lists are merged through the same rank rule over all entries instead.
+// theta = the K-th largest of the 64 per-lane tile maxima is a lower bound on the row's K-th largest
+// logit (those K values are maxima of K distinct tiles), so only tiles whose maximum reaches theta can
+// contribute. Their lists are loaded in one batch (one qualifying tile per lane), the entries >= theta
+// are appended to LDS, and each survivor's position in the result is the number of survivors that come
+// before it, which every lane counts for its own entry independently. Rows with more qualifying tiles
+// or survivors than fit (ties at theta) are merged by the same rank rule over all entries instead.
 constexpr int kMaxTilesPerLane = 16;          // tiles per row <= 64 * 16 (vocabulary <= 131072)
 constexpr int kSurvivorCap = 256;
+constexpr int kQualCap = 256;                 // qualifying tiles listed per row
 
 // Row partials start at pmax/psum + row * ntiles and pval/pid + row * ntiles * K. Lane 0 writes
-// out_val[k] = logit - lse (K entries), out_id[k] and *out_lse. sv/si/cnt: this wave's LDS scratch
-// (kSurvivorCap entries; sv doubles as the 64 lane maxima while theta is found).
+// out_val[k] = logit - lse (K entries), out_id[k] and *out_lse. sv/si/cnt/qt: this wave's LDS scratch
+// (kSurvivorCap survivors, kQualCap qualifying tile ids).
 __device__ __forceinline__ void row_merge_wave(const float* __restrict__ pmax, const float* __restrict__ psum,
                                                const float* __restrict__ pval, const int32_t* __restrict__ pid,
-                                               int ntiles, int K, float* sv, int* si, int* cnt, float* out_val,
-                                               int32_t* out_id, float* out_lse) {
+                                               int ntiles, int K, float* sv, int* si, int* cnt, int* qt,
+                                               float* out_val, int32_t* out_id, float* out_lse) {
   const int lane = threadIdx.x & 63;
   const float ninf = -__builtin_inff();
-  float tm[kMaxTilesPerLane];
-  float mx = ninf;
+  // tile maxima and sums, every load issued before the first use
+  float tm[kMaxTilesPerLane], tq[kMaxTilesPerLane];
 #pragma unroll
   for (int j = 0; j < kMaxTilesPerLane; ++j) {
     const int t = lane + j * kWave;
     tm[j] = t < ntiles ? pmax[t] : ninf;
-    mx = fmaxf(mx, tm[j]);
+    tq[j] = t < ntiles ? psum[t] : 0.f;
   }
-  float sm = 0.f;
+  float mx = ninf;
+#pragma unroll
+  for (int j = 0; j < kMaxTilesPerLane; ++j) mx = fmaxf(mx, tm[j]);
   const float gmx = wave_max(mx);
+  float sm = 0.f;
 #pragma unroll
   for (int j = 0; j < kMaxTilesPerLane; ++j) {
     const int t = lane + j * kWave;
-    if (t < ntiles) sm += psum[t] * __expf(tm[j] - gmx);
+    if (t < ntiles) sm += tq[j] * __expf(tm[j] - gmx);
   }
   const float lse = gmx + __logf(wave_sum(sm));
 
-  // theta: K-th largest lane maximum, by rank among the 64 (lane index breaks ties), broadcast through
-  // the scalar unit
-  int rank = 0;
-  for (int l = 0; l < kWave; ++l) {
-    const float o = readlane_f(mx, l);
-    rank += (o > mx || (o == mx && l < lane)) ? 1 : 0;
+  // theta: K rounds of a wave maximum, each removing the (lowest) lane that holds it
+  float cur = mx, theta = ninf;
+  for (int k = 0; k < K; ++k) {
+    const float m = wave_max(cur);
+    theta = m;
+    const unsigned long long owner = __ballot(cur == m);
+    if (lane == __builtin_ctzll(owner)) cur = ninf;
   }
-  const unsigned long long sel = __ballot(rank == K - 1);
-  const float theta = sel ? readlane_f(mx, __builtin_ctzll(sel)) : ninf;
-  if (lane == 0) *cnt = 0;
-  __builtin_amdgcn_wave_barrier();
 
-  // survivors: entries >= theta of the tiles whose maximum reaches theta; a qualifying tile's list is
-  // loaded whole (no data-dependent exit), so its loads overlap
+  // qualifying tiles (maximum >= theta), listed in LDS in (j, lane) order
+  const unsigned long long below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  int nq = 0;
 #pragma unroll
   for (int j = 0; j < kMaxTilesPerLane; ++j) {
     const int t = lane + j * kWave;
-    if (!(t < ntiles && tm[j] >= theta)) continue;
-    const size_t o = (size_t)t * K;
-    float v[kMaxBeam];
-    int id[kMaxBeam];
-#pragma unroll
-    for (int i = 0; i < kMaxBeam; ++i) {
-      v[i] = i < K ? pval[o + i] : ninf;
-      id[i] = i < K ? pid[o + i] : 0;
+    const bool q = t < ntiles && tm[j] >= theta;
+    const unsigned long long m = __ballot(q);
+    if (q) {
+      const int pos = nq + __popcll(m & below);
+      if (pos < kQualCap) qt[pos] = t;
     }
+    nq += __popcll(m);
+  }
+  if (lane == 0) *cnt = 0;
+  __builtin_amdgcn_wave_barrier();
+
+  // survivors: the lists of the qualifying tiles, one tile per lane, loaded in one batch
+  if (nq <= kQualCap) {
+    for (int q0 = 0; q0 < nq; q0 += kWave) {
+      const int qi = q0 + lane;
+      if (qi < nq) {
+        const size_t o = (size_t)qt[qi] * K;
+        float v[kMaxBeam];
+        int id[kMaxBeam];
 #pragma unroll
-    for (int i = 0; i < kMaxBeam; ++i) {
-      if (i < K && v[i] >= theta) {
-        const int pos = atomicAdd(cnt, 1);
-        if (pos < kSurvivorCap) {
-          sv[pos] = v[i];
-          si[pos] = id[i];
+        for (int i = 0; i < kMaxBeam; ++i) {
+          v[i] = i < K ? pval[o + i] : ninf;
+          id[i] = i < K ? pid[o + i] : 0;
+        }
+#pragma unroll
+        for (int i = 0; i < kMaxBeam; ++i) {
+          if (i < K && v[i] >= theta) {
+            const int pos = atomicAdd(cnt, 1);
+            if (pos < kSurvivorCap) {
+              sv[pos] = v[i];
+              si[pos] = id[i];
+            }
+          }
         }
       }
     }
   }
   __builtin_amdgcn_wave_barrier();
   const int n = *cnt;
-  if (n <= kWave) {
+  if (nq <= kQualCap && n <= kWave) {
     // one survivor per lane, ranked against the others through the scalar unit
     const float v = lane < n ? sv[lane] : ninf;
     const int id = lane < n ? si[lane] : 0x7fffffff;
@@ -96,7 +115,7 @@ __device__ __forceinline__ void row_merge_wave(const float* __restrict__ pmax, c
       out_val[r] = v - lse;
       if (out_id) out_id[r] = id;
     }
-  } else if (n <= kSurvivorCap) {
+  } else if (nq <= kQualCap && n <= kSurvivorCap) {
     for (int c = lane; c < n; c += kWave) {
       const float v = sv[c];
       const int id = si[c];
@@ -135,14 +154,15 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_lse_topk(const float* _
                                                                   float* __restrict__ out_lse) {
   __shared__ float sv[kMergeWaves][kSurvivorCap];
   __shared__ int si[kMergeWaves][kSurvivorCap];
+  __shared__ int qt[kMergeWaves][kQualCap];
   __shared__ int cnt[kMergeWaves];
   const int w = threadIdx.x >> 6;
   const int row = blockIdx.x * kMergeWaves + w;
   if (row >= M) return;
   const size_t base = (size_t)row * ntiles;
-  row_merge_wave(pmax + base, psum + base, pval + base * K, pid + base * K, ntiles, K, sv[w], si[w], &cnt[w],
-                     out_val + (size_t)row * K, out_id ? out_id + (size_t)row * K : nullptr,
-                     out_lse ? out_lse + row : nullptr);
+  row_merge_wave(pmax + base, psum + base, pval + base * K, pid + base * K, ntiles, K, sv[w], si[w], &cnt[w], qt[w],
+                 out_val + (size_t)row * K, out_id ? out_id + (size_t)row * K : nullptr,
+                 out_lse ? out_lse + row : nullptr);
 }
 
 hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pval, const int32_t* pid, int M,
@@ -202,142 +222,134 @@ hipError_t beam_init(const BeamParams& p, int bos, hipStream_t st) {
 }
 
 // One workgroup per sentence, one wave per beam slot. Each live slot's wave first merges its row's
-// generator partials (logsumexp and per-row top-K, as in k_lse_topk). Candidates are then the K per-row
-// top-K entries of every live slot; the sentence's top-K over them (larger fp64 score first, smaller
-// flat index slot*V + token on ties) is selected by rank in wave 0 and walked in rank order by lane 0:
-// EOS (or any choice at the last step) goes to the finished pool, which only keeps its best entry by
-// normalised score, the rest fill live slots.
+// generator partials (logsumexp and per-row top-K, as in k_lse_topk). The sentence's top K of the K x K
+// candidates cand = score_k + logp (fp64; larger first, smaller flat index k*V + w on ties) is then a
+// K-way merge: every row list is in that order already (adding the slot's score keeps it, and equal sums
+// come only from equal log-probs, listed by ascending id), so each round takes the largest list head,
+// the smaller slot winning ties. Lane r of wave 0 ends up holding the rank-r choice, and the lanes write
+// the outcome together: EOS (or any choice at the last step) goes to the finished pool, which keeps only
+// its best entry by normalised score (earlier rank on ties), the others fill the live slots in rank order.
 __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, GenPartials gp, int t, double lp_t) {
   __shared__ float sv[kMaxBeam][kSurvivorCap];
   __shared__ int si[kMaxBeam][kSurvivorCap];
+  __shared__ int qt[kMaxBeam][kQualCap];
   __shared__ int cnt[kMaxBeam];
   __shared__ float tkv[kMaxBeam][kMaxBeam];
   __shared__ int tki[kMaxBeam][kMaxBeam];
-  __shared__ double sel_v[kMaxBeam];
-  __shared__ int sel_slot[kMaxBeam];
-  __shared__ int sel_tok[kMaxBeam];
-  __shared__ float sel_l[kMaxBeam];
-  __shared__ double s_score[kMaxBeam];
-  __shared__ double s_best_norm;
-  __shared__ int s_best_t;
   const int b = blockIdx.x;
   const int w = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   if (p.done[b]) return;
   const int K = p.K;
   const int r0 = b * K;
-  // sentence state, fetched once up front so the serial tail below does not wait on memory
+  const double ninf = -__builtin_inf();
+  // sentence state, fetched up front so that the tail below does not wait on memory
   const double my_score = p.score[r0 + w];
-  if (lane == 0) s_score[w] = my_score;
-  if (threadIdx.x == 0) {
-    s_best_norm = p.best_norm[b];
-    s_best_t = p.best_t[b];
+  double best_norm0 = ninf;
+  int best_t0 = 0;
+  if (w == 0) {
+    best_norm0 = p.best_norm[b];
+    best_t0 = p.best_t[b];
   }
-  if (my_score > -__builtin_inf()) {
+  if (my_score > ninf) {
     const size_t base = (size_t)(r0 + w) * gp.ntiles;
     row_merge_wave(gp.pmax + base, gp.psum + base, gp.pval + base * K, gp.pid + base * K, gp.ntiles, K, sv[w], si[w],
-                   &cnt[w], tkv[w], tki[w], nullptr);
+                   &cnt[w], qt[w], tkv[w], tki[w], nullptr);
   }
   __syncthreads();
   if (w != 0) return;
 
-  // the sentence's top K of the K x K candidates, by rank: lane c holds candidates c + 64 i and counts
-  // the candidates before each of them (broadcast through the scalar unit)
-  const int nc = K * K;
-  constexpr int PER = (kMaxBeam * kMaxBeam) / kWave;
-  double cv[PER];
-  long long cf[PER];
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int c = lane + i * kWave;
-    cv[i] = -__builtin_inf();
-    cf[i] = 0x7fffffffffffffffLL;
-    if (c < nc) {
-      const int k = c / K, j = c % K;
-      const double sc = s_score[k];
-      if (sc > -__builtin_inf()) {
-        cv[i] = sc + (double)tkv[k][j];
-        cf[i] = (long long)k * p.V + tki[k][j];
+  // K-way merge: lane k < K holds slot k's score and the head of its list
+  const double sc = lane < K ? p.score[r0 + lane] : ninf;
+  int h = 0;
+  double my_v = ninf;
+  int my_slot = 0, my_tok = 0;
+  float my_l = 0.f;
+  int nsel = 0;
+  for (int r = 0; r < K; ++r) {
+    const bool has = lane < K && sc > ninf && h < K;
+    const float hv = has ? tkv[lane][h] : 0.f;
+    const int hi = has ? tki[lane][h] : 0;
+    const double cand = has ? sc + (double)hv : ninf;
+    double best = ninf;
+    int bk = -1;
+    for (int k = 0; k < K; ++k) {
+      const double v = readlane_d(cand, k);
+      if (v > best) {            // strict: the smaller slot wins ties
+        best = v;
+        bk = k;
       }
     }
-  }
-  int rk[PER];
-#pragma unroll
-  for (int i = 0; i < PER; ++i) rk[i] = 0;
-#pragma unroll
-  for (int i2 = 0; i2 < PER; ++i2) {
-    const int nd = nc - i2 * kWave < kWave ? nc - i2 * kWave : kWave;    // <= 0: nothing in this set
-    const double mv = cv[i2];
-    const long long mf = cf[i2];
-    for (int d = 0; d < nd; ++d) {
-      const double ov = readlane_d(mv, d);
-      const long long of = readlane_ll(mf, d);
-#pragma unroll
-      for (int i = 0; i < PER; ++i) rk[i] += before(ov, of, cv[i], cf[i]) ? 1 : 0;
+    if (bk < 0) break;           // fewer finite candidates than K
+    const int wt = readlane_i(hi, bk);
+    const float wl = readlane_f(hv, bk);
+    if (lane == r) {
+      my_v = best;
+      my_slot = bk;
+      my_tok = wt;
+      my_l = wl;
     }
+    if (lane == bk) ++h;
+    nsel = r + 1;
   }
-  if (lane < K) sel_v[lane] = -__builtin_inf();
-  __builtin_amdgcn_wave_barrier();
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int c = lane + i * kWave;
-    if (c < nc && cv[i] > -__builtin_inf() && rk[i] < K) {
-      sel_v[rk[i]] = cv[i];
-      sel_slot[rk[i]] = c / K;
-      sel_tok[rk[i]] = tki[c / K][c % K];
-      sel_l[rk[i]] = tkv[c / K][c % K];
-    }
-  }
-  __builtin_amdgcn_wave_barrier();
-  if (lane != 0) return;
 
-  const size_t N = (size_t)p.B * K;
-  int live = 0;
-  double live_max = -__builtin_inf();
-  double best_norm = s_best_norm;
-  int best_t = s_best_t;
-  for (int k = 0; k < K; ++k) {
-    const double v = sel_v[k];
-    if (!(v > -__builtin_inf())) break;                    // fewer finite candidates than K
-    const int slot = sel_slot[k];
-    const int wtok = sel_tok[k];
-    const float lp = sel_l[k];
-  if (p.tr_slot) {
-      const size_t o = ((size_t)(t - 1) * p.B + b) * K + k;
-      p.tr_slot[o] = slot;
-      p.tr_tok[o] = wtok;
-      p.tr_cand[o] = v;
-    }
-    if (wtok == p.eos || t == p.T_max) {
-      const double norm = v / lp_t;
-      if (norm > best_norm) {
-        best_norm = norm;
-        best_t = t;
-        p.best_norm[b] = norm;
-        p.best_raw[b] = v;
-        p.best_t[b] = t;
-        p.best_slot[b] = slot;
-        p.best_tok[b] = wtok;
-        p.best_logp[b] = lp;
-      }
-    } else {
-      const int j = live++;
-      p.score[r0 + j] = v;
-      p.parent[r0 + j] = r0 + slot;
-      p.tok[r0 + j] = wtok;
-      p.bp_slot[(size_t)(t - 1) * N + r0 + j] = slot;
-      p.bp_tok[(size_t)(t - 1) * N + r0 + j] = wtok;
-      p.bp_logp[(size_t)(t - 1) * N + r0 + j] = lp;
-      if (v > live_max) live_max = v;
-    }
+  const bool has = lane < nsel;
+  const bool fin = has && (my_tok == p.eos || t == p.T_max);
+  const bool liv = has && !fin;
+  if (has && p.tr_slot) {
+    const size_t o = ((size_t)(t - 1) * p.B + b) * K + lane;
+    p.tr_slot[o] = my_slot;
+    p.tr_tok[o] = my_tok;
+    p.tr_cand[o] = my_v;
   }
-  for (int j = live; j < K; ++j) {
-    p.score[r0 + j] = -__builtin_inf();
-    p.parent[r0 + j] = r0;
-    p.tok[r0 + j] = p.pad;
+  // live slots in rank order
+  const unsigned long long below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  const unsigned long long lm = __ballot(liv);
+  const int live = __popcll(lm);
+  const size_t N = (size_t)p.B * K;
+  if (liv) {
+    const int j = __popcll(lm & below);
+    p.score[r0 + j] = my_v;
+    p.parent[r0 + j] = r0 + my_slot;
+    p.tok[r0 + j] = my_tok;
+    p.bp_slot[(size_t)(t - 1) * N + r0 + j] = my_slot;
+    p.bp_tok[(size_t)(t - 1) * N + r0 + j] = my_tok;
+    p.bp_logp[(size_t)(t - 1) * N + r0 + j] = my_l;
+  }
+  if (lane >= live && lane < K) {
+    p.score[r0 + lane] = ninf;
+    p.parent[r0 + lane] = r0;
+    p.tok[r0 + lane] = p.pad;
+  }
+  // finished pool: the best new entry by normalised score (earliest rank on ties) replaces the pool's
+  // entry if strictly better
+  const double norm = fin ? my_v / lp_t : ninf;
+  double bn = ninf, live_max = ninf;
+  int bl = -1;
+  for (int k = 0; k < nsel; ++k) {
+    const double nv = readlane_d(norm, k);
+    if (nv > bn) {
+      bn = nv;
+      bl = k;
+    }
+    if ((lm >> k) & 1ull) live_max = fmax(live_max, readlane_d(my_v, k));
+  }
+  double best_norm = best_norm0;
+  int best_t = best_t0;
+  if (bl >= 0 && bn > best_norm0) {
+    best_norm = bn;
+    best_t = t;
+    if (lane == bl) {
+      p.best_norm[b] = bn;
+      p.best_raw[b] = my_v;
+      p.best_t[b] = t;
+      p.best_slot[b] = my_slot;
+      p.best_tok[b] = my_tok;
+      p.best_logp[b] = my_l;
+    }
   }
   const bool stop = (t == p.T_max) || (live == 0) || (best_t > 0 && best_norm >= live_max / p.lp_tmax);
-  if (stop) {
+  if (stop && lane == 0) {
     p.done[b] = 1;
     p.steps[b] = t;
     atomicAdd(p.done_count, 1);

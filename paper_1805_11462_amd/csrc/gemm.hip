@@ -320,10 +320,11 @@ __global__ __launch_bounds__(C::NT) void k_gemm_store(AOp a, BOp b, StoreParams 
   }
 }
 
+// One output tile of an LSTM GEMM (block bid of nblocks) with the gate/cell epilogue.
 template <class T, class C, int NSEG>
-__global__ __launch_bounds__(C::NT) void k_gemm_lstm(AOp a, BOp b, LstmParams p, int nm, int nblocks) {
-  __shared__ __attribute__((aligned(16))) char smem[C::LDS];
-  const int L = xcd_remap(blockIdx.x, nblocks);
+__device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p, int nm, int nblocks, int bid,
+                                 char* smem) {
+  const int L = xcd_remap(bid, nblocks);
   const int m0 = (L % nm) * C::BM, n0 = (L / nm) * C::BN;
   gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
   const float* Ct = (const float*)smem;
@@ -357,6 +358,26 @@ __global__ __launch_bounds__(C::NT) void k_gemm_lstm(AOp a, BOp b, LstmParams p,
     p.h_out[(size_t)row * p.ld_out + unit] = h_new;
     p.c_out[(size_t)row * p.ld_out + unit] = c_new;
     if (p.y_out) p.y_out[(size_t)(row * p.y_S + p.y_s) * p.ld_y + p.y_col0 + unit] = y;
+  }
+}
+
+template <class T, class C, int NSEG>
+__global__ __launch_bounds__(C::NT) void k_gemm_lstm(AOp a, BOp b, LstmParams p, int nm, int nblocks) {
+  __shared__ __attribute__((aligned(16))) char smem[C::LDS];
+  lstm_tile<T, C, NSEG>(a, b, p, nm, nblocks, blockIdx.x, smem);
+}
+
+// Two independent LSTM GEMMs in one launch (the encoder's two directions at one step, or two stacked
+// layers at consecutive timesteps): blocks [0, nb[0]) run problem 0, the next nb[1] blocks problem 1.
+// nb[0] is a multiple of 8, so both problems see the same block-to-XCD dealing.
+template <class T, class C, int NS0, int NS1>
+__global__ __launch_bounds__(C::NT) void k_gemm_lstm2(LstmPair g) {
+  __shared__ __attribute__((aligned(16))) char smem[C::LDS];
+  const int bid = blockIdx.x;
+  if (bid < g.nb[0]) {
+    if (bid < g.nt[0]) lstm_tile<T, C, NS0>(g.a[0], g.b[0], g.p[0], g.nm[0], g.nt[0], bid, smem);
+  } else {
+    lstm_tile<T, C, NS1>(g.a[1], g.b[1], g.p[1], g.nm[1], g.nt[1], bid - g.nb[0], smem);
   }
 }
 
@@ -496,6 +517,21 @@ static hipError_t launch_lstm(const AOp& a, const BOp& b, const LstmParams& p, h
   return hipGetLastError();
 }
 
+template <class T, class C, int NS0, int NS1>
+static hipError_t launch_lstm2(LstmPair g, hipStream_t st) {
+  for (int i = 0; i < 2; ++i) {
+    grid_of<C>(g.a[i], g.b[i], g.nm[i], g.nt[i]);
+    if (!operands_fit<T>(g.a[i], g.b[i])) return hipErrorInvalidValue;
+  }
+  if (g.a[0].nseg != NS0 || g.a[1].nseg != NS1) return hipErrorInvalidValue;
+  g.nb[0] = (g.nt[0] + 7) / 8 * 8;
+  g.nb[1] = g.nt[1];
+  const int nb = g.nb[0] + g.nb[1];
+  if (nb == 0) return hipSuccess;
+  hipLaunchKernelGGL((k_gemm_lstm2<T, C, NS0, NS1>), dim3(nb), dim3(C::NT), 0, st, g);
+  return hipGetLastError();
+}
+
 // The generator's A operand is the attentional vector alone (one segment).
 template <class T, class C>
 static hipError_t launch_gen(const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
@@ -527,6 +563,20 @@ hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const Lstm
   if (shape == kShapeWide) return launch_lstm<float, TileWide32>(a, b, p, st);
   if (shape == kShapeSplitK) return launch_lstm<float, TileSplit32>(a, b, p, st);
   return launch_lstm<float, TileThin32>(a, b, p, st);
+}
+
+template <class T, class C>
+static hipError_t lstm2_dispatch(const LstmPair& g, hipStream_t st) {
+  const int n0 = g.a[0].nseg, n1 = g.a[1].nseg;
+  if (n0 == 1 && n1 == 1) return launch_lstm2<T, C, 1, 1>(g, st);
+  if (n0 == 1 && n1 == 2) return launch_lstm2<T, C, 1, 2>(g, st);
+  if (n0 == 2 && n1 == 2) return launch_lstm2<T, C, 2, 2>(g, st);
+  return hipErrorInvalidValue;
+}
+
+hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st) {
+  if (shape != kShapeSplitKThin) return hipErrorInvalidValue;
+  return bf16 ? lstm2_dispatch<__bf16, TileThin16>(g, st) : lstm2_dispatch<float, TileThin32>(g, st);
 }
 
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {

@@ -63,6 +63,16 @@ struct LstmParams {
   int H;                        // real units
 };
 
+// Two LSTM GEMM problems for one launch (nm/nt/nb are filled in by the launcher).
+struct LstmPair {
+  AOp a[2];
+  BOp b[2];
+  LstmParams p[2];
+  int nm[2];     // row tiles
+  int nt[2];     // tiles
+  int nb[2];     // blocks (problem 0's rounded up to a multiple of 8)
+};
+
 // Generator epilogue: per (row, column tile) max, sum of exp and top-K; optional raw logits.
 struct GenParams {
   const float* bias;
@@ -81,6 +91,8 @@ enum GemmShape { kShapeWide = 0, kShapeSplitK = 1, kShapeSplitKThin = 2 };
 
 hipError_t gemm_store(int bf16, int shape, const AOp& a, const BOp& b, const StoreParams& p, hipStream_t st);
 hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const LstmParams& p, hipStream_t st);
+// Two independent thin-shape LSTM GEMMs in one launch (segment counts 1+1, 1+2 or 2+2).
+hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st);
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st);
 int gen_tile_cols();
 

@@ -150,9 +150,13 @@ struct onmt_model {
   char* dev = nullptr;
   const void* E_src = nullptr;
   const void* E_tgt = nullptr;
+  // Encoder. Bidirectional: every layer has an input projection (both directions stacked) and a recurrent
+  // matrix per direction. Unidirectional: layer 0 likewise; layers >= 1 keep [input | recurrent] in one
+  // matrix, so that they can run one timestep behind the layer below in the same launch.
   std::vector<Packed> enc_x;               // per layer: both directions stacked [ndir * 4 Hd_pad, pad(in)]
   std::vector<const float*> enc_bias;      // per layer [ndir * 4 Hd_pad]
   std::vector<Packed> enc_h;               // per layer * ndir: [4 Hd_pad, pad(Hd)]
+  std::vector<Packed> enc_xh;              // unidirectional layers >= 1: [4 Hd_pad, pad(in) + pad(Hd)]
   std::vector<Packed> dec_w;               // per layer [4 H_pad, sum of padded segment widths]
   std::vector<const float*> dec_bias;      // per layer [4 H_pad]
   Packed W_a, W_c, W_s;
@@ -190,13 +194,20 @@ size_t model_layout(const onmt_config* c, onmt_model* m) {
     return o;
   };
   Packed esrc = mat(d.Vs, d.E);
-  std::vector<Packed> ex, eh, dw;
+  std::vector<Packed> ex, eh, exh, dw;
   std::vector<size_t> eb, db;
   for (int l = 0; l < d.L; ++l) {
     const int in = l == 0 ? d.E : d.Hm;
-    ex.push_back(mat(d.ndir * 4 * d.Hd_pad, d.pad(in)));
+    if (d.ndir == 1 && l > 0) {
+      ex.push_back(Packed{});
+      eh.push_back(Packed{});
+      exh.push_back(mat(4 * d.Hd_pad, d.pad(in) + d.pad(d.Hd)));
+    } else {
+      ex.push_back(mat(d.ndir * 4 * d.Hd_pad, d.pad(in)));
+      for (int dir = 0; dir < d.ndir; ++dir) eh.push_back(mat(4 * d.Hd_pad, d.pad(d.Hd)));
+      exh.push_back(Packed{});
+    }
     eb.push_back(vec((size_t)d.ndir * 4 * d.Hd_pad));
-    for (int dir = 0; dir < d.ndir; ++dir) eh.push_back(mat(4 * d.Hd_pad, d.pad(d.Hd)));
   }
   Packed etgt = mat(d.Vt, d.E);
   for (int l = 0; l < d.L; ++l) {
@@ -220,6 +231,7 @@ size_t model_layout(const onmt_config* c, onmt_model* m) {
     for (auto& p : ex) m->enc_x.push_back(fix(p));
     for (auto o : eb) m->enc_bias.push_back((const float*)(base + o));
     for (auto& p : eh) m->enc_h.push_back(fix(p));
+    for (auto& p : exh) m->enc_xh.push_back(fix(p));
     for (auto& p : dw) m->dec_w.push_back(fix(p));
     for (auto o : db) m->dec_bias.push_back((const float*)(base + o));
     m->W_a = fix(wa);
@@ -312,18 +324,22 @@ int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, 
   }
   for (int l = 0; l < d.L; ++l) {
     const int in = l == 0 ? d.E : d.Hm;
-    const Packed& X = m->enc_x[l];
     const size_t bo = off_of(m->enc_bias[l]);
+    const bool joint = d.ndir == 1 && l > 0;
     for (int dir = 0; dir < d.ndir; ++dir) {
       const float* W = host_weights[wi++];
       const float* bvec = host_weights[wi++];
-      const Packed& Hh = m->enc_h[l * d.ndir + dir];
       for (int g = 0; g < 4; ++g)
         for (int u = 0; u < d.Hd; ++u) {
           const float* row = W + (size_t)(g * d.Hd + u) * (in + d.Hd);
           const int xr = dir * 4 * d.Hd_pad + gate_row(g, u);
-          pack_row(img, X, xr, 0, row, 0, in);
-          pack_row(img, Hh, gate_row(g, u), 0, row, in, d.Hd);
+          if (joint) {   // segments [layer below | recurrent]
+            pack_row(img, m->enc_xh[l], xr, 0, row, 0, in);
+            pack_row(img, m->enc_xh[l], xr, d.pad(in), row, in, d.Hd);
+          } else {
+            pack_row(img, m->enc_x[l], xr, 0, row, 0, in);
+            pack_row(img, m->enc_h[l * d.ndir + dir], gate_row(g, u), 0, row, in, d.Hd);
+          }
           img.putf(bo, xr, bvec[g * d.Hd + u]);
         }
     }
@@ -401,8 +417,9 @@ struct EncWs {
   float* final_c;
   float* gx;         // [B*S, ndir * 4 Hd_pad]
   float* y[2];       // [B*S, Hm]
-  float* hs[2];      // [ndir, B, Hd]
+  float* hs[2];      // [max(ndir, L), B, Hd]: state after an even / odd timestep, one slot per direction or layer
   float* cs[2];
+  int32_t* rowmap;   // [S, B]: rowmap[s * B + b] = b * S + s (row of position s of sentence b)
 };
 
 size_t enc_layout(const Dims& d, int B, int S, char* base, EncWs* w) {
@@ -418,8 +435,10 @@ size_t enc_layout(const Dims& d, int B, int S, char* base, EncWs* w) {
   t.final_c = c.take<float>((size_t)d.L * B * d.H);
   t.gx = c.take<float>(BS * d.ndir * 4 * d.Hd_pad);
   for (int i = 0; i < 2; ++i) t.y[i] = c.take<float>(BS * d.Hm);
-  for (int i = 0; i < 2; ++i) t.hs[i] = c.take<float>((size_t)d.ndir * B * d.Hd);
-  for (int i = 0; i < 2; ++i) t.cs[i] = c.take<float>((size_t)d.ndir * B * d.Hd);
+  const size_t slots = (size_t)(d.ndir > d.L ? d.ndir : d.L);
+  for (int i = 0; i < 2; ++i) t.hs[i] = c.take<float>(slots * B * d.Hd);
+  for (int i = 0; i < 2; ++i) t.cs[i] = c.take<float>(slots * B * d.Hd);
+  t.rowmap = c.take<int32_t>(BS);
   if (w) *w = t;
   return align_up(c.off);
 }
@@ -550,7 +569,7 @@ int small_shape(int M, int Np) {
 // its sentence's length replaced by 0 into clean_src (device, [B, S]), so no kernel gathers an embedding
 // row through an unchecked id.
 int check_len_src(const onmt_model* m, const int32_t* src, const int32_t* len, int B, int S, hipStream_t st,
-                  int* max_len, int32_t* clean_src) {
+                  int* max_len, int32_t* clean_src, int32_t* rowmap) {
   if (!src || !len) return fail(ONMT_EINVAL, "src/len is NULL");
   if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
   if ((long long)B * S > (1LL << 28)) return fail(ONMT_EUNSUPPORTED, "B * S_max too large");
@@ -570,6 +589,10 @@ int check_len_src(const onmt_model* m, const int32_t* src, const int32_t* len, i
   for (int b = 0; b < B; ++b)
     for (int s = hl[b]; s < S; ++s) hs[(size_t)b * S + s] = 0;
   HIP_TRY(hipMemcpyAsync(clean_src, hs.data(), sizeof(int32_t) * hs.size(), hipMemcpyHostToDevice, st));
+  std::vector<int32_t> rm((size_t)B * S);
+  for (int s = 0; s < S; ++s)
+    for (int b = 0; b < B; ++b) rm[(size_t)s * B + b] = b * S + s;
+  HIP_TRY(hipMemcpyAsync(rowmap, rm.data(), sizeof(int32_t) * rm.size(), hipMemcpyHostToDevice, st));
   HIP_TRY(hipStreamSynchronize(st));
   *max_len = mx;
   return ONMT_OK;
@@ -584,8 +607,67 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
   HIP_TRY(hipMemcpyAsync(w.lens, len, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, st));
   HIP_TRY(fill_f32(w.memory, (size_t)BS * d.Hm, 0.f, st));
   const int gxw = d.ndir * 4 * d.Hd_pad;
-  for (int l = 0; l < d.L; ++l) {
-    // input projection for every position and both directions at once
+  const size_t SB = (size_t)B * d.Hd;       // one state slot
+  // Recurrent GEMM of (layer l, direction dir) at position s, its step-th step, state slot `slot`: the
+  // state after step k goes to buffer k & 1 and step k reads the other buffer (buffer 1 holds the zero
+  // state before step 0).
+  auto recurrent = [&](int l, int dir, int s, int step, int slot, AOp& r, BOp& wb, LstmParams& lp) {
+    const int pin = (step + 1) & 1;
+    const float* hp = w.hs[pin] + slot * SB;
+    const float* cp = w.cs[pin] + slot * SB;
+    const bool joint = d.ndir == 1 && l > 0;
+    r = AOp{};
+    r.M = B;
+    if (joint) {   // [output of layer l-1 at position s | h]
+      r.nseg = 2;
+      r.seg[0] = seg(w.y[(l - 1) & 1], w.rowmap + (size_t)s * B, BS, d.Hm, d.Hm, d.pad(d.Hm), 0);
+      r.seg[1] = seg(hp, nullptr, B, d.Hd, d.Hd, d.pad(d.Hd), 0);
+      wb = bop(m->enc_xh[l]);
+    } else {       // h, plus the precomputed input projection
+      r.nseg = 1;
+      r.seg[0] = seg(hp, nullptr, B, d.Hd, d.Hd, d.pad(d.Hd), 0);
+      wb = bop(m->enc_h[l * d.ndir + dir]);
+    }
+    lp = LstmParams{};
+    lp.bias = joint ? m->enc_bias[l] : nullptr;
+    lp.gx = joint ? nullptr : w.gx;
+    lp.ld_gx = gxw;
+    lp.gx_col0 = dir * 4 * d.Hd_pad;
+    lp.gx_S = S;
+    lp.gx_s = s;
+    lp.c_in = cp;
+    lp.c_idx = nullptr;
+    lp.ld_c = d.Hd;
+    lp.h_in = hp;
+    lp.ld_h_in = d.Hd;
+    lp.h_out = w.hs[pin ^ 1] + slot * SB;
+    lp.c_out = w.cs[pin ^ 1] + slot * SB;
+    lp.ld_out = d.Hd;
+    lp.y_out = (l == d.L - 1) ? w.memory : w.y[l & 1];
+    lp.ld_y = d.Hm;
+    lp.y_S = S;
+    lp.y_s = s;
+    lp.y_col0 = dir * d.Hd;
+    lp.lens = w.lens;
+    lp.H = d.Hd;
+  };
+  auto run_one = [&](int l, int dir, int s, int step, int slot) -> int {
+    AOp r;
+    BOp wb;
+    LstmParams lp;
+    recurrent(l, dir, s, step, slot, r, wb, lp);
+    HIP_TRY(gemm_lstm(d.bf16, small_shape(B, wb.Np), r, wb, lp, st));
+    return ONMT_OK;
+  };
+  auto run_two = [&](int l0, int dir0, int s0, int step0, int slot0, int l1, int dir1, int s1, int step1,
+                     int slot1) -> int {
+    LstmPair g{};
+    recurrent(l0, dir0, s0, step0, slot0, g.a[0], g.b[0], g.p[0]);
+    recurrent(l1, dir1, s1, step1, slot1, g.a[1], g.b[1], g.p[1]);
+    HIP_TRY(gemm_lstm2(d.bf16, kShapeSplitKThin, g, st));
+    return ONMT_OK;
+  };
+  auto project = [&](int l) -> int {   // input projection of every position, both directions at once
     AOp a{};
     a.M = BS;
     a.nseg = 1;
@@ -593,51 +675,44 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
     else a.seg[0] = seg(w.y[(l - 1) & 1], nullptr, BS, d.Hm, d.Hm, d.pad(d.Hm), 0);
     StoreParams sp{m->enc_bias[l], w.gx, gxw, gxw, 0};
     HIP_TRY(gemm_store(d.bf16, kShapeWide, a, bop(m->enc_x[l]), sp, st));
-    HIP_TRY(fill_f32(w.hs[0], (size_t)d.ndir * B * d.Hd, 0.f, st));
-    HIP_TRY(fill_f32(w.cs[0], (size_t)d.ndir * B * d.Hd, 0.f, st));
-    float* yout = (l == d.L - 1) ? w.memory : w.y[l & 1];
-    int cur = 0;
-    for (int step = 0; step < max_len; ++step) {
-      for (int dir = 0; dir < d.ndir; ++dir) {
-        const int s = dir == 0 ? step : max_len - 1 - step;
-        const float* hp = w.hs[cur] + (size_t)dir * B * d.Hd;
-        const float* cp = w.cs[cur] + (size_t)dir * B * d.Hd;
-        AOp r{};
-        r.M = B;
-        r.nseg = 1;
-        r.seg[0] = seg(hp, nullptr, B, d.Hd, d.Hd, d.pad(d.Hd), 0);
-        LstmParams lp{};
-        lp.bias = nullptr;
-        lp.gx = w.gx;
-        lp.ld_gx = gxw;
-        lp.gx_col0 = dir * 4 * d.Hd_pad;
-        lp.gx_S = S;
-        lp.gx_s = s;
-        lp.c_in = cp;
-        lp.c_idx = nullptr;
-        lp.ld_c = d.Hd;
-        lp.h_in = hp;
-        lp.ld_h_in = d.Hd;
-        lp.h_out = w.hs[cur ^ 1] + (size_t)dir * B * d.Hd;
-        lp.c_out = w.cs[cur ^ 1] + (size_t)dir * B * d.Hd;
-        lp.ld_out = d.Hd;
-        lp.y_out = yout;
-        lp.ld_y = d.Hm;
-        lp.y_S = S;
-        lp.y_s = s;
-        lp.y_col0 = dir * d.Hd;
-        lp.lens = w.lens;
-        lp.H = d.Hd;
-        const Packed& Wh = m->enc_h[l * d.ndir + dir];
-        HIP_TRY(gemm_lstm(d.bf16, small_shape(B, Wh.Np), r, bop(Wh), lp, st));
+    return ONMT_OK;
+  };
+  const int slots = d.ndir > d.L ? d.ndir : d.L;
+  HIP_TRY(fill_f32(w.hs[1], (size_t)slots * SB, 0.f, st));
+  HIP_TRY(fill_f32(w.cs[1], (size_t)slots * SB, 0.f, st));
+  const int last = (max_len - 1) & 1;      // buffer holding the state after the last step
+  int rc = ONMT_OK;
+  if (d.ndir == 1) {
+    // layer l processes position s = wave - l: each layer runs one step behind the layer below, and the
+    // layers of one wave go out two per launch
+    if ((rc = project(0))) return rc;
+    for (int wave = 0; wave < max_len + d.L - 1; ++wave) {
+      const int lo = wave - max_len + 1 > 0 ? wave - max_len + 1 : 0;
+      const int hi = wave < d.L - 1 ? wave : d.L - 1;
+      for (int l = lo; l <= hi; l += 2) {
+        const int t0 = wave - l, t1 = wave - l - 1;   // position = step for a forward layer
+        rc = l + 1 <= hi ? run_two(l, 0, t0, t0, l, l + 1, 0, t1, t1, l + 1) : run_one(l, 0, t0, t0, l);
+        if (rc) return rc;
       }
-      cur ^= 1;
     }
-    for (int dir = 0; dir < d.ndir; ++dir) {
-      HIP_TRY(copy_cols(w.hs[cur] + (size_t)dir * B * d.Hd, d.Hd, w.final_h + (size_t)l * B * d.H + dir * d.Hd, d.H, B,
-                        d.Hd, st));
-      HIP_TRY(copy_cols(w.cs[cur] + (size_t)dir * B * d.Hd, d.Hd, w.final_c + (size_t)l * B * d.H + dir * d.Hd, d.H, B,
-                        d.Hd, st));
+    for (int l = 0; l < d.L; ++l) {
+      HIP_TRY(copy_cols(w.hs[last] + l * SB, d.Hd, w.final_h + (size_t)l * B * d.H, d.H, B, d.Hd, st));
+      HIP_TRY(copy_cols(w.cs[last] + l * SB, d.Hd, w.final_c + (size_t)l * B * d.H, d.H, B, d.Hd, st));
+    }
+  } else {
+    // both directions of a layer step together, one launch per step
+    for (int l = 0; l < d.L; ++l) {
+      if ((rc = project(l))) return rc;
+      if (l > 0) {
+        HIP_TRY(fill_f32(w.hs[1], (size_t)slots * SB, 0.f, st));
+        HIP_TRY(fill_f32(w.cs[1], (size_t)slots * SB, 0.f, st));
+      }
+      for (int step = 0; step < max_len; ++step)
+        if ((rc = run_two(l, 0, step, step, 0, l, 1, max_len - 1 - step, step, 1))) return rc;
+      for (int dir = 0; dir < d.ndir; ++dir) {
+        HIP_TRY(copy_cols(w.hs[last] + dir * SB, d.Hd, w.final_h + (size_t)l * B * d.H + dir * d.Hd, d.H, B, d.Hd, st));
+        HIP_TRY(copy_cols(w.cs[last] + dir * SB, d.Hd, w.final_c + (size_t)l * B * d.H + dir * d.Hd, d.H, B, d.Hd, st));
+      }
     }
   }
   // attention keys W_a m_s, once per batch
@@ -793,7 +868,7 @@ int onmt_encode(onmt_model* m, const int32_t* src, const int32_t* len, int B, in
   EncWs w;
   enc_layout(m->d, B, S, (char*)ws, &w);
   int mx = 0;
-  int rc = check_len_src(m, src, len, B, S, st, &mx, w.src);
+  int rc = check_len_src(m, src, len, B, S, st, &mx, w.src, w.rowmap);
   if (rc) return rc;
   return encode_compute(m, src, len, B, S, mx, w, st);
 }
@@ -877,7 +952,7 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   SearchWs w;
   search_layout(m->d, B, S, K, T, (char*)ws, &w);
   int mx = 0;
-  rc = check_len_src(m, src, len, B, S, st, &mx, w.enc.src);
+  rc = check_len_src(m, src, len, B, S, st, &mx, w.enc.src, w.enc.rowmap);
   if (rc) return rc;
 
   BeamParams bp = w.bp;

@@ -363,38 +363,70 @@ hipError_t beam_step(const BeamParams& p, const GenPartials& gp, int t, hipStrea
   return hipGetLastError();
 }
 
-// One thread per sentence: follow back-pointers from the best finished hypothesis.
-__global__ void k_backtrack(BeamParams p, int32_t* out_tok, int32_t* out_len, double* out_raw, double* out_norm,
-                            float* out_tok_logp) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= p.B) return;
+// One workgroup per sentence: the sentence's back-pointer slots are staged in LDS (coalesced loads,
+// kBtChunk steps at a time, from the finish step backwards), then one lane follows them from the best
+// finished hypothesis; tokens and log-probs are gathered by all lanes once the slot path is known.
+constexpr int kBtThreads = 256;
+constexpr int kBtChunk = 256;      // steps staged per round
+
+__global__ __launch_bounds__(kBtThreads) void k_backtrack(BeamParams p, int32_t* out_tok, int32_t* out_len,
+                                                          double* out_raw, double* out_norm, float* out_tok_logp) {
+  __shared__ int8_t slots[kBtChunk * kMaxBeam];   // slot (< 16) of each (step, rank) in the current chunk
+  __shared__ int8_t path[kBtChunk];               // rank of the path's entry at each step of the chunk
+  __shared__ int s_slot;
+  const int b = blockIdx.x;
   const int K = p.K;
   const size_t N = (size_t)p.B * K;
   const int tb = p.best_t[b];
   int32_t* tok = out_tok + (size_t)b * p.T_max;
   float* lp = out_tok_logp ? out_tok_logp + (size_t)b * p.T_max : nullptr;
-  for (int i = tb; i < p.T_max; ++i) {
+  for (int i = tb + threadIdx.x; i < p.T_max; i += kBtThreads) {
     tok[i] = p.pad;
     if (lp) lp[i] = 0.f;
   }
-  out_len[b] = tb;
-  out_raw[b] = p.best_raw[b];
-  out_norm[b] = p.best_norm[b];
+  if (threadIdx.x == 0) {
+    out_len[b] = tb;
+    out_raw[b] = p.best_raw[b];
+    out_norm[b] = p.best_norm[b];
+    s_slot = p.best_slot[b];
+  }
   if (tb == 0) return;
-  tok[tb - 1] = p.best_tok[b];
-  if (lp) lp[tb - 1] = p.best_logp[b];
-  int slot = p.best_slot[b];
-  for (int tt = tb - 1; tt >= 1; --tt) {
-    const size_t o = (size_t)(tt - 1) * N + (size_t)b * K + slot;
-    tok[tt - 1] = p.bp_tok[o];
-    if (lp) lp[tt - 1] = p.bp_logp[o];
-    slot = p.bp_slot[o];
+  if (threadIdx.x == 0) {
+    tok[tb - 1] = p.best_tok[b];
+    if (lp) lp[tb - 1] = p.best_logp[b];
+  }
+  // entries at steps tt = tb-1 .. 1 (1-based step tt is stored at row tt - 1), walked downwards in chunks
+  for (int hi = tb - 1; hi >= 1; hi -= kBtChunk) {
+    const int lo = hi - kBtChunk + 1 > 1 ? hi - kBtChunk + 1 : 1;
+    const int n = hi - lo + 1;
+    __syncthreads();
+    for (int e = threadIdx.x; e < n * K; e += kBtThreads) {
+      const int i = e / K, k = e % K;
+      slots[i * kMaxBeam + k] = (int8_t)p.bp_slot[(size_t)(lo + i - 1) * N + (size_t)b * K + k];
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int slot = s_slot;
+      for (int tt = hi; tt >= lo; --tt) {
+        path[tt - lo] = (int8_t)slot;
+        slot = slots[(tt - lo) * kMaxBeam + slot];
+      }
+      s_slot = slot;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += kBtThreads) {
+      const int tt = lo + i;
+      const size_t o = (size_t)(tt - 1) * N + (size_t)b * K + path[i];
+      tok[tt - 1] = p.bp_tok[o];
+      if (lp) lp[tt - 1] = p.bp_logp[o];
+    }
   }
 }
 
 hipError_t backtrack(const BeamParams& p, int32_t* out_tok, int32_t* out_len, double* out_raw, double* out_norm,
                      float* out_tok_logp, hipStream_t st) {
-  hipLaunchKernelGGL(k_backtrack, dim3((p.B + 63) / 64), dim3(64), 0, st, p, out_tok, out_len, out_raw, out_norm,
+  if (p.K > kMaxBeam) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_backtrack, dim3(p.B), dim3(kBtThreads), 0, st, p, out_tok, out_len, out_raw, out_norm,
                      out_tok_logp);
   return hipGetLastError();
 }

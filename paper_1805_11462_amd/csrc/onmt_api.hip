@@ -560,6 +560,9 @@ BOp bop(const Packed& p) {
 #ifndef ONMT_SMALL_M_TILES
 #define ONMT_SMALL_M_TILES 4096
 #endif
+// Unidirectional encoders with fewer rows than this run their layers as a wavefront (see encode_compute).
+constexpr int kWavefrontMaxRows = 256;
+
 int small_shape(int M, int Np) {
   const long tiles32 = (long)((M + 31) / 32) * (Np / 64);
   return tiles32 >= ONMT_SMALL_M_TILES ? kShapeSplitK : kShapeSplitKThin;
@@ -611,11 +614,13 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
   // Recurrent GEMM of (layer l, direction dir) at position s, its step-th step, state slot `slot`: the
   // state after step k goes to buffer k & 1 and step k reads the other buffer (buffer 1 holds the zero
   // state before step 0).
-  auto recurrent = [&](int l, int dir, int s, int step, int slot, AOp& r, BOp& wb, LstmParams& lp) {
+  // Unidirectional layers >= 1 keep [W_x | W_h] in one matrix: `joint` steps read [y_{l-1} at s | h]
+  // against all of it; otherwise the step reads h against the W_h columns and adds the projection gx.
+  const bool uni = d.ndir == 1;
+  auto recurrent = [&](int l, int dir, int s, int step, int slot, bool joint, AOp& r, BOp& wb, LstmParams& lp) {
     const int pin = (step + 1) & 1;
     const float* hp = w.hs[pin] + slot * SB;
     const float* cp = w.cs[pin] + slot * SB;
-    const bool joint = d.ndir == 1 && l > 0;
     r = AOp{};
     r.M = B;
     if (joint) {   // [output of layer l-1 at position s | h]
@@ -626,7 +631,12 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
     } else {       // h, plus the precomputed input projection
       r.nseg = 1;
       r.seg[0] = seg(hp, nullptr, B, d.Hd, d.Hd, d.pad(d.Hd), 0);
-      wb = bop(m->enc_h[l * d.ndir + dir]);
+      if (uni && l > 0) {   // the W_h columns of the joint matrix (row stride unchanged)
+        wb = bop(m->enc_xh[l]);
+        wb.W = (const char*)wb.W + (size_t)d.pad(d.Hm) * d.esz;
+      } else {
+        wb = bop(m->enc_h[l * d.ndir + dir]);
+      }
     }
     lp = LstmParams{};
     lp.bias = joint ? m->enc_bias[l] : nullptr;
@@ -651,19 +661,19 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
     lp.lens = w.lens;
     lp.H = d.Hd;
   };
-  auto run_one = [&](int l, int dir, int s, int step, int slot) -> int {
+  auto run_one = [&](int l, int dir, int s, int step, int slot, bool joint) -> int {
     AOp r;
     BOp wb;
     LstmParams lp;
-    recurrent(l, dir, s, step, slot, r, wb, lp);
+    recurrent(l, dir, s, step, slot, joint, r, wb, lp);
     HIP_TRY(gemm_lstm(d.bf16, small_shape(B, wb.Np), r, wb, lp, st));
     return ONMT_OK;
   };
-  auto run_two = [&](int l0, int dir0, int s0, int step0, int slot0, int l1, int dir1, int s1, int step1,
-                     int slot1) -> int {
+  auto run_two = [&](int l0, int dir0, int s0, int step0, int slot0, bool joint0, int l1, int dir1, int s1,
+                     int step1, int slot1, bool joint1) -> int {
     LstmPair g{};
-    recurrent(l0, dir0, s0, step0, slot0, g.a[0], g.b[0], g.p[0]);
-    recurrent(l1, dir1, s1, step1, slot1, g.a[1], g.b[1], g.p[1]);
+    recurrent(l0, dir0, s0, step0, slot0, joint0, g.a[0], g.b[0], g.p[0]);
+    recurrent(l1, dir1, s1, step1, slot1, joint1, g.a[1], g.b[1], g.p[1]);
     HIP_TRY(gemm_lstm2(d.bf16, kShapeSplitKThin, g, st));
     return ONMT_OK;
   };
@@ -674,7 +684,8 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
     if (l == 0) a.seg[0] = seg(m->E_src, w.src, d.Vs, d.E, d.E, d.pad(d.E), d.bf16);
     else a.seg[0] = seg(w.y[(l - 1) & 1], nullptr, BS, d.Hm, d.Hm, d.pad(d.Hm), 0);
     StoreParams sp{m->enc_bias[l], w.gx, gxw, gxw, 0};
-    HIP_TRY(gemm_store(d.bf16, kShapeWide, a, bop(m->enc_x[l]), sp, st));
+    // unidirectional layers >= 1: the W_x columns of the joint matrix (the product reads only pad(Hm))
+    HIP_TRY(gemm_store(d.bf16, kShapeWide, a, bop(uni && l > 0 ? m->enc_xh[l] : m->enc_x[l]), sp, st));
     return ONMT_OK;
   };
   const int slots = d.ndir > d.L ? d.ndir : d.L;
@@ -682,18 +693,31 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
   HIP_TRY(fill_f32(w.cs[1], (size_t)slots * SB, 0.f, st));
   const int last = (max_len - 1) & 1;      // buffer holding the state after the last step
   int rc = ONMT_OK;
-  if (d.ndir == 1) {
-    // layer l processes position s = wave - l: each layer runs one step behind the layer below, and the
-    // layers of one wave go out two per launch
+  if (uni && B < kWavefrontMaxRows) {
+    // few rows per step (launch-bound): layer l processes position s = wave - l, one step behind the
+    // layer below, and the layers of one wave go out two per launch
     if ((rc = project(0))) return rc;
     for (int wave = 0; wave < max_len + d.L - 1; ++wave) {
       const int lo = wave - max_len + 1 > 0 ? wave - max_len + 1 : 0;
       const int hi = wave < d.L - 1 ? wave : d.L - 1;
       for (int l = lo; l <= hi; l += 2) {
         const int t0 = wave - l, t1 = wave - l - 1;   // position = step for a forward layer
-        rc = l + 1 <= hi ? run_two(l, 0, t0, t0, l, l + 1, 0, t1, t1, l + 1) : run_one(l, 0, t0, t0, l);
+        rc = l + 1 <= hi ? run_two(l, 0, t0, t0, l, l > 0, l + 1, 0, t1, t1, l + 1, true)
+                         : run_one(l, 0, t0, t0, l, l > 0);
         if (rc) return rc;
       }
+    }
+    for (int l = 0; l < d.L; ++l) {
+      HIP_TRY(copy_cols(w.hs[last] + l * SB, d.Hd, w.final_h + (size_t)l * B * d.H, d.H, B, d.Hd, st));
+      HIP_TRY(copy_cols(w.cs[last] + l * SB, d.Hd, w.final_c + (size_t)l * B * d.H, d.H, B, d.Hd, st));
+    }
+  } else if (uni) {
+    // many rows per step (compute-bound): layer by layer, each with its input projection of every
+    // position done as one large GEMM first
+    for (int l = 0; l < d.L; ++l) {
+      if ((rc = project(l))) return rc;
+      for (int step = 0; step < max_len; ++step)
+        if ((rc = run_one(l, 0, step, step, l, false))) return rc;
     }
     for (int l = 0; l < d.L; ++l) {
       HIP_TRY(copy_cols(w.hs[last] + l * SB, d.Hd, w.final_h + (size_t)l * B * d.H, d.H, B, d.Hd, st));
@@ -708,7 +732,7 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
         HIP_TRY(fill_f32(w.cs[1], (size_t)slots * SB, 0.f, st));
       }
       for (int step = 0; step < max_len; ++step)
-        if ((rc = run_two(l, 0, step, step, 0, l, 1, max_len - 1 - step, step, 1))) return rc;
+        if ((rc = run_two(l, 0, step, step, 0, false, l, 1, max_len - 1 - step, step, 1, false))) return rc;
       for (int dir = 0; dir < d.ndir; ++dir) {
         HIP_TRY(copy_cols(w.hs[last] + dir * SB, d.Hd, w.final_h + (size_t)l * B * d.H + dir * d.Hd, d.H, B, d.Hd, st));
         HIP_TRY(copy_cols(w.cs[last] + dir * SB, d.Hd, w.final_c + (size_t)l * B * d.H + dir * d.Hd, d.H, B, d.Hd, st));

@@ -33,6 +33,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="default")
+    ap.add_argument("--mode", choices=["search", "score"], default="search",
+                    help="search: beam search (the headline metric); score: teacher-forced scoring of "
+                         "max-decode-long synthetic targets")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sentences", type=int, default=4)
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -69,15 +72,19 @@ def traffic_from_counters(per_launch_flops_key):
     return c.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, weights, src, lens, n_sent):
-    """The oracle (fp64 NumPy) on the first n_sent sentences of the same batch, on this host's cores."""
-    import numpy as np
-    from oracle import onmt_oracle as O
+def cpu_threads():
+    """Threads the oracle's BLAS actually uses on this host."""
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        return int(max([p.get("num_threads", 1) for p in threadpool_info()] or [1]))
     except Exception:
-        threads = len(os.sched_getaffinity(0))
+        return len(os.sched_getaffinity(0))
+
+
+def cpu_baseline(w, weights, src, lens, n_sent):
+    """The oracle (fp64 NumPy) on the first n_sent sentences of the same batch, on this host's cores."""
+    from oracle import onmt_oracle as O
+    threads = cpu_threads()
     m = O.model_from(w, weights)
     t0 = time.perf_counter()
     res = O.beam_search(m, src[:n_sent], lens[:n_sent], w.beam, w.max_len, w.alpha)
@@ -112,6 +119,8 @@ def main():
     tr = Translator(cfg, [weights[n] for n, _ in W.weight_specs(w)], device="cuda:0")
     src_d = torch.from_numpy(src).cuda()
     lens_d = torch.from_numpy(lens).cuda()
+    if args.mode == "score":
+        return bench_score(args, w, weights, tr, src, lens, src_d, lens_d)
     buf = tr.search_buffers(B, S, w.beam, w.max_len, w.alpha)
 
     for i in range(args.warmup):
@@ -172,6 +181,61 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, weights, src, lens, args.cpu_sentences)
+    print(json.dumps(out), flush=True)
+
+
+def bench_score(args, w, weights, tr, src, lens, src_d, lens_d):
+    """Teacher-forced scoring throughput: scored target tokens per second (same timing rules)."""
+    import torch
+    import workloads as W
+
+    B, S = src.shape
+    tgt, tgt_len = W.make_targets(w)
+    T = tgt.shape[1]
+    tgt_d = torch.from_numpy(tgt).cuda()
+    tlen_d = torch.from_numpy(tgt_len).cuda()
+    buf = tr.score_buffers(B, S, T)
+    for i in range(args.warmup):
+        tr.score(src_d, lens_d, tgt_d, tlen_d, buf)
+    torch.cuda.synchronize()
+    tr.profile(GEN_TIMING_PERIOD)
+    tr.profile_read(reset=True)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        tr.score(src_d, lens_d, tgt_d, tlen_d, buf)     # returns with its outputs written
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    n_gen, gen_ms = tr.profile_read(reset=True)
+    tr.profile(False)
+    tokens = int(tgt_len.sum()) * args.steps
+    gen_flops = 2.0 * B * w.tgt_vocab * w.hidden
+    avg_gen_s = gen_ms / 1e3 / max(n_gen, 1)
+    achieved = gen_flops / avg_gen_s / 1e12 if n_gen else 0.0
+    peak = PEAK_BF16_TFLOPS if w.wdtype == "bf16" else PEAK_FP32_TFLOPS
+    out = {
+        "metric": "teacher-forced target tokens/sec (per-token log-probs and NLL of given targets)",
+        "value": round(tokens / dt, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(dt / args.steps * 1e3, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32" if w.wdtype == "fp32" else "bf16",
+        "data": "synthetic (seeded weights, bounded-Zipf source and target tokens)",
+        "config": {"workload": f"{w.name} teacher-forced scoring, batch {B}, target length {T}",
+                   "global_batch": B, "target_len": T},
+        "roofline": {"kernel": "k_gemm_gen (generator GEMM + fused log-softmax partials)", "bound": "mfma",
+                     "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None, "launches_timed": n_gen,
+                     "avg_launch_us": round(avg_gen_s * 1e6, 2), "flops_per_launch": gen_flops},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import onmt_oracle as O
+        m = O.model_from(w, weights)
+        n = max(1, min(args.cpu_sentences, B))
+        t1 = time.perf_counter()
+        O.score_batch(m, src[:n], lens[:n], tgt[:n], tgt_len[:n])
+        ct = time.perf_counter() - t1
+        out["cpu_baseline"] = {"value": round(int(tgt_len[:n].sum()) / ct, 3), "unit": "tokens/s",
+                               "cores": cpu_threads(), "kind": "oracle",
+                               "sample": f"{n} of the {B} sentences, {int(tgt_len[:n].sum())} target tokens "
+                                         f"in {ct:.1f} s, fp64 NumPy"}
     print(json.dumps(out), flush=True)
 
 

@@ -160,6 +160,20 @@ int onmt_beam_search(onmt_model* model, const int32_t* src, const int32_t* len, 
                      int32_t* out_len, double* out_raw, double* out_norm, float* out_tok_logp,
                      const onmt_trace* trace, void* stream);
 
+/* ---- Teacher-forced scoring: the training objective's per-token terms (Section 2: the model is trained
+ * to minimise the negative log-likelihood of the corpus; the same conditional factorisation) ----------
+ * For sentence b the decoder is fed BOS, tgt[b, 0], ..., tgt[b, tgt_len[b] - 2] and scores the next target
+ * token at every step: out_logp[b, t] = log p(tgt[b, t] | tgt[b, <t], src_b) for t < tgt_len[b], 0 after;
+ * out_nll[b] = -sum_t out_logp[b, t] (fp64). tgt [B, T_max] and tgt_len [B] are device int32 arrays
+ * (1 <= tgt_len[b] <= T_max, ids in [0, tgt_vocab) below the length); they are copied to the host for
+ * validation. src/len as in onmt_encode. ws holds onmt_score_ws_bytes(model, B, S_max, T_max) bytes.
+ * out_logp [B, T_max] fp32 and out_nll [B] fp64 are device pointers. Returns when the outputs are
+ * written (the stream is synchronized). */
+size_t onmt_score_ws_bytes(const onmt_model* model, int B, int S_max, int T_max);
+int onmt_score(onmt_model* model, const int32_t* src, const int32_t* len, int B, int S_max, const int32_t* tgt,
+               const int32_t* tgt_len, int T_max, void* ws, size_t ws_bytes, float* out_logp, double* out_nll,
+               void* stream);
+
 /* ---- Kernel timing -----------------------------------------------------------------------------------
  * onmt_profile_enable(model, every): every >= 1 makes onmt_beam_search record HIP events on `stream`
  * around every `every`-th launch of the decoder's generator kernel (the vocabulary projection with its

@@ -374,6 +374,30 @@ def score_forced(m: Model, src_row, n_src, target):
     return np.array(out)
 
 
+def score_batch(m: Model, src, lens, tgt, tgt_len):
+    """Teacher-forced scoring of a batch: the per-token terms of the training objective.
+
+    Section 2: the model is trained to minimise the negative log-likelihood of the corpus under
+    p(w_1:T | x) = prod_t p(w_t | w_<t, x). Sentence b's decoder is fed BOS, tgt[b, 0], ... and scores
+    tgt[b, t] at step t. Returns (logp [B, T] with 0 from tgt_len[b] on, nll [B] = -sum of the row).
+    """
+    src = np.asarray(src)
+    tgt = np.asarray(tgt)
+    tgt_len = np.asarray(tgt_len)
+    B, T = tgt.shape
+    enc = encode(m, src, np.asarray(lens))
+    st = init_state(m, enc, 1)
+    logp = np.zeros((B, T), F64)
+    prev = np.full(B, BOS_ID)
+    rows = np.arange(B)
+    for t in range(int(tgt_len.max())):
+        st, lp, _ = decode_step(m, enc, st, prev, rows)
+        on = t < tgt_len
+        logp[on, t] = lp[rows[on], tgt[on, t]]
+        prev = np.where(on, tgt[:, t], PAD_ID)
+    return logp, -logp.sum(axis=1)
+
+
 def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0):
     """Best normalised score over every output sequence (exhaustive; tiny vocabularies only).
 

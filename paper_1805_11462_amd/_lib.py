@@ -47,6 +47,9 @@ SIGNATURES = {
     "onmt_beam_search": (c_int, [c_void_p, c_void_p, c_void_p, c_int, c_int, POINTER(OnmtSearchParams), c_void_p,
                                  c_size_t, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, POINTER(OnmtTrace),
                                  c_void_p]),
+    "onmt_score_ws_bytes": (c_size_t, [c_void_p, c_int, c_int, c_int]),
+    "onmt_score": (c_int, [c_void_p, c_void_p, c_void_p, c_int, c_int, c_void_p, c_void_p, c_int, c_void_p, c_size_t,
+                           c_void_p, c_void_p, c_void_p]),
     "onmt_profile_enable": (c_int, [c_void_p, c_int]),
     "onmt_profile_read": (c_int, [c_void_p, POINTER(c_int), POINTER(c_double), c_int]),
 }

@@ -173,6 +173,66 @@ hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pva
   return hipGetLastError();
 }
 
+// One wave per row: logsumexp from the per-tile maxima and sums, as in row_merge_wave.
+__global__ __launch_bounds__(kMergeWaves * kWave) void k_score_step(const float* __restrict__ pmax,
+                                                                    const float* __restrict__ psum, int ntiles,
+                                                                    const float* __restrict__ want_logit,
+                                                                    const int32_t* __restrict__ len, int M, int t,
+                                                                    float* __restrict__ logp, int ld,
+                                                                    double* __restrict__ nll) {
+  const int row = blockIdx.x * kMergeWaves + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= M) return;
+  const float* pm = pmax + (size_t)row * ntiles;
+  const float* ps = psum + (size_t)row * ntiles;
+  const float ninf = -__builtin_inff();
+  float tm[kMaxTilesPerLane], tq[kMaxTilesPerLane];
+#pragma unroll
+  for (int j = 0; j < kMaxTilesPerLane; ++j) {
+    const int tt = lane + j * kWave;
+    tm[j] = tt < ntiles ? pm[tt] : ninf;
+    tq[j] = tt < ntiles ? ps[tt] : 0.f;
+  }
+  float mx = ninf;
+#pragma unroll
+  for (int j = 0; j < kMaxTilesPerLane; ++j) mx = fmaxf(mx, tm[j]);
+  const float gmx = wave_max(mx);
+  float sm = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxTilesPerLane; ++j) {
+    const int tt = lane + j * kWave;
+    if (tt < ntiles) sm += tq[j] * __expf(tm[j] - gmx);
+  }
+  const float lse = gmx + __logf(wave_sum(sm));
+  if (lane == 0) {
+    const bool on = t < len[row];
+    const float v = on ? want_logit[row] - lse : 0.f;
+    logp[(size_t)row * ld + t] = v;
+    if (on) nll[row] -= (double)v;
+  }
+}
+
+hipError_t score_step(const float* pmax, const float* psum, int ntiles, const float* want_logit, const int32_t* len,
+                      int M, int t, float* logp, int ld, double* nll, hipStream_t st) {
+  if (ntiles > kWave * kMaxTilesPerLane) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_score_step, dim3((M + kMergeWaves - 1) / kMergeWaves), dim3(kMergeWaves * kWave), 0, st, pmax,
+                     psum, ntiles, want_logit, len, M, t, logp, ld, nll);
+  return hipGetLastError();
+}
+
+__global__ void k_fill64(double* dst, size_t n, double v) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = v;
+}
+
+hipError_t fill_f64(double* dst, size_t n, double v, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_fill64, dim3((unsigned)blocks), dim3(256), 0, st, dst, n, v);
+  return hipGetLastError();
+}
+
 __global__ void k_subtract_rows(float* x, int ld, const float* lse, int M, int ncols) {
   const int row = blockIdx.y;
   const float l = lse[row];

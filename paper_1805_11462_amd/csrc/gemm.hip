@@ -406,6 +406,14 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
     z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) + p.bias[gc] : ninf;
     mx = fmaxf(mx, z[j]);
   }
+  if (p.want && row < a.M) {
+    const int wc = p.want[row] - n0;      // this thread holds column 4 j + part of the tile
+    if (wc >= 0 && wc < C::BN && (wc & 3) == part) {
+#pragma unroll
+      for (int j = 0; j < 32; ++j)
+        if (4 * j + part == wc) p.want_logit[row] = z[j];
+    }
+  }
   if (p.logits && row < a.M) {
 #pragma unroll
     for (int j = 0; j < 32; ++j) {

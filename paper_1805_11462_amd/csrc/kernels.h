@@ -85,6 +85,8 @@ struct GenParams {
   int32_t* pid;                 // [M, ntiles, K]
   float* logits;                // optional [M, ld_logits]
   int ld_logits;
+  const int32_t* want;          // optional [M]: column whose logit is copied to want_logit[row]
+  float* want_logit;
 };
 
 enum GemmShape { kShapeWide = 0, kShapeSplitK = 1, kShapeSplitKThin = 2 };
@@ -102,6 +104,11 @@ size_t attention_lds_bytes(int S_max, int H, int K);
 
 hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pval, const int32_t* pid, int M,
                           int ntiles, int K, float* out_val, int32_t* out_id, float* out_lse, hipStream_t st);
+// Teacher-forced scoring, one decoder step: logp[row * ld + t] = want_logit[row] - logsumexp(row) from the
+// generator partials for rows with t < len[row] (0 otherwise), and nll[row] -= logp in fp64.
+hipError_t score_step(const float* pmax, const float* psum, int ntiles, const float* want_logit, const int32_t* len,
+                      int M, int t, float* logp, int ld, double* nll, hipStream_t st);
+hipError_t fill_f64(double* dst, size_t n, double v, hipStream_t st);
 hipError_t subtract_rows(float* x, int ld, const float* lse, int M, int ncols, hipStream_t st);
 
 struct BeamParams {

@@ -535,6 +535,41 @@ size_t search_layout(const Dims& d, int B, int S, int K, int T, char* base, Sear
   return align_up(c.off);
 }
 
+struct ScoreWs {
+  EncWs enc;
+  State st[2];
+  StepWs step;
+  int32_t* in_tok;     // [T, B] decoder input at step t
+  int32_t* want;       // [T, B] target predicted at step t
+  int32_t* tlen;       // [B]
+  float* want_logit;   // [B]
+  double* nll;         // [B]
+};
+
+size_t score_layout(const Dims& d, int B, int S, int T, char* base, ScoreWs* w) {
+  Carver c;
+  c.base = base;
+  ScoreWs t{};
+  const size_t eb = enc_layout(d, B, S, nullptr, nullptr);
+  char* e = c.take<char>(eb);
+  enc_layout(d, B, S, e, &t.enc);
+  for (int i = 0; i < 2; ++i) {
+    const size_t sb = state_layout(d, B, nullptr, nullptr);
+    char* p = c.take<char>(sb);
+    state_layout(d, B, p, &t.st[i]);
+  }
+  const size_t pb = step_layout(d, B, S, 1, nullptr, nullptr);
+  char* p = c.take<char>(pb);
+  step_layout(d, B, S, 1, p, &t.step);
+  t.in_tok = c.take<int32_t>((size_t)T * B);
+  t.want = c.take<int32_t>((size_t)T * B);
+  t.tlen = c.take<int32_t>(B);
+  t.want_logit = c.take<float>(B);
+  t.nll = c.take<double>(B);
+  if (w) *w = t;
+  return align_up(c.off);
+}
+
 Seg seg(const void* base, const int32_t* idx, int rows, int ld, int width, int kpad, int bf16) {
   Seg s;
   s.base = base;
@@ -792,9 +827,11 @@ void time_collect(onmt_model* m) {
 // One decoder step on validated inputs (Section 2; Figure 1(a); items (a)-(c); Section 4.2 attention).
 // mode 0: logp [N, V] full log-softmax; mode 1: top-K (logp [N, K], ids [N, K]); mode 2 (beam search):
 // stop after the generator, leaving its per-tile partials in the step workspace for the beam step.
+// want/want_logit (optional): the logit of column want[r] of every row is copied to want_logit[r].
 int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const State& in, const State& out,
                    const int32_t* prev_tok, const int32_t* parent, int mode, float* logp, int32_t* ids, float* lse,
-                   float* attn, const StepWs& sw, hipStream_t st) {
+                   float* attn, const StepWs& sw, hipStream_t st, const int32_t* want = nullptr,
+                   float* want_logit = nullptr) {
   const Dims& d = m->d;
   const int N = B * K;
   const size_t LH = (size_t)N * d.H;
@@ -849,6 +886,8 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     gp.pid = sw.pid;
     gp.logits = mode == 0 ? logp : nullptr;
     gp.ld_logits = d.Vt;
+    gp.want = want;
+    gp.want_logit = want_logit;
     time_begin(m, st);
     HIP_TRY(gemm_gen(d.bf16, a, bop(m->W_s), gp, st));
     time_end(m, st);
@@ -1015,6 +1054,73 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   }
   HIP_TRY(backtrack(bp, out_tok, out_len, out_raw, out_norm, out_tok_logp, st));
   if (trace) HIP_TRY(hipMemcpyAsync(trace->steps, bp.steps, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  if (m->prof) time_collect(m);
+  return ONMT_OK;
+}
+
+size_t onmt_score_ws_bytes(const onmt_model* m, int B, int S, int T) {
+  if (!m || B < 1 || S < 1 || T < 1) return 0;
+  return score_layout(m->d, B, S, T, nullptr, nullptr);
+}
+
+int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int S, const int32_t* tgt,
+               const int32_t* tgt_len, int T, void* ws, size_t ws_bytes, float* out_logp, double* out_nll,
+               void* stream) {
+  if (!m || !ws || !tgt || !tgt_len) return fail(ONMT_EINVAL, "NULL argument");
+  if (!out_logp || !out_nll) return fail(ONMT_EINVAL, "NULL output pointer");
+  if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
+  if (T < 1 || T > 100000) return fail(ONMT_EINVAL, "T_max %d outside [1, 100000]", T);
+  int rc = check_beam(m, S, 1);
+  if (rc) return rc;
+  if (ws_bytes < score_layout(m->d, B, S, T, nullptr, nullptr)) return fail(ONMT_ESIZE, "score workspace too small");
+  hipStream_t st = (hipStream_t)stream;
+  ScoreWs w;
+  score_layout(m->d, B, S, T, (char*)ws, &w);
+  int mx = 0;
+  rc = check_len_src(m, src, len, B, S, st, &mx, w.enc.src, w.enc.rowmap);
+  if (rc) return rc;
+  // targets: validated on the host, then laid out per step (decoder input and predicted token)
+  std::vector<int32_t> ht((size_t)B * T), hl(B);
+  HIP_TRY(hipMemcpyAsync(hl.data(), tgt_len, sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipMemcpyAsync(ht.data(), tgt, sizeof(int32_t) * ht.size(), hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  int steps = 0;
+  for (int b = 0; b < B; ++b) {
+    if (hl[b] < 1 || hl[b] > T) return fail(ONMT_EINVAL, "tgt_len[%d] = %d outside [1, %d]", b, hl[b], T);
+    steps = hl[b] > steps ? hl[b] : steps;
+    for (int t = 0; t < hl[b]; ++t) {
+      const int v = ht[(size_t)b * T + t];
+      if (v < 0 || v >= m->cfg.tgt_vocab)
+        return fail(ONMT_EINVAL, "tgt[%d, %d] = %d outside [0, %d)", b, t, v, m->cfg.tgt_vocab);
+    }
+  }
+  std::vector<int32_t> in((size_t)T * B), want((size_t)T * B);
+  for (int t = 0; t < T; ++t)
+    for (int b = 0; b < B; ++b) {
+      const bool on = t < hl[b];
+      in[(size_t)t * B + b] = !on ? m->cfg.pad_id : (t == 0 ? m->cfg.bos_id : ht[(size_t)b * T + t - 1]);
+      want[(size_t)t * B + b] = on ? ht[(size_t)b * T + t] : 0;
+    }
+  HIP_TRY(hipMemcpyAsync(w.in_tok, in.data(), sizeof(int32_t) * in.size(), hipMemcpyHostToDevice, st));
+  HIP_TRY(hipMemcpyAsync(w.want, want.data(), sizeof(int32_t) * want.size(), hipMemcpyHostToDevice, st));
+  HIP_TRY(hipMemcpyAsync(w.tlen, hl.data(), sizeof(int32_t) * B, hipMemcpyHostToDevice, st));
+
+  rc = encode_compute(m, src, len, B, S, mx, w.enc, st);
+  if (rc) return rc;
+  rc = decode_init_compute(m, w.enc, B, 1, w.st[0], st);
+  if (rc) return rc;
+  HIP_TRY(fill_f32(out_logp, (size_t)B * T, 0.f, st));
+  HIP_TRY(fill_f64(w.nll, B, 0.0, st));
+  int cur = 0;
+  for (int t = 0; t < steps; ++t) {
+    rc = decode_compute(m, w.enc, B, S, 1, w.st[cur], w.st[cur ^ 1], w.in_tok + (size_t)t * B, nullptr, 2, nullptr,
+                        nullptr, nullptr, nullptr, w.step, st, w.want + (size_t)t * B, w.want_logit);
+    if (rc) return rc;
+    HIP_TRY(score_step(w.step.pmax, w.step.psum, w.step.ntiles, w.want_logit, w.tlen, B, t, out_logp, T, w.nll, st));
+    cur ^= 1;
+  }
+  HIP_TRY(hipMemcpyAsync(out_nll, w.nll, sizeof(double) * B, hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipStreamSynchronize(st));
   if (m->prof) time_collect(m);
   return ONMT_OK;

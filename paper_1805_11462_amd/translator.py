@@ -169,6 +169,25 @@ class Translator:
                                         _ptr(buf["raw"]), _ptr(buf["norm"]), _ptr(buf["tok_logp"]), tr, _stream()))
         return buf
 
+    # ---------------------------------------------------------------- teacher-forced scoring
+    def score_buffers(self, B, S, T):
+        """Allocate what one onmt_score call needs (reusable across calls)."""
+        n = self.lib.onmt_score_ws_bytes(self.handle, B, S, T)
+        d = self.device
+        return {"ws": _bytes(n, d), "ws_bytes": n, "T": T,
+                "logp": torch.empty(B, T, dtype=torch.float32, device=d),
+                "nll": torch.empty(B, dtype=torch.float64, device=d)}
+
+    def score(self, src, lens, tgt, tgt_len, buf=None):
+        """Per-token log-probs [B, T] and NLL [B] of the given targets (int32 device tensors)."""
+        B, S = src.shape
+        T = tgt.shape[1]
+        if buf is None:
+            buf = self.score_buffers(B, S, T)
+        check(self.lib.onmt_score(self.handle, _ptr(src), _ptr(lens), B, S, _ptr(tgt), _ptr(tgt_len), T,
+                                  _ptr(buf["ws"]), buf["ws_bytes"], _ptr(buf["logp"]), _ptr(buf["nll"]), _stream()))
+        return buf["logp"], buf["nll"]
+
     # ---------------------------------------------------------------- timing
     def profile(self, every):
         """Time every ``every``-th generator launch of later searches (0 or False: off)."""

@@ -101,3 +101,18 @@ def make_batch(w: Workload, seed: int = None, batch: int = None):
     pos = np.arange(w.s_max)[None, :]
     src[pos >= lens[:, None]] = PAD_ID
     return src, lens
+
+
+def make_targets(w: Workload, seed: int = None, batch: int = None, T: int = None):
+    """(tgt int32 [B, T], tgt_len int32 [B]) for teacher-forced scoring: bounded-Zipf target ids
+    (same law as the source, ids 3 + r over the target vocabulary), every sentence T = max decode
+    tokens long unless T is given. Seed 2000 + workload index unless given."""
+    if seed is None:
+        seed = 2000 + w.index
+    B = w.batch if batch is None else batch
+    T = w.max_len if T is None else T
+    rng = np.random.Generator(np.random.PCG64(seed))
+    cdf = zipf_cdf(w.tgt_vocab - 4, w.zipf_s)
+    ranks = np.minimum(np.searchsorted(cdf, rng.random(size=(B, T)), side="right") + 1, w.tgt_vocab - 4)
+    return (3 + ranks).astype(np.int32), np.full(B, T, dtype=np.int32)
+

@@ -53,6 +53,11 @@ R12 bf16 workloads: the oracle runs in fp64 on the bf16-rounded weights. (The GP
     weights and fp32 accumulation; it carries each activation entering a product as two bf16 terms,
     which keeps the chaotic decoder recurrence within the bf16 tolerance over full-length outputs.)
 R15 Throughput counts target tokens of the 1-best, EOS included.
+R17 Coverage normalisation (named with length normalisation in Section 4.2, citing GNMT): a finished
+    hypothesis is ranked by raw / lp(n) + beta * sum over the real source positions of
+    log(min(c_i, 1)), c_i = the attention it put on position i summed over its steps (EOS included);
+    live hypotheses are ranked by raw score only, as with the length penalty. Since the penalty is
+    <= 0, the stop rule's bound stays exact.
 R16 Near-ties: any choice within the tolerance is a correct result.
 
 Pins (tests that tie this file to the mathematics rather than to itself) live
@@ -250,6 +255,17 @@ def length_penalty(n, alpha):
 class Hyp:
     tokens: list
     logps: list
+    cov: np.ndarray = None   # attention summed over the hypothesis's steps, per source position (R17)
+
+
+def coverage_penalty(cov, n_src, beta):
+    """GNMT coverage penalty beta * sum_{i < n_src} log(min(cov_i, 1)) (Section 4.2 names attention
+    coverage normalisation beside length normalisation; R17). 0 when beta is 0."""
+    if beta == 0.0:
+        return 0.0
+    c = np.minimum(np.asarray(cov, F64)[:n_src], 1.0)
+    with np.errstate(divide="ignore"):
+        return float(beta * np.log(c).sum())
 
 
 @dataclass
@@ -262,21 +278,23 @@ class Result:
     trace: dict = None      # per step: chosen (slot, token, cand) by rank
 
 
-def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, record=False):
+def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, record=False, beta=0.0):
     """Beam search for every sentence, one set of K slots per sentence.
 
     Sentences are independent; the decoder runs all B*K rows at once only to
-    share the matrix products.
+    share the matrix products. A finished hypothesis is ranked by
+    raw / lp(n) + coverage_penalty (R10, R17).
     """
     src = np.asarray(src)
-    B = src.shape[0]
+    lens = np.asarray(lens)
+    B, S = src.shape
     V = m.tgt_vocab
     enc = encode(m, src, lens)
     st = init_state(m, enc, K)
     row_sentence = np.repeat(np.arange(B), K)
     scores = np.full((B, K), -np.inf)
     scores[:, 0] = 0.0
-    hyps = [[Hyp([], []) for _ in range(K)] for _ in range(B)]
+    hyps = [[Hyp([], [], np.zeros(S, F64)) for _ in range(K)] for _ in range(B)]
     tok = np.full(B * K, BOS_ID, np.int64)
     done = np.zeros(B, bool)
     steps = np.zeros(B, np.int64)
@@ -284,7 +302,7 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
     trace = {"slot": [], "tok": [], "cand": []} if record else None
     lp_max = length_penalty(max_len, alpha)
     for t in range(1, max_len + 1):
-        st_new, logp, _ = decode_step(m, enc, st, tok, row_sentence)
+        st_new, logp, attn = decode_step(m, enc, st, tok, row_sentence)
         parent = np.arange(B * K)
         new_tok = np.full(B * K, PAD_ID, np.int64)
         if record:
@@ -300,15 +318,16 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
             order = np.argsort(-flat, kind="stable")            # ties: smaller flat index first
             chosen = [i for i in order[:K] if np.isfinite(flat[i])]
             new_scores = np.full(K, -np.inf)
-            new_hyps = [Hyp([], []) for _ in range(K)]
+            new_hyps = [Hyp([], [], np.zeros(S, F64)) for _ in range(K)]
             j = 0
             for rank, i in enumerate(chosen):
                 k, w = divmod(int(i), V)
-                hyp = Hyp(hyps[b][k].tokens + [w], hyps[b][k].logps + [logp[b * K + k, w]])
+                hyp = Hyp(hyps[b][k].tokens + [w], hyps[b][k].logps + [logp[b * K + k, w]],
+                          hyps[b][k].cov + attn[b * K + k])
                 if record:
                     t_slot[b, rank], t_tok[b, rank], t_cand[b, rank] = k, w, flat[i]
                 if w == EOS_ID or t == max_len:
-                    norm = flat[i] / length_penalty(t, alpha)
+                    norm = flat[i] / length_penalty(t, alpha) + coverage_penalty(hyp.cov, lens[b], beta)
                     if best[b] is None or norm > best[b][0]:
                         best[b] = (norm, flat[i], hyp)
                 else:
@@ -398,7 +417,21 @@ def score_batch(m: Model, src, lens, tgt, tgt_len):
     return logp, -logp.sum(axis=1)
 
 
-def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0):
+def coverage_forced(m: Model, src_row, n_src, target):
+    """Attention summed over the teacher-forced steps of ``target`` for one sentence, per source position."""
+    src_row = np.asarray(src_row)[None, :]
+    enc = encode(m, src_row, np.array([n_src]))
+    st = init_state(m, enc, 1)
+    prev = BOS_ID
+    cov = np.zeros(src_row.shape[1], F64)
+    for w in target:
+        st, _, a = decode_step(m, enc, st, np.array([prev]), np.array([0]))
+        cov += a[0]
+        prev = w
+    return cov
+
+
+def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0, beta=0.0):
     """Best normalised score over every output sequence (exhaustive; tiny vocabularies only).
 
     Sequences: those whose first EOS ends them at length n <= max_len, plus
@@ -414,6 +447,8 @@ def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0):
             if w == EOS_ID or len(seq) == max_len:
                 raw = score_forced(m, src_row, n_src, seq).sum()
                 norm = raw / length_penalty(len(seq), alpha)
+                if beta:
+                    norm += coverage_penalty(coverage_forced(m, src_row, n_src, seq), n_src, beta)
                 if best is None or norm > best[2]:
                     best = (seq, raw, norm)
             else:

@@ -36,6 +36,7 @@ def parse():
     ap.add_argument("--mode", choices=["search", "score"], default="search",
                     help="search: beam search (the headline metric); score: teacher-forced scoring of "
                          "max-decode-long synthetic targets")
+    ap.add_argument("--beta", type=float, default=0.0, help="coverage penalty weight of the search (0 = off)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sentences", type=int, default=4)
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -121,7 +122,7 @@ def main():
     lens_d = torch.from_numpy(lens).cuda()
     if args.mode == "score":
         return bench_score(args, w, weights, tr, src, lens, src_d, lens_d)
-    buf = tr.search_buffers(B, S, w.beam, w.max_len, w.alpha)
+    buf = tr.search_buffers(B, S, w.beam, w.max_len, w.alpha, beta=args.beta)
 
     for i in range(args.warmup):
         tr.beam_search(src_d, lens_d, buf)
@@ -168,7 +169,8 @@ def main():
         "data": "synthetic (seeded uniform(-0.1,0.1) weights, bounded-Zipf source tokens)",
         "config": {"workload": f"{w.name}: {w.enc_layers}x{w.hidden} LSTM enc/dec, emb {w.emb}, vocab {w.tgt_vocab}, "
                                f"batch {w.batch}, src len {w.len_lo}-{w.len_hi}, beam {w.beam}, "
-                               f"max decode {w.max_len}, alpha {w.alpha}, {w.wdtype}",
+                               f"max decode {w.max_len}, alpha {w.alpha}, {w.wdtype}"
+                               + (f", coverage beta {args.beta}" if args.beta else ""),
                    "global_batch": B, "beam": w.beam, "max_decode": w.max_len,
                    "target_tokens_per_step": tokens // max(args.steps, 1)},
         "step_ms": {"min": round(min(step_s) * 1e3, 3), "median": round(sorted(step_s)[len(step_s) // 2] * 1e3, 3),

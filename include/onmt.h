@@ -60,15 +60,17 @@ typedef struct {
   int pad_id, unk_id, bos_id, eos_id;
 } onmt_config;
 
-/* Beam search settings (Section 2 item (d); Section 4.2 length normalisation, GNMT form
- * lp(n) = ((5 + n) / 6)^alpha). max_len counts generated tokens including EOS. The host reads an
- * "all sentences finished" counter every check_every steps (<= 0: every step when
- * max_len <= 32, else every 8). */
+/* Beam search settings (Section 2 item (d); Section 4.2 length and attention coverage normalisation,
+ * GNMT forms lp(n) = ((5 + n) / 6)^alpha and cp = beta * sum over the real source positions i of
+ * log(min(c_i, 1)), c_i = attention on position i summed over the hypothesis's steps). max_len counts
+ * generated tokens including EOS. beta >= 0 (0 = no coverage penalty). The host reads an "all sentences
+ * finished" counter every check_every steps (<= 0: every step when max_len <= 32, else every 8). */
 typedef struct {
   int beam;
   int max_len;
   double alpha;
   int check_every;
+  double beta;
 } onmt_search_params;
 
 /* Optional per-step record of the search, device pointers, each [max_len, B, beam] by rank:
@@ -146,7 +148,8 @@ int onmt_decode_step(onmt_model* model, const void* enc_ws, int B, int S_max, in
  * Translates B sentences with beam width K = params->beam (1 <= K <= 16, K <= tgt_vocab). Per sentence:
  * slot scores start [0, -inf, ...] with input BOS; each step scores cand = s_k + logp_k(w) in fp64 and
  * keeps the K best (larger first, smaller k*V + w on ties); a chosen EOS, or any choice at step
- * max_len, enters the finished pool with norm = cand / lp(t); the others become the next live slots in
+ * max_len, enters the finished pool with norm = cand / lp(t) + cp (cp over the attention of the
+ * hypothesis's steps, this one included); the others become the next live slots in
  * rank order. A sentence stops at max_len, when no live slot remains, or when the pool's best norm is
  * >= best live score / lp(max_len) (no descendant can beat it). The result is the pool entry with the
  * largest norm (earlier step, then better rank, on ties).

@@ -20,7 +20,8 @@ class OnmtConfig(ctypes.Structure):
 
 
 class OnmtSearchParams(ctypes.Structure):
-    _fields_ = [("beam", c_int), ("max_len", c_int), ("alpha", c_double), ("check_every", c_int)]
+    _fields_ = [("beam", c_int), ("max_len", c_int), ("alpha", c_double), ("check_every", c_int),
+                ("beta", c_double)]
 
 
 class OnmtTrace(ctypes.Structure):

@@ -102,7 +102,7 @@ __global__ __launch_bounds__(kCtxThreads) void k_attn_context(const float* __res
                                                               const float* __restrict__ mem,
                                                               const int32_t* __restrict__ lens, int S_max, int Hm,
                                                               int K, int G, float* __restrict__ ctx,
-                                                              float* __restrict__ attn) {
+                                                              float* __restrict__ attn, Coverage cov) {
   extern __shared__ __attribute__((aligned(16))) float as[];      // [K][S_max] attention weights
   constexpr int CW = kCtxThreads / PL;
   const int b = blockIdx.x / G, g = blockIdx.x % G;
@@ -155,6 +155,21 @@ __global__ __launch_bounds__(kCtxThreads) void k_attn_context(const float* __res
     for (int s = lane; s < n; s += kWave) row[s] *= inv;
     if (attn && g == 0) {
       for (int s = lane; s < S_max; s += kWave) attn[(size_t)(r0 + k) * S_max + s] = s < n ? row[s] : 0.f;
+    }
+    if (cov.out && g == 0) {
+      // coverage of this row's hypothesis: its parent's coverage plus this step's weights
+      const int r = r0 + k;
+      const float* ci = cov.in + (size_t)cov.parent[r] * S_max;
+      float* co = cov.out + (size_t)r * S_max;
+      double lsum = 0.0;
+      for (int s = lane; s < S_max; s += kWave) {
+        const float c = s < n ? ci[s] + row[s] : 0.f;
+        co[s] = c;
+        if (s < n) lsum += (double)logf(fminf(c, 1.f));
+      }
+#pragma unroll
+      for (int o = kWave / 2; o > 0; o >>= 1) lsum += __shfl_xor(lsum, o, kWave);
+      if (lane == 0) cov.cp[r] = cov.beta * lsum;
     }
   }
   __syncthreads();
@@ -224,19 +239,22 @@ static int ctx_lanes(int B, int Hm4) {
 
 template <int KMAX>
 static void launch_context(int pl, dim3 grid, size_t lds, hipStream_t st, const float* e, const float* mem,
-                           const int32_t* lens, int S_max, int Hm, int K, int G, float* ctx, float* attn) {
+                           const int32_t* lens, int S_max, int Hm, int K, int G, float* ctx, float* attn,
+                           const Coverage& cov) {
   const dim3 block(kCtxThreads);
   switch (pl) {
-    case 4: hipLaunchKernelGGL((k_attn_context<KMAX, 4>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
-    case 8: hipLaunchKernelGGL((k_attn_context<KMAX, 8>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
-    case 16: hipLaunchKernelGGL((k_attn_context<KMAX, 16>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
-    case 32: hipLaunchKernelGGL((k_attn_context<KMAX, 32>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
-    default: hipLaunchKernelGGL((k_attn_context<KMAX, 64>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn); break;
+    case 4: hipLaunchKernelGGL((k_attn_context<KMAX, 4>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
+    case 8: hipLaunchKernelGGL((k_attn_context<KMAX, 8>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
+    case 16: hipLaunchKernelGGL((k_attn_context<KMAX, 16>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
+    case 32: hipLaunchKernelGGL((k_attn_context<KMAX, 32>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
+    default: hipLaunchKernelGGL((k_attn_context<KMAX, 64>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
   }
 }
 
 hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens, int B,
-                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, hipStream_t st) {
+                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, const Coverage* cov,
+                     hipStream_t st) {
+  const Coverage cv = cov ? *cov : Coverage{};
   if (H / 4 > kScoreLanes * kScoreChunks || H % 4 || Hm % 4 || K < 1 || K > kMaxBeam) return hipErrorInvalidValue;
   if (attention_lds_bytes(S_max, H, K) > kAttnLdsLimit) return hipErrorInvalidValue;
   const int nchunk = (S_max + kScorePos - 1) / kScorePos;
@@ -261,11 +279,11 @@ hipError_t attention(const float* q, int ld_q, const float* keys, const float* m
   const int G = (Hm4 + cw - 1) / cw;
   const dim3 cgrid(B * G);
   const size_t clds = (size_t)K * S_max * sizeof(float);
-  if (K <= 1) launch_context<1>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
-  else if (K <= 2) launch_context<2>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
-  else if (K <= 4) launch_context<4>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
-  else if (K <= 8) launch_context<8>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
-  else launch_context<16>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn);
+  if (K <= 1) launch_context<1>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
+  else if (K <= 2) launch_context<2>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
+  else if (K <= 4) launch_context<4>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
+  else if (K <= 8) launch_context<8>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
+  else launch_context<16>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
   return hipGetLastError();
 }
 

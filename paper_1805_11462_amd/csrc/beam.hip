@@ -383,7 +383,7 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
   }
   // finished pool: the best new entry by normalised score (earliest rank on ties) replaces the pool's
   // entry if strictly better
-  const double norm = fin ? my_v / lp_t : ninf;
+  const double norm = fin ? my_v / lp_t + (p.cp ? p.cp[r0 + my_slot] : 0.0) : ninf;
   double bn = ninf, live_max = ninf;
   int bl = -1;
   for (int k = 0; k < nsel; ++k) {

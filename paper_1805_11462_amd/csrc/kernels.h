@@ -98,8 +98,19 @@ hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st);
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st);
 int gen_tile_cols();
 
+// Attention coverage of the hypotheses (optional): out[r, s] = in[parent[r], s] + a[r, s] for the real
+// positions (0 at pads), cp[r] = beta * sum over the real positions of log(min(out[r, s], 1)).
+struct Coverage {
+  const float* in;              // [N, S_max]
+  float* out;                   // [N, S_max]
+  const int32_t* parent;        // [N]
+  double beta;
+  double* cp;                   // [N]
+};
+
 hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens, int B,
-                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, hipStream_t st);
+                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, const Coverage* cov,
+                     hipStream_t st);
 size_t attention_lds_bytes(int S_max, int H, int K);
 
 hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pval, const int32_t* pid, int M,
@@ -129,6 +140,7 @@ struct BeamParams {
   int32_t* best_slot;
   int32_t* best_tok;
   float* best_logp;
+  const double* cp;             // optional coverage penalty of each row's hypothesis this step [N]
   int32_t* tr_slot;             // optional trace [T_max, B, K]
   int32_t* tr_tok;
   double* tr_cand;

@@ -497,6 +497,8 @@ struct SearchWs {
   State st[2];
   StepWs step;
   BeamParams bp;
+  float* cov[2];     // [N, S] attention coverage of the hypotheses (ping-pong with the state)
+  double* cp;        // [N] coverage penalty of each row's hypothesis at the current step
 };
 
 size_t search_layout(const Dims& d, int B, int S, int K, int T, char* base, SearchWs* w) {
@@ -531,6 +533,8 @@ size_t search_layout(const Dims& d, int B, int S, int K, int T, char* base, Sear
   q.best_slot = c.take<int32_t>(B);
   q.best_tok = c.take<int32_t>(B);
   q.best_logp = c.take<float>(B);
+  for (int i = 0; i < 2; ++i) t.cov[i] = c.take<float>(N * S);
+  t.cp = c.take<double>(N);
   if (w) *w = t;
   return align_up(c.off);
 }
@@ -831,7 +835,7 @@ void time_collect(onmt_model* m) {
 int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const State& in, const State& out,
                    const int32_t* prev_tok, const int32_t* parent, int mode, float* logp, int32_t* ids, float* lse,
                    float* attn, const StepWs& sw, hipStream_t st, const int32_t* want = nullptr,
-                   float* want_logit = nullptr) {
+                   float* want_logit = nullptr, const Coverage* cov = nullptr) {
   const Dims& d = m->d;
   const int N = B * K;
   const size_t LH = (size_t)N * d.H;
@@ -860,7 +864,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     HIP_TRY(gemm_lstm(d.bf16, small_shape(N, m->dec_w[l].Np), a, bop(m->dec_w[l]), lp, st));
   }
   const float* q = out.h + (d.L - 1) * LH;
-  HIP_TRY(attention(q, d.H, w.keys, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.scores, sw.ctx, attn, st));
+  HIP_TRY(attention(q, d.H, w.keys, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.scores, sw.ctx, attn, cov, st));
   {
     AOp a{};
     a.M = N;
@@ -1005,6 +1009,7 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   const int K = prm->beam, T = prm->max_len;
   if (T < 1 || T > 100000) return fail(ONMT_EINVAL, "max_len %d outside [1, 100000]", T);
   if (!(prm->alpha >= 0.0) || !std::isfinite(prm->alpha)) return fail(ONMT_EINVAL, "alpha must be finite and >= 0");
+  if (!(prm->beta >= 0.0) || !std::isfinite(prm->beta)) return fail(ONMT_EINVAL, "beta must be finite and >= 0");
   if (trace && (!trace->slot || !trace->tok || !trace->cand || !trace->steps))
     return fail(ONMT_EINVAL, "trace given with a NULL array");
   if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
@@ -1036,12 +1041,17 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   if (rc) return rc;
   rc = decode_init_compute(m, w.enc, B, K, w.st[0], st);
   if (rc) return rc;
+  const bool coverage = prm->beta > 0.0;
+  bp.cp = coverage ? w.cp : nullptr;
   HIP_TRY(beam_init(bp, m->cfg.bos_id, st));
+  if (coverage) HIP_TRY(fill_f32(w.cov[0], (size_t)B * K * S, 0.f, st));
   const int every = prm->check_every > 0 ? prm->check_every : (T <= 32 ? 1 : 8);
   int cur = 0;
   for (int t = 1; t <= T; ++t) {
+    // coverage of the rows' hypotheses: the parents' coverage (previous layout) plus this step's weights
+    const Coverage cv{w.cov[cur], w.cov[cur ^ 1], bp.parent, prm->beta, w.cp};
     rc = decode_compute(m, w.enc, B, S, K, w.st[cur], w.st[cur ^ 1], bp.tok, bp.parent, 2, nullptr, nullptr,
-                        nullptr, nullptr, w.step, st);
+                        nullptr, nullptr, w.step, st, nullptr, nullptr, coverage ? &cv : nullptr);
     if (rc) return rc;
     HIP_TRY(beam_step(bp, gp, t, st));
     cur ^= 1;

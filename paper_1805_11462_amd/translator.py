@@ -138,9 +138,9 @@ class Translator:
         return out_state, logp, ids, lse, attn
 
     # ---------------------------------------------------------------- search
-    def search_buffers(self, B, S, beam, max_len, alpha=0.0, check_every=0, trace=False):
+    def search_buffers(self, B, S, beam, max_len, alpha=0.0, check_every=0, trace=False, beta=0.0):
         """Allocate everything one onmt_beam_search call needs (reusable across calls)."""
-        p = OnmtSearchParams(beam, max_len, float(alpha), check_every)
+        p = OnmtSearchParams(beam, max_len, float(alpha), check_every, float(beta))
         n = self.lib.onmt_search_ws_bytes(self.handle, B, S, ctypes.byref(p))
         d = self.device
         buf = {

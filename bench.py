@@ -82,13 +82,13 @@ def cpu_threads():
         return len(os.sched_getaffinity(0))
 
 
-def cpu_baseline(w, weights, src, lens, n_sent):
+def cpu_baseline(w, weights, src, lens, n_sent, beta=0.0):
     """The oracle (fp64 NumPy) on the first n_sent sentences of the same batch, on this host's cores."""
     from oracle import onmt_oracle as O
     threads = cpu_threads()
     m = O.model_from(w, weights)
     t0 = time.perf_counter()
-    res = O.beam_search(m, src[:n_sent], lens[:n_sent], w.beam, w.max_len, w.alpha)
+    res = O.beam_search(m, src[:n_sent], lens[:n_sent], w.beam, w.max_len, w.alpha, beta=beta)
     dt = time.perf_counter() - t0
     toks = int(sum(len(t) for t in res.tokens))
     return {"value": round(toks / dt, 3), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
@@ -182,7 +182,7 @@ def main():
                      "flops_per_launch": gen_flops},
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, weights, src, lens, args.cpu_sentences)
+        out["cpu_baseline"] = cpu_baseline(w, weights, src, lens, args.cpu_sentences, args.beta)
     print(json.dumps(out), flush=True)
 
 

@@ -53,6 +53,12 @@ R12 bf16 workloads: the oracle runs in fp64 on the bf16-rounded weights. (The GP
     weights and fp32 accumulation; it carries each activation entering a product as two bf16 terms,
     which keeps the chaotic decoder recurrence within the bf16 tolerance over full-length outputs.)
 R15 Throughput counts target tokens of the 1-best, EOS included.
+R18 Hypothesis filters (Section 4.2: constraints such as a maximum number of OOVs and lexical
+    constraints): a candidate whose token is in the banned set, or which would be an UNK beyond
+    max_unk UNKs, is not a candidate (log-probs stay normalised over the whole vocabulary).
+R19 Unknown-word replacement (Section 4.2 OOV handling, citing Luong et al. 2015b): every output token
+    is aligned to the source position with the largest attention weight of its step (smaller position
+    on ties); an UNK output takes the source token there.
 R17 Coverage normalisation (named with length normalisation in Section 4.2, citing GNMT): a finished
     hypothesis is ranked by raw / lp(n) + beta * sum over the real source positions of
     log(min(c_i, 1)), c_i = the attention it put on position i summed over its steps (EOS included);
@@ -69,7 +75,7 @@ trained weights that are not available.
 from dataclasses import dataclass, field
 import numpy as np
 
-from workloads.configs import PAD_ID, BOS_ID, EOS_ID
+from workloads.configs import PAD_ID, UNK_ID, BOS_ID, EOS_ID
 
 F64 = np.float64
 
@@ -256,6 +262,8 @@ class Hyp:
     tokens: list
     logps: list
     cov: np.ndarray = None   # attention summed over the hypothesis's steps, per source position (R17)
+    align: list = None       # per token: source position of the largest attention weight (R19)
+    n_unk: int = 0           # UNK tokens so far (R18)
 
 
 def coverage_penalty(cov, n_src, beta):
@@ -276,9 +284,33 @@ class Result:
     logps: list             # per-token log-probs of the 1-best
     steps: np.ndarray       # [B] step after which the sentence was done
     trace: dict = None      # per step: chosen (slot, token, cand) by rank
+    align: list = None      # per token of the 1-best: argmax source position of its step's attention
 
 
-def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, record=False, beta=0.0):
+def allowed(w, n_unk, banned, max_unk):
+    """Hypothesis filter (Section 4.2: beam search under constraints such as a maximum number of OOVs and
+    lexical constraints; R18): a banned token, or an UNK beyond max_unk UNKs (max_unk < 0: no limit),
+    cannot extend a hypothesis."""
+    if w in banned:
+        return False
+    return not (max_unk >= 0 and w == UNK_ID and n_unk >= max_unk)
+
+
+def attention_argmax(a, n_src):
+    """Source position with the largest attention weight, the smaller position on ties (R19)."""
+    return int(np.argmax(np.asarray(a)[:n_src]))
+
+
+def replace_unk(tokens, align, src_row, unk_id=None):
+    """Unknown-word replacement (Section 4.2 OOV handling): every UNK output token takes the source token at
+    its aligned position. Source and target ids share no vocabulary here, so the result marks a copied
+    source token as ('src', id) and keeps other tokens as ('tgt', id)."""
+    unk = UNK_ID if unk_id is None else unk_id
+    return [("src", int(src_row[a])) if t == unk else ("tgt", int(t)) for t, a in zip(tokens, align)]
+
+
+def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, record=False, beta=0.0,
+                banned=(), max_unk=-1):
     """Beam search for every sentence, one set of K slots per sentence.
 
     Sentences are independent; the decoder runs all B*K rows at once only to
@@ -294,7 +326,9 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
     row_sentence = np.repeat(np.arange(B), K)
     scores = np.full((B, K), -np.inf)
     scores[:, 0] = 0.0
-    hyps = [[Hyp([], [], np.zeros(S, F64)) for _ in range(K)] for _ in range(B)]
+    banned = set(int(x) for x in banned)
+    filtering = bool(banned) or max_unk >= 0
+    hyps = [[Hyp([], [], np.zeros(S, F64), []) for _ in range(K)] for _ in range(B)]
     tok = np.full(B * K, BOS_ID, np.int64)
     done = np.zeros(B, bool)
     steps = np.zeros(B, np.int64)
@@ -314,16 +348,24 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
                 continue
             rows = slice(b * K, (b + 1) * K)
             cand = scores[b][:, None] + logp[rows]              # [K, V]; dead slots stay -inf
+            if filtering:                                       # R18, the same rule as allowed()
+                if banned:
+                    cand[:, sorted(banned)] = -np.inf
+                for k in range(K):
+                    if max_unk >= 0 and hyps[b][k].n_unk >= max_unk:
+                        cand[k, UNK_ID] = -np.inf
             flat = cand.ravel()
             order = np.argsort(-flat, kind="stable")            # ties: smaller flat index first
             chosen = [i for i in order[:K] if np.isfinite(flat[i])]
             new_scores = np.full(K, -np.inf)
-            new_hyps = [Hyp([], [], np.zeros(S, F64)) for _ in range(K)]
+            new_hyps = [Hyp([], [], np.zeros(S, F64), []) for _ in range(K)]
             j = 0
             for rank, i in enumerate(chosen):
                 k, w = divmod(int(i), V)
                 hyp = Hyp(hyps[b][k].tokens + [w], hyps[b][k].logps + [logp[b * K + k, w]],
-                          hyps[b][k].cov + attn[b * K + k])
+                          hyps[b][k].cov + attn[b * K + k],
+                          hyps[b][k].align + [attention_argmax(attn[b * K + k], lens[b])],
+                          hyps[b][k].n_unk + (1 if w == UNK_ID else 0))
                 if record:
                     t_slot[b, rank], t_tok[b, rank], t_cand[b, rank] = k, w, flat[i]
                 if w == EOS_ID or t == max_len:
@@ -353,7 +395,7 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
             break
     return Result([bst[2].tokens for bst in best],
                   np.array([bst[1] for bst in best]), np.array([bst[0] for bst in best]),
-                  [bst[2].logps for bst in best], steps, trace)
+                  [bst[2].logps for bst in best], steps, trace, [bst[2].align for bst in best])
 
 
 def greedy(m: Model, src, lens, max_len):
@@ -431,7 +473,7 @@ def coverage_forced(m: Model, src_row, n_src, target):
     return cov
 
 
-def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0, beta=0.0):
+def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0, beta=0.0, banned=(), max_unk=-1):
     """Best normalised score over every output sequence (exhaustive; tiny vocabularies only).
 
     Sequences: those whose first EOS ends them at length n <= max_len, plus
@@ -443,6 +485,8 @@ def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0, beta=0.0):
     while stack:
         prefix = stack.pop()
         for w in range(V):
+            if not allowed(w, sum(1 for x in prefix if x == UNK_ID), set(banned), max_unk):
+                continue
             seq = prefix + [w]
             if w == EOS_ID or len(seq) == max_len:
                 raw = score_forced(m, src_row, n_src, seq).sum()

@@ -71,6 +71,13 @@ typedef struct {
   double alpha;
   int check_every;
   double beta;
+  /* Hypothesis filters (Section 4.2: beam search under constraints such as a maximum number of OOVs and
+   * lexical constraints): a candidate whose token is one of banned[0 .. n_banned) (host array, ids in
+   * [0, tgt_vocab)), or an unk_id beyond max_unk UNKs of its hypothesis (max_unk < 0: no limit), is not
+   * a candidate; log-probs stay normalised over the whole vocabulary. */
+  int max_unk;
+  const int32_t* banned;
+  int n_banned;
 } onmt_search_params;
 
 /* Optional per-step record of the search, device pointers, each [max_len, B, beam] by rank:
@@ -155,13 +162,16 @@ int onmt_decode_step(onmt_model* model, const void* enc_ws, int B, int S_max, in
  * largest norm (earlier step, then better rank, on ties).
  * Outputs (device pointers): out_tok [B, max_len] (BOS excluded, EOS included if chosen, pad_id after
  * the end), out_len [B], out_raw [B] (sum of log-probs), out_norm [B], out_tok_logp [B, max_len]
- * (optional; 0 after the end), trace (optional). ws holds onmt_search_ws_bytes(...) bytes. src/len as
- * in onmt_encode. Returns when the outputs are written (the stream is synchronized). */
+ * (optional; 0 after the end), out_align [B, max_len] (optional; for every output token the source
+ * position with the largest attention weight of its step, smaller position on ties, -1 after the end:
+ * the alignment for unknown-word replacement, Section 4.2 OOV handling), trace (optional). ws holds
+ * onmt_search_ws_bytes(...) bytes. src/len as in onmt_encode. Returns when the outputs are written (the
+ * stream is synchronized). */
 size_t onmt_search_ws_bytes(const onmt_model* model, int B, int S_max, const onmt_search_params* params);
 int onmt_beam_search(onmt_model* model, const int32_t* src, const int32_t* len, int B, int S_max,
                      const onmt_search_params* params, void* ws, size_t ws_bytes, int32_t* out_tok,
                      int32_t* out_len, double* out_raw, double* out_norm, float* out_tok_logp,
-                     const onmt_trace* trace, void* stream);
+                     int32_t* out_align, const onmt_trace* trace, void* stream);
 
 /* ---- Teacher-forced scoring: the training objective's per-token terms (Section 2: the model is trained
  * to minimise the negative log-likelihood of the corpus; the same conditional factorisation) ----------

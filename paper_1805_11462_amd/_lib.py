@@ -21,7 +21,7 @@ class OnmtConfig(ctypes.Structure):
 
 class OnmtSearchParams(ctypes.Structure):
     _fields_ = [("beam", c_int), ("max_len", c_int), ("alpha", c_double), ("check_every", c_int),
-                ("beta", c_double)]
+                ("beta", c_double), ("max_unk", c_int), ("banned", c_void_p), ("n_banned", c_int)]
 
 
 class OnmtTrace(ctypes.Structure):
@@ -46,8 +46,8 @@ SIGNATURES = {
                                  c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "onmt_search_ws_bytes": (c_size_t, [c_void_p, c_int, c_int, POINTER(OnmtSearchParams)]),
     "onmt_beam_search": (c_int, [c_void_p, c_void_p, c_void_p, c_int, c_int, POINTER(OnmtSearchParams), c_void_p,
-                                 c_size_t, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, POINTER(OnmtTrace),
-                                 c_void_p]),
+                                 c_size_t, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                 POINTER(OnmtTrace), c_void_p]),
     "onmt_score_ws_bytes": (c_size_t, [c_void_p, c_int, c_int, c_int]),
     "onmt_score": (c_int, [c_void_p, c_void_p, c_void_p, c_int, c_int, c_void_p, c_void_p, c_int, c_void_p, c_size_t,
                            c_void_p, c_void_p, c_void_p]),

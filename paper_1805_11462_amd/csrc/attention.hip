@@ -102,7 +102,8 @@ __global__ __launch_bounds__(kCtxThreads) void k_attn_context(const float* __res
                                                               const float* __restrict__ mem,
                                                               const int32_t* __restrict__ lens, int S_max, int Hm,
                                                               int K, int G, float* __restrict__ ctx,
-                                                              float* __restrict__ attn, Coverage cov) {
+                                                              float* __restrict__ attn, Coverage cov,
+                                                              int32_t* __restrict__ align) {
   extern __shared__ __attribute__((aligned(16))) float as[];      // [K][S_max] attention weights
   constexpr int CW = kCtxThreads / PL;
   const int b = blockIdx.x / G, g = blockIdx.x % G;
@@ -155,6 +156,27 @@ __global__ __launch_bounds__(kCtxThreads) void k_attn_context(const float* __res
     for (int s = lane; s < n; s += kWave) row[s] *= inv;
     if (attn && g == 0) {
       for (int s = lane; s < S_max; s += kWave) attn[(size_t)(r0 + k) * S_max + s] = s < n ? row[s] : 0.f;
+    }
+    if (align && g == 0) {
+      // largest weight, smaller position on ties
+      float bv = -1.f;
+      int bs = 0x7fffffff;
+      for (int s = lane; s < n; s += kWave) {
+        if (row[s] > bv) {                    // s increases per lane, so strict keeps the smaller s
+          bv = row[s];
+          bs = s;
+        }
+      }
+#pragma unroll
+      for (int o = kWave / 2; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(bv, o, kWave);
+        const int os = __shfl_xor(bs, o, kWave);
+        if (ov > bv || (ov == bv && os < bs)) {
+          bv = ov;
+          bs = os;
+        }
+      }
+      if (lane == 0) align[r0 + k] = bs;
     }
     if (cov.out && g == 0) {
       // coverage of this row's hypothesis: its parent's coverage plus this step's weights
@@ -240,21 +262,21 @@ static int ctx_lanes(int B, int Hm4) {
 template <int KMAX>
 static void launch_context(int pl, dim3 grid, size_t lds, hipStream_t st, const float* e, const float* mem,
                            const int32_t* lens, int S_max, int Hm, int K, int G, float* ctx, float* attn,
-                           const Coverage& cov) {
+                           const Coverage& cov, int32_t* align) {
   const dim3 block(kCtxThreads);
   switch (pl) {
-    case 4: hipLaunchKernelGGL((k_attn_context<KMAX, 4>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
-    case 8: hipLaunchKernelGGL((k_attn_context<KMAX, 8>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
-    case 16: hipLaunchKernelGGL((k_attn_context<KMAX, 16>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
-    case 32: hipLaunchKernelGGL((k_attn_context<KMAX, 32>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
-    default: hipLaunchKernelGGL((k_attn_context<KMAX, 64>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov); break;
+    case 4: hipLaunchKernelGGL((k_attn_context<KMAX, 4>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov, align); break;
+    case 8: hipLaunchKernelGGL((k_attn_context<KMAX, 8>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov, align); break;
+    case 16: hipLaunchKernelGGL((k_attn_context<KMAX, 16>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov, align); break;
+    case 32: hipLaunchKernelGGL((k_attn_context<KMAX, 32>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov, align); break;
+    default: hipLaunchKernelGGL((k_attn_context<KMAX, 64>), grid, block, lds, st, e, mem, lens, S_max, Hm, K, G, ctx, attn, cov, align); break;
   }
 }
 
 hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens, int B,
-                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, const Coverage* cov,
+                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, const AttnExtra& ex,
                      hipStream_t st) {
-  const Coverage cv = cov ? *cov : Coverage{};
+  const Coverage cv = ex.cov ? *ex.cov : Coverage{};
   if (H / 4 > kScoreLanes * kScoreChunks || H % 4 || Hm % 4 || K < 1 || K > kMaxBeam) return hipErrorInvalidValue;
   if (attention_lds_bytes(S_max, H, K) > kAttnLdsLimit) return hipErrorInvalidValue;
   const int nchunk = (S_max + kScorePos - 1) / kScorePos;
@@ -279,11 +301,11 @@ hipError_t attention(const float* q, int ld_q, const float* keys, const float* m
   const int G = (Hm4 + cw - 1) / cw;
   const dim3 cgrid(B * G);
   const size_t clds = (size_t)K * S_max * sizeof(float);
-  if (K <= 1) launch_context<1>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
-  else if (K <= 2) launch_context<2>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
-  else if (K <= 4) launch_context<4>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
-  else if (K <= 8) launch_context<8>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
-  else launch_context<16>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv);
+  if (K <= 1) launch_context<1>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv, ex.align);
+  else if (K <= 2) launch_context<2>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv, ex.align);
+  else if (K <= 4) launch_context<4>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv, ex.align);
+  else if (K <= 8) launch_context<8>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv, ex.align);
+  else launch_context<16>(pl, cgrid, clds, st, scores, mem, lens, S_max, Hm, K, G, ctx, attn, cv, ex.align);
   return hipGetLastError();
 }
 

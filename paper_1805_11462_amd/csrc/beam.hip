@@ -25,10 +25,13 @@ constexpr int kQualCap = 256;                 // qualifying tiles listed per row
 // Row partials start at pmax/psum + row * ntiles and pval/pid + row * ntiles * K. Lane 0 writes
 // out_val[k] = logit - lse (K entries), out_id[k] and *out_lse. sv/si/cnt/qt: this wave's LDS scratch
 // (kSurvivorCap survivors, kQualCap qualifying tile ids).
+// pfmax (optional, filters active): per-tile largest allowed logit, which then replaces the tile maximum
+// in the bound (the lists hold allowed entries only; the logsumexp still covers every column).
 __device__ __forceinline__ void row_merge_wave(const float* __restrict__ pmax, const float* __restrict__ psum,
                                                const float* __restrict__ pval, const int32_t* __restrict__ pid,
-                                               int ntiles, int K, float* sv, int* si, int* cnt, int* qt,
-                                               float* out_val, int32_t* out_id, float* out_lse) {
+                                               const float* __restrict__ pfmax, int ntiles, int K, float* sv,
+                                               int* si, int* cnt, int* qt, float* out_val, int32_t* out_id,
+                                               float* out_lse) {
   const int lane = threadIdx.x & 63;
   const float ninf = -__builtin_inff();
   // tile maxima and sums, every load issued before the first use
@@ -50,6 +53,15 @@ __device__ __forceinline__ void row_merge_wave(const float* __restrict__ pmax, c
     if (t < ntiles) sm += tq[j] * __expf(tm[j] - gmx);
   }
   const float lse = gmx + __logf(wave_sum(sm));
+  if (pfmax) {
+    mx = ninf;
+#pragma unroll
+    for (int j = 0; j < kMaxTilesPerLane; ++j) {
+      const int t = lane + j * kWave;
+      tm[j] = t < ntiles ? pfmax[t] : ninf;
+      mx = fmaxf(mx, tm[j]);
+    }
+  }
 
   // theta: K rounds of a wave maximum, each removing the (lowest) lane that holds it
   float cur = mx, theta = ninf;
@@ -160,7 +172,8 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_lse_topk(const float* _
   const int row = blockIdx.x * kMergeWaves + w;
   if (row >= M) return;
   const size_t base = (size_t)row * ntiles;
-  row_merge_wave(pmax + base, psum + base, pval + base * K, pid + base * K, ntiles, K, sv[w], si[w], &cnt[w], qt[w],
+  row_merge_wave(pmax + base, psum + base, pval + base * K, pid + base * K, nullptr, ntiles, K, sv[w], si[w], &cnt[w],
+                 qt[w],
                  out_val + (size_t)row * K, out_id ? out_id + (size_t)row * K : nullptr,
                  out_lse ? out_lse + row : nullptr);
 }
@@ -253,6 +266,7 @@ __global__ void k_beam_init(BeamParams p, int bos) {
     p.score[r] = (r % p.K == 0) ? 0.0 : -__builtin_inf();
     p.parent[r] = r;
     p.tok[r] = bos;
+    if (p.unk_cnt) p.unk_cnt[r] = 0;
     if (r < p.B) {
       p.done[r] = 0;
       p.steps[r] = 0;
@@ -313,8 +327,9 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
   }
   if (my_score > ninf) {
     const size_t base = (size_t)(r0 + w) * gp.ntiles;
-    row_merge_wave(gp.pmax + base, gp.psum + base, gp.pval + base * K, gp.pid + base * K, gp.ntiles, K, sv[w], si[w],
-                   &cnt[w], qt[w], tkv[w], tki[w], nullptr);
+    row_merge_wave(gp.pmax + base, gp.psum + base, gp.pval + base * K, gp.pid + base * K,
+                   gp.pfmax ? gp.pfmax + base : nullptr, gp.ntiles, K, sv[w], si[w], &cnt[w], qt[w], tkv[w], tki[w],
+                   nullptr);
   }
   __syncthreads();
   if (w != 0) return;
@@ -367,6 +382,10 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
   const unsigned long long lm = __ballot(liv);
   const int live = __popcll(lm);
   const size_t N = (size_t)p.B * K;
+  // per-candidate facts of its slot (read by every lane before any slot is rewritten)
+  const int my_align = (has && p.align) ? p.align[r0 + my_slot] : -1;
+  const int my_unk = (has && p.unk_cnt) ? p.unk_cnt[r0 + my_slot] + (my_tok == p.unk_id ? 1 : 0) : 0;
+  __threadfence_block();       // those loads complete before any slot below is rewritten
   if (liv) {
     const int j = __popcll(lm & below);
     p.score[r0 + j] = my_v;
@@ -375,11 +394,14 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
     p.bp_slot[(size_t)(t - 1) * N + r0 + j] = my_slot;
     p.bp_tok[(size_t)(t - 1) * N + r0 + j] = my_tok;
     p.bp_logp[(size_t)(t - 1) * N + r0 + j] = my_l;
+    if (p.align) p.bp_align[(size_t)(t - 1) * N + r0 + j] = my_align;
+    if (p.unk_cnt) p.unk_cnt[r0 + j] = my_unk;
   }
   if (lane >= live && lane < K) {
     p.score[r0 + lane] = ninf;
     p.parent[r0 + lane] = r0;
     p.tok[r0 + lane] = p.pad;
+    if (p.unk_cnt) p.unk_cnt[r0 + lane] = 0;
   }
   // finished pool: the best new entry by normalised score (earliest rank on ties) replaces the pool's
   // entry if strictly better
@@ -406,6 +428,7 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
       p.best_slot[b] = my_slot;
       p.best_tok[b] = my_tok;
       p.best_logp[b] = my_l;
+      if (p.align) p.best_align[b] = my_align;
     }
   }
   const bool stop = (t == p.T_max) || (live == 0) || (best_t > 0 && best_norm >= live_max / p.lp_tmax);
@@ -430,7 +453,8 @@ constexpr int kBtThreads = 256;
 constexpr int kBtChunk = 256;      // steps staged per round
 
 __global__ __launch_bounds__(kBtThreads) void k_backtrack(BeamParams p, int32_t* out_tok, int32_t* out_len,
-                                                          double* out_raw, double* out_norm, float* out_tok_logp) {
+                                                          double* out_raw, double* out_norm, float* out_tok_logp,
+                                                          int32_t* out_align) {
   __shared__ int8_t slots[kBtChunk * kMaxBeam];   // slot (< 16) of each (step, rank) in the current chunk
   __shared__ int8_t path[kBtChunk];               // rank of the path's entry at each step of the chunk
   __shared__ int s_slot;
@@ -440,9 +464,11 @@ __global__ __launch_bounds__(kBtThreads) void k_backtrack(BeamParams p, int32_t*
   const int tb = p.best_t[b];
   int32_t* tok = out_tok + (size_t)b * p.T_max;
   float* lp = out_tok_logp ? out_tok_logp + (size_t)b * p.T_max : nullptr;
+  int32_t* al = out_align ? out_align + (size_t)b * p.T_max : nullptr;
   for (int i = tb + threadIdx.x; i < p.T_max; i += kBtThreads) {
     tok[i] = p.pad;
     if (lp) lp[i] = 0.f;
+    if (al) al[i] = -1;
   }
   if (threadIdx.x == 0) {
     out_len[b] = tb;
@@ -454,6 +480,7 @@ __global__ __launch_bounds__(kBtThreads) void k_backtrack(BeamParams p, int32_t*
   if (threadIdx.x == 0) {
     tok[tb - 1] = p.best_tok[b];
     if (lp) lp[tb - 1] = p.best_logp[b];
+    if (al) al[tb - 1] = p.best_align[b];
   }
   // entries at steps tt = tb-1 .. 1 (1-based step tt is stored at row tt - 1), walked downwards in chunks
   for (int hi = tb - 1; hi >= 1; hi -= kBtChunk) {
@@ -479,15 +506,16 @@ __global__ __launch_bounds__(kBtThreads) void k_backtrack(BeamParams p, int32_t*
       const size_t o = (size_t)(tt - 1) * N + (size_t)b * K + path[i];
       tok[tt - 1] = p.bp_tok[o];
       if (lp) lp[tt - 1] = p.bp_logp[o];
+      if (al) al[tt - 1] = p.bp_align[o];
     }
   }
 }
 
 hipError_t backtrack(const BeamParams& p, int32_t* out_tok, int32_t* out_len, double* out_raw, double* out_norm,
-                     float* out_tok_logp, hipStream_t st) {
-  if (p.K > kMaxBeam) return hipErrorInvalidValue;
+                     float* out_tok_logp, int32_t* out_align, hipStream_t st) {
+  if (p.K > kMaxBeam || (out_align && !p.align)) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_backtrack, dim3(p.B), dim3(kBtThreads), 0, st, p, out_tok, out_len, out_raw, out_norm,
-                     out_tok_logp);
+                     out_tok_logp, out_align);
   return hipGetLastError();
 }
 

@@ -433,7 +433,24 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
     p.pmax[o] = rmx;
     p.psum[o] = sm;
   }
+  // filtered columns start out taken, so the top-K never picks them
   uint32_t taken = 0;
+  if (p.banned_bits) {
+    uint32_t words[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c0 = n0 + 32 * i;
+      words[i] = c0 < p.V ? p.banned_bits[c0 >> 5] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {            // column offset 4 j + part lies in word j / 8
+      if ((words[j >> 3] >> (4 * (j & 7) + part)) & 1u) taken |= 1u << j;
+    }
+  }
+  if (p.unk_cnt && row < a.M && p.max_unk >= 0 && p.unk_cnt[row] >= p.max_unk) {
+    const int c = p.unk_id - n0;
+    if (c >= 0 && c < C::BN && (c & 3) == part) taken |= 1u << (c >> 2);
+  }
   for (int k = 0; k < p.K; ++k) {
     float bv = ninf;
     int bj = 0;
@@ -460,6 +477,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
     if (part == 0 && row < a.M) {
       p.pval[o * p.K + k] = bv;
       p.pid[o * p.K + k] = bid;
+      if (k == 0 && p.pfmax) p.pfmax[o] = bv;
     }
   }
 }

@@ -87,6 +87,13 @@ struct GenParams {
   int ld_logits;
   const int32_t* want;          // optional [M]: column whose logit is copied to want_logit[row]
   float* want_logit;
+  // hypothesis filters (optional): columns never entered into the top-K lists (max and sum of exp
+  // still cover every column): banned_bits[c >> 5] bit c & 31, and unk_id on rows whose UNK count has
+  // reached max_unk (max_unk < 0: no limit). pfmax (set when filtering) = each tile's largest allowed logit.
+  const uint32_t* banned_bits;
+  const int32_t* unk_cnt;       // [M]
+  int unk_id, max_unk;
+  float* pfmax;                 // [M, ntiles]
 };
 
 enum GemmShape { kShapeWide = 0, kShapeSplitK = 1, kShapeSplitKThin = 2 };
@@ -108,8 +115,14 @@ struct Coverage {
   double* cp;                   // [N]
 };
 
+// Optional per-row outputs of the attention softmax (beyond the weights themselves).
+struct AttnExtra {
+  const Coverage* cov;          // coverage update and penalty
+  int32_t* align;               // [N]: position of the largest weight (smaller position on ties)
+};
+
 hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens, int B,
-                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, const Coverage* cov,
+                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, const AttnExtra& ex,
                      hipStream_t st);
 size_t attention_lds_bytes(int S_max, int H, int K);
 
@@ -141,6 +154,11 @@ struct BeamParams {
   int32_t* best_tok;
   float* best_logp;
   const double* cp;             // optional coverage penalty of each row's hypothesis this step [N]
+  const int32_t* align;         // optional [N]: attention argmax of each row at this step
+  int32_t* bp_align;            // [T_max, N] (with align)
+  int32_t* best_align;          // [B] (with align)
+  int32_t* unk_cnt;             // [N] UNK tokens of each slot's hypothesis
+  int unk_id;
   int32_t* tr_slot;             // optional trace [T_max, B, K]
   int32_t* tr_tok;
   double* tr_cand;
@@ -153,12 +171,13 @@ struct GenPartials {
   const float* pval;
   const int32_t* pid;
   int ntiles;
+  const float* pfmax;           // optional: per-tile largest allowed logit (filters active)
 };
 
 hipError_t beam_init(const BeamParams& p, int bos, hipStream_t st);
 hipError_t beam_step(const BeamParams& p, const GenPartials& gp, int t, hipStream_t st);
 hipError_t backtrack(const BeamParams& p, int32_t* out_tok, int32_t* out_len, double* out_raw, double* out_norm,
-                     float* out_tok_logp, hipStream_t st);
+                     float* out_tok_logp, int32_t* out_align, hipStream_t st);
 
 hipError_t replicate_rows(const float* src, int ld_src, int rows, int K, float* dst, int ld_dst, int ncols,
                           hipStream_t st);

@@ -470,6 +470,8 @@ struct StepWs {
   float* tk_val;   // [N, K]
   int32_t* tk_id;
   float* lse;      // [N]
+  int32_t* align;  // [N] attention argmax
+  float* pfmax;    // [N, ntiles] largest allowed logit per tile (hypothesis filters)
   int ntiles;
 };
 
@@ -488,6 +490,8 @@ size_t step_layout(const Dims& d, int B, int S, int K, char* base, StepWs* w) {
   t.tk_val = c.take<float>(N * K);
   t.tk_id = c.take<int32_t>(N * K);
   t.lse = c.take<float>(N);
+  t.align = c.take<int32_t>(N);
+  t.pfmax = c.take<float>(N * t.ntiles);
   if (w) *w = t;
   return align_up(c.off);
 }
@@ -499,6 +503,7 @@ struct SearchWs {
   BeamParams bp;
   float* cov[2];     // [N, S] attention coverage of the hypotheses (ping-pong with the state)
   double* cp;        // [N] coverage penalty of each row's hypothesis at the current step
+  uint32_t* banned_bits;   // [ceil(V / 32)]
 };
 
 size_t search_layout(const Dims& d, int B, int S, int K, int T, char* base, SearchWs* w) {
@@ -535,6 +540,10 @@ size_t search_layout(const Dims& d, int B, int S, int K, int T, char* base, Sear
   q.best_logp = c.take<float>(B);
   for (int i = 0; i < 2; ++i) t.cov[i] = c.take<float>(N * S);
   t.cp = c.take<double>(N);
+  q.bp_align = c.take<int32_t>((size_t)T * N);
+  q.best_align = c.take<int32_t>(B);
+  q.unk_cnt = c.take<int32_t>(N);
+  t.banned_bits = c.take<uint32_t>((size_t)(d.Vt + 31) / 32);
   if (w) *w = t;
   return align_up(c.off);
 }
@@ -831,11 +840,21 @@ void time_collect(onmt_model* m) {
 // One decoder step on validated inputs (Section 2; Figure 1(a); items (a)-(c); Section 4.2 attention).
 // mode 0: logp [N, V] full log-softmax; mode 1: top-K (logp [N, K], ids [N, K]); mode 2 (beam search):
 // stop after the generator, leaving its per-tile partials in the step workspace for the beam step.
-// want/want_logit (optional): the logit of column want[r] of every row is copied to want_logit[r].
+// Optional work of a decoder step beyond the log-distribution.
+struct StepExtras {
+  const int32_t* want = nullptr;        // the logit of column want[r] of every row goes to want_logit[r]
+  float* want_logit = nullptr;
+  const Coverage* cov = nullptr;        // attention coverage and its penalty
+  int32_t* align = nullptr;             // attention argmax per row
+  const uint32_t* banned_bits = nullptr;   // hypothesis filters of the generator's top-K lists
+  const int32_t* unk_cnt = nullptr;
+  int unk_id = 0, max_unk = -1;
+  float* pfmax = nullptr;
+};
+
 int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const State& in, const State& out,
                    const int32_t* prev_tok, const int32_t* parent, int mode, float* logp, int32_t* ids, float* lse,
-                   float* attn, const StepWs& sw, hipStream_t st, const int32_t* want = nullptr,
-                   float* want_logit = nullptr, const Coverage* cov = nullptr) {
+                   float* attn, const StepWs& sw, hipStream_t st, const StepExtras& ex = StepExtras{}) {
   const Dims& d = m->d;
   const int N = B * K;
   const size_t LH = (size_t)N * d.H;
@@ -864,7 +883,8 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     HIP_TRY(gemm_lstm(d.bf16, small_shape(N, m->dec_w[l].Np), a, bop(m->dec_w[l]), lp, st));
   }
   const float* q = out.h + (d.L - 1) * LH;
-  HIP_TRY(attention(q, d.H, w.keys, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.scores, sw.ctx, attn, cov, st));
+  const AttnExtra ax{ex.cov, ex.align};
+  HIP_TRY(attention(q, d.H, w.keys, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.scores, sw.ctx, attn, ax, st));
   {
     AOp a{};
     a.M = N;
@@ -890,8 +910,13 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     gp.pid = sw.pid;
     gp.logits = mode == 0 ? logp : nullptr;
     gp.ld_logits = d.Vt;
-    gp.want = want;
-    gp.want_logit = want_logit;
+    gp.want = ex.want;
+    gp.want_logit = ex.want_logit;
+    gp.banned_bits = ex.banned_bits;
+    gp.unk_cnt = ex.unk_cnt;
+    gp.unk_id = ex.unk_id;
+    gp.max_unk = ex.max_unk;
+    gp.pfmax = ex.pfmax;
     time_begin(m, st);
     HIP_TRY(gemm_gen(d.bf16, a, bop(m->W_s), gp, st));
     time_end(m, st);
@@ -1003,13 +1028,18 @@ size_t onmt_search_ws_bytes(const onmt_model* m, int B, int S, const onmt_search
 
 int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int B, int S,
                      const onmt_search_params* prm, void* ws, size_t ws_bytes, int32_t* out_tok, int32_t* out_len,
-                     double* out_raw, double* out_norm, float* out_tok_logp, const onmt_trace* trace, void* stream) {
+                     double* out_raw, double* out_norm, float* out_tok_logp, int32_t* out_align,
+                     const onmt_trace* trace, void* stream) {
   if (!m || !prm || !ws) return fail(ONMT_EINVAL, "NULL argument");
   if (!out_tok || !out_len || !out_raw || !out_norm) return fail(ONMT_EINVAL, "NULL output pointer");
   const int K = prm->beam, T = prm->max_len;
   if (T < 1 || T > 100000) return fail(ONMT_EINVAL, "max_len %d outside [1, 100000]", T);
   if (!(prm->alpha >= 0.0) || !std::isfinite(prm->alpha)) return fail(ONMT_EINVAL, "alpha must be finite and >= 0");
   if (!(prm->beta >= 0.0) || !std::isfinite(prm->beta)) return fail(ONMT_EINVAL, "beta must be finite and >= 0");
+  if (prm->n_banned < 0 || (prm->n_banned > 0 && !prm->banned)) return fail(ONMT_EINVAL, "banned list invalid");
+  for (int i = 0; i < prm->n_banned; ++i)
+    if (prm->banned[i] < 0 || prm->banned[i] >= m->cfg.tgt_vocab)
+      return fail(ONMT_EINVAL, "banned[%d] = %d outside [0, %d)", i, prm->banned[i], m->cfg.tgt_vocab);
   if (trace && (!trace->slot || !trace->tok || !trace->cand || !trace->steps))
     return fail(ONMT_EINVAL, "trace given with a NULL array");
   if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
@@ -1043,6 +1073,26 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   if (rc) return rc;
   const bool coverage = prm->beta > 0.0;
   bp.cp = coverage ? w.cp : nullptr;
+  const bool filtering = prm->n_banned > 0 || prm->max_unk >= 0;
+  bp.unk_cnt = filtering ? bp.unk_cnt : nullptr;
+  bp.unk_id = m->cfg.unk_id;
+  bp.align = out_align ? w.step.align : nullptr;
+  std::vector<uint32_t> bits;
+  if (prm->n_banned > 0) {
+    bits.assign((size_t)(m->cfg.tgt_vocab + 31) / 32, 0u);
+    for (int i = 0; i < prm->n_banned; ++i) bits[prm->banned[i] >> 5] |= 1u << (prm->banned[i] & 31);
+    HIP_TRY(hipMemcpyAsync(w.banned_bits, bits.data(), bits.size() * sizeof(uint32_t), hipMemcpyHostToDevice, st));
+  }
+  StepExtras ex;
+  ex.align = bp.align ? w.step.align : nullptr;
+  if (filtering) {
+    ex.banned_bits = prm->n_banned > 0 ? w.banned_bits : nullptr;
+    ex.unk_cnt = prm->max_unk >= 0 ? bp.unk_cnt : nullptr;
+    ex.unk_id = m->cfg.unk_id;
+    ex.max_unk = prm->max_unk;
+    ex.pfmax = w.step.pfmax;
+    gp.pfmax = w.step.pfmax;
+  }
   HIP_TRY(beam_init(bp, m->cfg.bos_id, st));
   if (coverage) HIP_TRY(fill_f32(w.cov[0], (size_t)B * K * S, 0.f, st));
   const int every = prm->check_every > 0 ? prm->check_every : (T <= 32 ? 1 : 8);
@@ -1050,8 +1100,9 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   for (int t = 1; t <= T; ++t) {
     // coverage of the rows' hypotheses: the parents' coverage (previous layout) plus this step's weights
     const Coverage cv{w.cov[cur], w.cov[cur ^ 1], bp.parent, prm->beta, w.cp};
+    ex.cov = coverage ? &cv : nullptr;
     rc = decode_compute(m, w.enc, B, S, K, w.st[cur], w.st[cur ^ 1], bp.tok, bp.parent, 2, nullptr, nullptr,
-                        nullptr, nullptr, w.step, st, nullptr, nullptr, coverage ? &cv : nullptr);
+                        nullptr, nullptr, w.step, st, ex);
     if (rc) return rc;
     HIP_TRY(beam_step(bp, gp, t, st));
     cur ^= 1;
@@ -1062,7 +1113,7 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
       if (done >= B) break;
     }
   }
-  HIP_TRY(backtrack(bp, out_tok, out_len, out_raw, out_norm, out_tok_logp, st));
+  HIP_TRY(backtrack(bp, out_tok, out_len, out_raw, out_norm, out_tok_logp, out_align, st));
   if (trace) HIP_TRY(hipMemcpyAsync(trace->steps, bp.steps, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipStreamSynchronize(st));
   if (m->prof) time_collect(m);
@@ -1124,8 +1175,11 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
   HIP_TRY(fill_f64(w.nll, B, 0.0, st));
   int cur = 0;
   for (int t = 0; t < steps; ++t) {
+    StepExtras ex;
+    ex.want = w.want + (size_t)t * B;
+    ex.want_logit = w.want_logit;
     rc = decode_compute(m, w.enc, B, S, 1, w.st[cur], w.st[cur ^ 1], w.in_tok + (size_t)t * B, nullptr, 2, nullptr,
-                        nullptr, nullptr, nullptr, w.step, st, w.want + (size_t)t * B, w.want_logit);
+                        nullptr, nullptr, nullptr, w.step, st, ex);
     if (rc) return rc;
     HIP_TRY(score_step(w.step.pmax, w.step.psum, w.step.ntiles, w.want_logit, w.tlen, B, t, out_logp, T, w.nll, st));
     cur ^= 1;

@@ -138,18 +138,22 @@ class Translator:
         return out_state, logp, ids, lse, attn
 
     # ---------------------------------------------------------------- search
-    def search_buffers(self, B, S, beam, max_len, alpha=0.0, check_every=0, trace=False, beta=0.0):
+    def search_buffers(self, B, S, beam, max_len, alpha=0.0, check_every=0, trace=False, beta=0.0, max_unk=-1,
+                       banned=(), align=False):
         """Allocate everything one onmt_beam_search call needs (reusable across calls)."""
-        p = OnmtSearchParams(beam, max_len, float(alpha), check_every, float(beta))
+        banned_arr = (ctypes.c_int32 * max(len(banned), 1))(*[int(x) for x in banned])
+        p = OnmtSearchParams(beam, max_len, float(alpha), check_every, float(beta), int(max_unk),
+                             ctypes.cast(banned_arr, ctypes.c_void_p) if len(banned) else None, len(banned))
         n = self.lib.onmt_search_ws_bytes(self.handle, B, S, ctypes.byref(p))
         d = self.device
         buf = {
-            "params": p, "ws": _bytes(n, d), "ws_bytes": n,
+            "params": p, "banned": banned_arr, "ws": _bytes(n, d), "ws_bytes": n,
             "tok": torch.empty(B, max_len, dtype=torch.int32, device=d),
             "len": torch.empty(B, dtype=torch.int32, device=d),
             "raw": torch.empty(B, dtype=torch.float64, device=d),
             "norm": torch.empty(B, dtype=torch.float64, device=d),
             "tok_logp": torch.empty(B, max_len, dtype=torch.float32, device=d),
+            "align": torch.empty(B, max_len, dtype=torch.int32, device=d) if align else None,
             "trace": None,
         }
         if trace:
@@ -164,10 +168,18 @@ class Translator:
     def beam_search(self, src, lens, buf):
         B, S = src.shape
         tr = ctypes.byref(buf["trace"]) if buf["trace"] is not None else None
+        al = _ptr(buf["align"]) if buf.get("align") is not None else None
         check(self.lib.onmt_beam_search(self.handle, _ptr(src), _ptr(lens), B, S, ctypes.byref(buf["params"]),
                                         _ptr(buf["ws"]), buf["ws_bytes"], _ptr(buf["tok"]), _ptr(buf["len"]),
-                                        _ptr(buf["raw"]), _ptr(buf["norm"]), _ptr(buf["tok_logp"]), tr, _stream()))
+                                        _ptr(buf["raw"]), _ptr(buf["norm"]), _ptr(buf["tok_logp"]), al, tr,
+                                        _stream()))
         return buf
+
+    @staticmethod
+    def replace_unk(tokens, align, src_row, unk_id):
+        """Unknown-word replacement on the host (Section 4.2 OOV handling): each UNK output token takes
+        the source token at its aligned position; returns ('src', id) for copied tokens, ('tgt', id) else."""
+        return [("src", int(src_row[a])) if int(t) == unk_id else ("tgt", int(t)) for t, a in zip(tokens, align)]
 
     # ---------------------------------------------------------------- teacher-forced scoring
     def score_buffers(self, B, S, T):

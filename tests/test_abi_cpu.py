@@ -77,7 +77,7 @@ def test_null_handles_are_rejected_without_a_device():
     assert lib.onmt_model_destroy(None) == _lib.ONMT_EINVAL
     assert lib.onmt_encode(None, None, None, 1, 1, None, 0, None) == _lib.ONMT_EINVAL
     assert lib.onmt_beam_search(None, None, None, 1, 1, None, None, 0, None, None, None, None, None, None,
-                                None) == _lib.ONMT_EINVAL
+                                None, None) == _lib.ONMT_EINVAL
     n = ctypes.c_int()
     ms = ctypes.c_double()
     assert lib.onmt_profile_read(None, ctypes.byref(n), ctypes.byref(ms), 0) == _lib.ONMT_EINVAL

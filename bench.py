@@ -37,6 +37,10 @@ def parse():
                     help="search: beam search (the headline metric); score: teacher-forced scoring of "
                          "max-decode-long synthetic targets")
     ap.add_argument("--beta", type=float, default=0.0, help="coverage penalty weight of the search (0 = off)")
+    ap.add_argument("--banned", type=int, default=0,
+                    help="ban this many target ids (4, 4 + 7, 4 + 14, ...) from every hypothesis (0 = none)")
+    ap.add_argument("--max-unk", type=int, default=-1, help="at most this many UNK tokens per hypothesis (-1 = no limit)")
+    ap.add_argument("--align", action="store_true", help="also return attention-argmax alignments of the outputs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sentences", type=int, default=4)
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -82,13 +86,18 @@ def cpu_threads():
         return len(os.sched_getaffinity(0))
 
 
-def cpu_baseline(w, weights, src, lens, n_sent, beta=0.0):
+def banned_ids(w, n):
+    return tuple(range(4, 4 + 7 * n, 7)) if n else ()
+
+
+def cpu_baseline(w, weights, src, lens, n_sent, beta=0.0, banned=(), max_unk=-1):
     """The oracle (fp64 NumPy) on the first n_sent sentences of the same batch, on this host's cores."""
     from oracle import onmt_oracle as O
     threads = cpu_threads()
     m = O.model_from(w, weights)
     t0 = time.perf_counter()
-    res = O.beam_search(m, src[:n_sent], lens[:n_sent], w.beam, w.max_len, w.alpha, beta=beta)
+    res = O.beam_search(m, src[:n_sent], lens[:n_sent], w.beam, w.max_len, w.alpha, beta=beta, banned=banned,
+                        max_unk=max_unk)
     dt = time.perf_counter() - t0
     toks = int(sum(len(t) for t in res.tokens))
     return {"value": round(toks / dt, 3), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
@@ -122,7 +131,11 @@ def main():
     lens_d = torch.from_numpy(lens).cuda()
     if args.mode == "score":
         return bench_score(args, w, weights, tr, src, lens, src_d, lens_d)
-    buf = tr.search_buffers(B, S, w.beam, w.max_len, w.alpha, beta=args.beta)
+    banned = banned_ids(w, args.banned)
+    if banned and banned[-1] >= w.tgt_vocab:
+        sys.exit(f"--banned {args.banned} reaches past the target vocabulary ({w.tgt_vocab})")
+    buf = tr.search_buffers(B, S, w.beam, w.max_len, w.alpha, beta=args.beta, banned=banned,
+                            max_unk=args.max_unk, align=args.align)
 
     for i in range(args.warmup):
         tr.beam_search(src_d, lens_d, buf)
@@ -170,7 +183,10 @@ def main():
         "config": {"workload": f"{w.name}: {w.enc_layers}x{w.hidden} LSTM enc/dec, emb {w.emb}, vocab {w.tgt_vocab}, "
                                f"batch {w.batch}, src len {w.len_lo}-{w.len_hi}, beam {w.beam}, "
                                f"max decode {w.max_len}, alpha {w.alpha}, {w.wdtype}"
-                               + (f", coverage beta {args.beta}" if args.beta else ""),
+                               + (f", coverage beta {args.beta}" if args.beta else "")
+                               + (f", {len(banned)} banned ids" if banned else "")
+                               + (f", max {args.max_unk} UNK" if args.max_unk >= 0 else "")
+                               + (", attention alignments" if args.align else ""),
                    "global_batch": B, "beam": w.beam, "max_decode": w.max_len,
                    "target_tokens_per_step": tokens // max(args.steps, 1)},
         "step_ms": {"min": round(min(step_s) * 1e3, 3), "median": round(sorted(step_s)[len(step_s) // 2] * 1e3, 3),
@@ -182,7 +198,8 @@ def main():
                      "flops_per_launch": gen_flops},
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, weights, src, lens, args.cpu_sentences, args.beta)
+        out["cpu_baseline"] = cpu_baseline(w, weights, src, lens, args.cpu_sentences, args.beta, banned,
+                                           args.max_unk)
     print(json.dumps(out), flush=True)
 
 

@@ -59,6 +59,10 @@ R18 Hypothesis filters (Section 4.2: constraints such as a maximum number of OOV
 R19 Unknown-word replacement (Section 4.2 OOV handling, citing Luong et al. 2015b): every output token
     is aligned to the source position with the largest attention weight of its step (smaller position
     on ties); an UNK output takes the source token there.
+R20 Attention types (Section 4.2 names general, dot product and concatenation, citing Luong et al.
+    2015 and Britz et al. 2017), all without biases: "dot" e_s = q^T m_s (the memory width equals H);
+    "concat" e_s = v_a^T tanh(W_a [q ; m_s]) with W_a [H, H + Hm] (attention size H, query columns
+    first) and v_a [H]. Softmax, context and the attentional vector are the same for every type.
 R17 Coverage normalisation (named with length normalisation in Section 4.2, citing GNMT): a finished
     hypothesis is ranked by raw / lp(n) + beta * sum over the real source positions of
     log(min(c_i, 1)), c_i = the attention it put on position i summed over its steps (EOS included);
@@ -95,6 +99,7 @@ class Model:
     src_vocab: int
     tgt_vocab: int
     w: dict = field(repr=False)
+    attn: str = "general"
 
     @property
     def enc_hidden(self):
@@ -104,7 +109,7 @@ class Model:
 def model_from(workload, weights) -> Model:
     return Model(workload.enc_layers, workload.dec_layers, workload.bidirectional,
                  workload.emb, workload.hidden, workload.src_vocab, workload.tgt_vocab,
-                 {k: np.asarray(v, dtype=F64) for k, v in weights.items()})
+                 {k: np.asarray(v, dtype=F64) for k, v in weights.items()}, workload.attn)
 
 
 # --------------------------------------------------------------------------
@@ -207,15 +212,27 @@ def init_state(m: Model, enc: Encoded, K: int) -> State:
                  np.zeros((N, m.hidden), F64))
 
 
+def attention_scores(m: Model, q, memory):
+    """Raw scores e [N, S] of rows q [N, H] against per-row memory [N, S, Hm] (R6, R20)."""
+    if m.attn == "general":
+        Wm = memory @ m.w["W_a"].T                           # W_a m_s, [N, S, H]
+        return np.einsum("nh,nsh->ns", q, Wm)
+    if m.attn == "dot":
+        return np.einsum("nh,nsh->ns", q, memory)
+    if m.attn == "concat":
+        N, S, _ = memory.shape
+        qm = np.concatenate([np.broadcast_to(q[:, None, :], (N, S, q.shape[-1])), memory], axis=-1)
+        return np.tanh(qm @ m.w["W_a"].T) @ m.w["v_a"]       # v_a . tanh(W_a [q ; m_s])
+    raise ValueError(f"unknown attention type {m.attn!r}")
+
+
 def attention(m: Model, q, memory, mask):
-    """Global "general" attention for rows q [N, H] over their sentences' memory.
+    """Global attention for rows q [N, H] over their sentences' memory (type m.attn).
 
     memory [N, S, Hm] and mask [N, S] are already per row. Returns (a [N, S],
-    ctx [N, Hm], h_tilde [N, H]). R4, R6.
+    ctx [N, Hm], h_tilde [N, H]). R4, R6, R20.
     """
-    Wm = memory @ m.w["W_a"].T                               # W_a m_s, [N, S, H]
-    e = np.einsum("nh,nsh->ns", q, Wm)
-    e = np.where(mask, e, -np.inf)
+    e = np.where(mask, attention_scores(m, q, memory), -np.inf)
     e_max = e.max(axis=1, keepdims=True)
     p = np.exp(e - e_max)                                    # exactly 0 on pads
     a = p / p.sum(axis=1, keepdims=True)

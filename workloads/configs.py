@@ -33,6 +33,7 @@ class Workload:
     alpha: float          # GNMT length-normalisation exponent
     wdtype: str           # "fp32" or "bf16" (weights rounded to bfloat16, fp32 accumulation)
     zipf_s: float         # exponent of the bounded Zipf source-token distribution
+    attn: str = "general"  # attention score: "general" q.W_a m, "dot" q.m, "concat" v_a.tanh(W_a [q; m])
 
     @property
     def enc_hidden(self) -> int:

@@ -30,7 +30,8 @@ def weight_specs(w: Workload):
 
     Layouts are row-major. LSTM layer: ``W [4*Hl, in + Hl]`` with gate blocks
     (i, f, g, o) along rows and columns ``[input | recurrent]``; ``b [4*Hl]``.
-    Attention: ``W_a [H, Hm]``, ``W_c [H, Hm + H]`` with columns ``[ctx | h]``.
+    Attention: "general" ``W_a [H, Hm]``; "dot" no score weights; "concat" ``W_a [H, H + Hm]`` with
+    columns ``[query | memory]`` and ``v_a [H]``. Then ``W_c [H, Hm + H]`` with columns ``[ctx | h]``.
     Generator: ``W_s [V, H]``, ``b_s [V]``.
     """
     H, Hd, E = w.hidden, w.enc_hidden, w.emb
@@ -46,7 +47,13 @@ def weight_specs(w: Workload):
         n_in = E + H if l == 0 else H
         specs.append((f"dec{l}_W", (4 * H, n_in + H)))
         specs.append((f"dec{l}_b", (4 * H,)))
-    specs += [("W_a", (H, Hm)), ("W_c", (H, Hm + H)), ("W_s", (w.tgt_vocab, H)), ("b_s", (w.tgt_vocab,))]
+    if w.attn == "general":
+        specs.append(("W_a", (H, Hm)))
+    elif w.attn == "concat":
+        specs += [("W_a", (H, H + Hm)), ("v_a", (H,))]
+    elif w.attn != "dot":
+        raise ValueError(f"unknown attention type {w.attn!r}")
+    specs += [("W_c", (H, Hm + H)), ("W_s", (w.tgt_vocab, H)), ("b_s", (w.tgt_vocab,))]
     return specs
 
 
@@ -62,7 +69,7 @@ def round_bf16(a: np.ndarray) -> np.ndarray:
 def make_weights(w: Workload, seed: int = WEIGHT_SEED, peaked: bool = False):
     """Dict name -> float32 array, drawn in :func:`weight_specs` order.
 
-    ``peaked`` (tests only) scales W_a by 30 and W_s, b_s by 10 after drawing,
+    ``peaked`` (tests only) scales W_a (if any) by 30 and W_s, b_s by 10 after drawing,
     which makes attention non-uniform and widens the gaps between log-probs.
     """
     rng = np.random.Generator(np.random.PCG64(seed))
@@ -70,7 +77,8 @@ def make_weights(w: Workload, seed: int = WEIGHT_SEED, peaked: bool = False):
     for name, shape in weight_specs(w):
         out[name] = rng.uniform(-0.1, 0.1, size=shape).astype(np.float32)
     if peaked:
-        out["W_a"] = (out["W_a"] * np.float32(30.0)).astype(np.float32)
+        if "W_a" in out:
+            out["W_a"] = (out["W_a"] * np.float32(30.0)).astype(np.float32)
         out["W_s"] = (out["W_s"] * np.float32(10.0)).astype(np.float32)
         out["b_s"] = (out["b_s"] * np.float32(10.0)).astype(np.float32)
     if w.wdtype == "bf16":

@@ -125,7 +125,7 @@ def main():
     src, lens = W.make_batch(w)
     B, S = src.shape
     cfg = make_config(w.enc_layers, w.dec_layers, w.bidirectional, w.emb, w.hidden, w.src_vocab, w.tgt_vocab,
-                      w.wdtype)
+                      w.wdtype, attn=w.attn)
     tr = Translator(cfg, [weights[n] for n, _ in W.weight_specs(w)], device="cuda:0")
     src_d = torch.from_numpy(src).cuda()
     lens_d = torch.from_numpy(lens).cuda()

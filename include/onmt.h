@@ -5,17 +5,18 @@
  * The model is the one the OpenNMT paper (Klein et al., arXiv 1805.11462) describes in Section 2
  * ("Background") and Figure 1(a): a conditional language model p(w_1:T | x) = prod_t p(w_t | w_<t, x)
  * computed by a stacked (optionally bidirectional, Tables 3-4) LSTM encoder, an input-feeding LSTM
- * decoder (Section 2 item (c)) with global "general" attention (Section 4.2), a softmax generator and
- * beam search with length normalisation (Section 2 item (d); Section 4.2). The paper's deployment
- * section (Section 4.1, "C/Mobile/GPU Translation") describes a batched GPU translator and a C
- * implementation; this library is that translator behind a C ABI.
+ * decoder (Section 2 item (c)) with global attention of the general, dot or concat type (Section 4.2),
+ * a softmax generator and beam search with length normalisation (Section 2 item (d); Section 4.2). The
+ * paper's deployment section (Section 4.1, "C/Mobile/GPU Translation") describes a batched GPU
+ * translator and a C implementation; this library is that translator behind a C ABI.
  *
  * Where the paper is silent the library follows these readings: forget-gate LSTM without peepholes,
  * one bias per gate, gate order (i, f, g, o); zero initial encoder state; no source BOS/EOS; packed
  * padding (pads never update state, memory is 0 and attention weight exactly 0 at pads);
- * bidirectional final state [forward after last token ; backward after token 0]; score
- * q^T W_a m_s without bias; attentional vector tanh(W_c [ctx ; q]) without bias; input feed starts at
- * 0 and the first decoder layer sees [embedding ; feed]; generator with bias, nothing masked.
+ * bidirectional final state [forward after last token ; backward after token 0]; scores without
+ * biases (general q^T W_a m_s, dot q^T m_s, concat v_a^T tanh(W_a [q ; m_s])); attentional vector
+ * tanh(W_c [ctx ; q]) without bias; input feed starts at 0 and the first decoder layer sees
+ * [embedding ; feed]; generator with bias, nothing masked.
  *
  * Conventions for every function:
  *   - Return 0 (ONMT_OK) or a negative error code; never throw or abort. onmt_last_error() gives a
@@ -58,7 +59,13 @@ typedef struct {
   int wdtype;                      /* 0 = fp32 weights and products; 1 = bf16 weights and MFMA operands,
                                       fp32 accumulation, cell state and softmax */
   int pad_id, unk_id, bos_id, eos_id;
+  int attn_type;                   /* attention score (Section 4.2 names three types, none with biases):
+                                      ONMT_ATTN_GENERAL e_s = q . W_a m_s;
+                                      ONMT_ATTN_DOT     e_s = q . m_s;
+                                      ONMT_ATTN_CONCAT  e_s = v_a . tanh(W_a [q ; m_s]) */
 } onmt_config;
+
+enum { ONMT_ATTN_GENERAL = 0, ONMT_ATTN_DOT = 1, ONMT_ATTN_CONCAT = 2 };
 
 /* Beam search settings (Section 2 item (d); Section 4.2 length and attention coverage normalisation,
  * GNMT forms lp(n) = ((5 + n) / 6)^alpha and cp = beta * sum over the real source positions i of
@@ -100,7 +107,9 @@ const char* onmt_last_error(void);
  * b [4*Hd], with Hd = hidden (/2 if bidirectional) and in = emb for l = 0, hidden above; E_tgt
  * [tgt_vocab, emb]; for each decoder layer l: W [4*hidden, in + hidden] with in = emb + hidden for
  * l = 0 (columns [embedding | input feed | recurrent]) and hidden above, b [4*hidden];
- * W_a [hidden, hidden]; W_c [hidden, 2*hidden] (columns [context | decoder state]);
+ * attention score weights: general W_a [hidden, hidden], dot none, concat W_a [hidden, 2*hidden]
+ * (columns [decoder state | memory]) then v_a [hidden]; W_c [hidden, 2*hidden] (columns
+ * [context | decoder state]);
  * W_s [tgt_vocab, hidden]; b_s [tgt_vocab]. Returns < 0 for an invalid config. */
 int onmt_num_weights(const onmt_config* cfg);
 int64_t onmt_weight_numel(const onmt_config* cfg, int i);
@@ -119,7 +128,8 @@ int onmt_model_destroy(onmt_model* model);
 /* ---- Encoder (Section 2: encoder RNN over word vectors; Figure 1(a)) -------------------------------
  * src [B, S_max] int32 token ids (device), len [B] int32 true lengths (device), 1 <= len[b] <= S_max,
  * ids in [0, src_vocab). Positions >= len[b] are ignored. Writes the memory bank, the attention keys
- * W_a m_s and the final states into enc_ws (>= onmt_encode_ws_bytes(model, B, S_max)), which the
+ * (general: W_a m_s; concat: the memory columns of W_a times m_s; dot: none, the scores read the
+ * memory) and the final states into enc_ws (>= onmt_encode_ws_bytes(model, B, S_max)), which the
  * decoder calls then read. Copies src and len to the host to validate them (one stream sync), then
  * enqueues the encoder asynchronously. */
 size_t onmt_encode_ws_bytes(const onmt_model* model, int B, int S_max);

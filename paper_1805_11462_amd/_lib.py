@@ -16,7 +16,8 @@ ERROR_NAMES = {ONMT_EINVAL: "EINVAL", ONMT_ESIZE: "ESIZE", ONMT_EDEVICE: "EDEVIC
 
 class OnmtConfig(ctypes.Structure):
     _fields_ = [(n, c_int) for n in ("enc_layers", "dec_layers", "bidirectional", "emb", "hidden", "src_vocab",
-                                     "tgt_vocab", "wdtype", "pad_id", "unk_id", "bos_id", "eos_id")]
+                                     "tgt_vocab", "wdtype", "pad_id", "unk_id", "bos_id", "eos_id",
+                                     "attn_type")]
 
 
 class OnmtSearchParams(ctypes.Structure):

@@ -1,9 +1,13 @@
-// Global "general" attention over the source memory (Section 2 attention pooling; Section 4.2 attention
-// types; Figure 1(a) caption).
+// Global attention over the source memory (Section 2 attention pooling; Section 4.2 attention types;
+// Figure 1(a) caption).
 //
-// score e[k, s] = q_k . keys[s] with keys = W_a m_s precomputed once per batch; pads (s >= n_b) are
-// excluded, so their weight is exactly zero; a[k, :] = softmax over the real positions;
-// ctx_k = sum_s a[k, s] m_s.
+// Scores, with keys precomputed once per batch:
+//   general  e[k, s] = q_k . keys[s], keys = W_a m_s;
+//   dot      e[k, s] = q_k . m_s (the keys are the memory);
+//   concat   e[k, s] = v_a . tanh(q'_k + keys[s]), q'_k = W_q q_k (one GEMM per step), keys = W_m m_s,
+//            where W_a = [W_q | W_m] splits the score's weight into its query and memory columns.
+// Pads (s >= n_b) are excluded, so their weight is exactly zero; a[k, :] = softmax over the real
+// positions; ctx_k = sum_s a[k, s] m_s.
 //
 // The step moves a few hundred KB per sentence, so it is bound by how many loads are in flight, not by
 // arithmetic. It runs as two launches that each issue all of their loads up front:
@@ -28,10 +32,24 @@ constexpr int kCtxBatch = 4;                                // memory rows in fl
 constexpr int kCtxTargetBlocks = 256;                       // at least one workgroup per CU when B allows
 constexpr size_t kAttnLdsLimit = 64 * 1024;
 
-// e [B*K, S_max]: raw scores of the real positions (pads are never written).
-template <int KMAX>
+// tanh(x) = 1 - 2 / (exp(2x) + 1) with the hardware exponential and reciprocal; it saturates to +-1 for
+// large |x| (the exponential overflows to inf or underflows to 0). Absolute error about 1e-7.
+__device__ inline float tanh_fast(float x) { return 1.f - 2.f * __builtin_amdgcn_rcpf(__expf(2.f * x) + 1.f); }
+
+template <bool CONCAT>
+__device__ inline float score_term(float4 k, float4 q, float4 v) {
+  if (CONCAT)
+    return v.x * tanh_fast(k.x + q.x) + v.y * tanh_fast(k.y + q.y) + v.z * tanh_fast(k.z + q.z) +
+           v.w * tanh_fast(k.w + q.w);
+  return k.x * q.x + k.y * q.y + k.z * q.z + k.w * q.w;
+}
+
+// e [B*K, S_max]: raw scores of the real positions (pads are never written). v: concat's v_a [H], unused
+// otherwise.
+template <int KMAX, bool CONCAT>
 __global__ __launch_bounds__(kScoreThreads) void k_attn_scores(const float* __restrict__ q, int ld_q,
                                                                const float* __restrict__ keys,
+                                                               const float* __restrict__ v,
                                                                const int32_t* __restrict__ lens, int S_max, int H,
                                                                int K, int nchunk, float* __restrict__ e) {
   extern __shared__ __attribute__((aligned(16))) float qs[];      // [K][H]
@@ -50,6 +68,12 @@ __global__ __launch_bounds__(kScoreThreads) void k_attn_scores(const float* __re
   for (int j = 0; j < kScoreChunks; ++j) {
     const int c = sub + j * kScoreLanes;
     kv[j] = c < H4 ? *(const float4*)(kr + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  float4 vv[kScoreChunks];
+#pragma unroll
+  for (int j = 0; j < kScoreChunks; ++j) {
+    const int c = sub + j * kScoreLanes;
+    vv[j] = CONCAT && c < H4 ? *(const float4*)(v + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   // the sentence's K query rows to LDS, all loads issued before the first store
   const int r0 = b * K;
@@ -76,8 +100,7 @@ __global__ __launch_bounds__(kScoreThreads) void k_attn_scores(const float* __re
       for (int j = 0; j < kScoreChunks; ++j) {
         const int c = sub + j * kScoreLanes;
         if (c < H4) {
-          const float4 qv = *(const float4*)(qs + k * H + 4 * c);
-          acc[k] += kv[j].x * qv.x + kv[j].y * qv.y + kv[j].z * qv.z + kv[j].w * qv.w;
+          acc[k] += score_term<CONCAT>(kv[j], *(const float4*)(qs + k * H + 4 * c), vv[j]);
         }
       }
     }
@@ -273,25 +296,36 @@ static void launch_context(int pl, dim3 grid, size_t lds, hipStream_t st, const 
   }
 }
 
-hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens, int B,
-                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, const AttnExtra& ex,
-                     hipStream_t st) {
+template <bool CONCAT>
+static void launch_scores(int K, dim3 grid, size_t lds, hipStream_t st, const float* q, int ld_q,
+                          const float* keys, const float* v, const int32_t* lens, int S_max, int H, int nchunk,
+                          float* e) {
+  const dim3 block(kScoreThreads);
+  if (K <= 1)
+    hipLaunchKernelGGL((k_attn_scores<1, CONCAT>), grid, block, lds, st, q, ld_q, keys, v, lens, S_max, H, K, nchunk, e);
+  else if (K <= 2)
+    hipLaunchKernelGGL((k_attn_scores<2, CONCAT>), grid, block, lds, st, q, ld_q, keys, v, lens, S_max, H, K, nchunk, e);
+  else if (K <= 4)
+    hipLaunchKernelGGL((k_attn_scores<4, CONCAT>), grid, block, lds, st, q, ld_q, keys, v, lens, S_max, H, K, nchunk, e);
+  else if (K <= 8)
+    hipLaunchKernelGGL((k_attn_scores<8, CONCAT>), grid, block, lds, st, q, ld_q, keys, v, lens, S_max, H, K, nchunk, e);
+  else
+    hipLaunchKernelGGL((k_attn_scores<16, CONCAT>), grid, block, lds, st, q, ld_q, keys, v, lens, S_max, H, K, nchunk, e);
+}
+
+hipError_t attention(const float* q, int ld_q, const float* keys, const float* v_a, const float* mem,
+                     const int32_t* lens, int B, int S_max, int H, int Hm, int K, float* scores, float* ctx,
+                     float* attn, const AttnExtra& ex, hipStream_t st) {
   const Coverage cv = ex.cov ? *ex.cov : Coverage{};
   if (H / 4 > kScoreLanes * kScoreChunks || H % 4 || Hm % 4 || K < 1 || K > kMaxBeam) return hipErrorInvalidValue;
   if (attention_lds_bytes(S_max, H, K) > kAttnLdsLimit) return hipErrorInvalidValue;
   const int nchunk = (S_max + kScorePos - 1) / kScorePos;
-  const dim3 sgrid(B * nchunk), sblock(kScoreThreads);
+  const dim3 sgrid(B * nchunk);
   const size_t slds = (size_t)K * H * sizeof(float);
-  if (K <= 1)
-    hipLaunchKernelGGL(k_attn_scores<1>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
-  else if (K <= 2)
-    hipLaunchKernelGGL(k_attn_scores<2>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
-  else if (K <= 4)
-    hipLaunchKernelGGL(k_attn_scores<4>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
-  else if (K <= 8)
-    hipLaunchKernelGGL(k_attn_scores<8>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
+  if (v_a)
+    launch_scores<true>(K, sgrid, slds, st, q, ld_q, keys, v_a, lens, S_max, H, nchunk, scores);
   else
-    hipLaunchKernelGGL(k_attn_scores<16>, sgrid, sblock, slds, st, q, ld_q, keys, lens, S_max, H, K, nchunk, scores);
+    launch_scores<false>(K, sgrid, slds, st, q, ld_q, keys, v_a, lens, S_max, H, nchunk, scores);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
 

@@ -121,9 +121,10 @@ struct AttnExtra {
   int32_t* align;               // [N]: position of the largest weight (smaller position on ties)
 };
 
-hipError_t attention(const float* q, int ld_q, const float* keys, const float* mem, const int32_t* lens, int B,
-                     int S_max, int H, int Hm, int K, float* scores, float* ctx, float* attn, const AttnExtra& ex,
-                     hipStream_t st);
+// v_a != nullptr selects concat scores v_a . tanh(q_k + keys[s]) (q = the projected query); else q_k . keys[s].
+hipError_t attention(const float* q, int ld_q, const float* keys, const float* v_a, const float* mem,
+                     const int32_t* lens, int B, int S_max, int H, int Hm, int K, float* scores, float* ctx,
+                     float* attn, const AttnExtra& ex, hipStream_t st);
 size_t attention_lds_bytes(int S_max, int H, int K);
 
 hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pval, const int32_t* pid, int M,

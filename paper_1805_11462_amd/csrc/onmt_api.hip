@@ -64,6 +64,7 @@ struct Dims {
   int Hd_pad, H_pad;   // units padded to multiples of 32 (gate-blocked groups, 128-column tiles)
   bool bf16;
   int esz;             // operand element size
+  int attn;            // ONMT_ATTN_GENERAL / _DOT / _CONCAT
   // Every K segment of a GEMM operand is padded to a multiple of kSegK so that no K stage of any tile
   // shape straddles two segments.
   int pad(int w) const { return ceil_to(w, kSegK); }
@@ -83,6 +84,7 @@ bool dims_of(const onmt_config* c, Dims* d) {
   d->H_pad = ceil_to(d->H, 32);
   d->bf16 = c->wdtype == 1;
   d->esz = d->bf16 ? 2 : 4;
+  d->attn = c->attn_type;
   return true;
 }
 
@@ -93,6 +95,8 @@ int check_config(const onmt_config* c) {
     return fail(ONMT_EINVAL, "enc_layers (%d) must equal dec_layers (%d)", c->enc_layers, c->dec_layers);
   if (c->bidirectional != 0 && c->bidirectional != 1) return fail(ONMT_EINVAL, "bidirectional must be 0 or 1");
   if (c->wdtype != 0 && c->wdtype != 1) return fail(ONMT_EINVAL, "wdtype must be 0 (fp32) or 1 (bf16)");
+  if (c->attn_type < ONMT_ATTN_GENERAL || c->attn_type > ONMT_ATTN_CONCAT)
+    return fail(ONMT_EINVAL, "attn_type must be 0 (general), 1 (dot) or 2 (concat)");
   if (c->emb < 4 || c->hidden < 4 || c->src_vocab < 1 || c->tgt_vocab < 4)
     return fail(ONMT_EINVAL, "emb/hidden >= 4, src_vocab >= 1, tgt_vocab >= 4 required");
   if (c->emb > 8192 || c->hidden > 8192 || c->enc_layers > 64) return fail(ONMT_EUNSUPPORTED, "model too large");
@@ -130,7 +134,11 @@ std::vector<WeightSpec> weight_specs(const onmt_config* c) {
     v.push_back({4LL * d.H, in + d.H});
     v.push_back({4LL * d.H, 1});
   }
-  v.push_back({d.H, d.Hm});
+  if (d.attn == ONMT_ATTN_GENERAL) v.push_back({d.H, d.Hm});
+  if (d.attn == ONMT_ATTN_CONCAT) {
+    v.push_back({d.H, d.H + d.Hm});
+    v.push_back({d.H, 1});
+  }
   v.push_back({d.H, d.Hm + d.H});
   v.push_back({d.Vt, d.H});
   v.push_back({d.Vt, 1});
@@ -159,7 +167,10 @@ struct onmt_model {
   std::vector<Packed> enc_xh;              // unidirectional layers >= 1: [4 Hd_pad, pad(in) + pad(Hd)]
   std::vector<Packed> dec_w;               // per layer [4 H_pad, sum of padded segment widths]
   std::vector<const float*> dec_bias;      // per layer [4 H_pad]
-  Packed W_a, W_c, W_s;
+  Packed W_a;                              // memory side of the score: general W_a, concat's memory columns
+  Packed W_q;                              // concat: the query columns of W_a
+  const float* v_a = nullptr;              // concat [H]
+  Packed W_c, W_s;
   const float* b_s = nullptr;
   // kernel timing
   int prof = 0;              // time every prof-th generator launch (0: off)
@@ -215,7 +226,9 @@ size_t model_layout(const onmt_config* c, onmt_model* m) {
     dw.push_back(mat(4 * d.H_pad, kp));
     db.push_back(vec((size_t)4 * d.H_pad));
   }
-  Packed wa = mat(ceil_to(d.H, 128), d.pad(d.Hm));
+  Packed wa = d.attn != ONMT_ATTN_DOT ? mat(ceil_to(d.H, 128), d.pad(d.Hm)) : Packed{};
+  Packed wq = d.attn == ONMT_ATTN_CONCAT ? mat(ceil_to(d.H, 128), d.pad(d.H)) : Packed{};
+  const size_t va = d.attn == ONMT_ATTN_CONCAT ? vec(d.H) : 0;
   Packed wc = mat(ceil_to(d.H, 128), d.pad(d.Hm) + d.pad(d.H));
   Packed ws = mat(ceil_to(d.Vt, 128), d.pad(d.H));
   size_t bs = vec(ceil_to(d.Vt, 128));
@@ -234,7 +247,11 @@ size_t model_layout(const onmt_config* c, onmt_model* m) {
     for (auto& p : exh) m->enc_xh.push_back(fix(p));
     for (auto& p : dw) m->dec_w.push_back(fix(p));
     for (auto o : db) m->dec_bias.push_back((const float*)(base + o));
-    m->W_a = fix(wa);
+    if (d.attn != ONMT_ATTN_DOT) m->W_a = fix(wa);
+    if (d.attn == ONMT_ATTN_CONCAT) {
+      m->W_q = fix(wq);
+      m->v_a = (const float*)(base + va);
+    }
     m->W_c = fix(wc);
     m->W_s = fix(ws);
     m->b_s = (const float*)(base + bs);
@@ -371,8 +388,19 @@ int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, 
       }
   }
   {
-    const float* Wa = host_weights[wi++];
-    for (int r = 0; r < d.H; ++r) pack_row(img, m->W_a, r, 0, Wa + (size_t)r * d.Hm, 0, d.Hm);
+    if (d.attn == ONMT_ATTN_GENERAL) {
+      const float* Wa = host_weights[wi++];
+      for (int r = 0; r < d.H; ++r) pack_row(img, m->W_a, r, 0, Wa + (size_t)r * d.Hm, 0, d.Hm);
+    } else if (d.attn == ONMT_ATTN_CONCAT) {   // columns [query | memory]
+      const float* Wa = host_weights[wi++];
+      for (int r = 0; r < d.H; ++r) {
+        pack_row(img, m->W_q, r, 0, Wa + (size_t)r * (d.H + d.Hm), 0, d.H);
+        pack_row(img, m->W_a, r, 0, Wa + (size_t)r * (d.H + d.Hm), d.H, d.Hm);
+      }
+      const float* va = host_weights[wi++];
+      const size_t vo = off_of(m->v_a);
+      for (int r = 0; r < d.H; ++r) img.putf(vo, r, va[r]);
+    }
     const float* Wc = host_weights[wi++];
     for (int r = 0; r < d.H; ++r) {
       pack_row(img, m->W_c, r, 0, Wc + (size_t)r * (d.Hm + d.H), 0, d.Hm);
@@ -412,7 +440,7 @@ struct EncWs {
   int32_t* lens;
   int32_t* src;
   float* memory;     // [B*S, Hm]
-  float* keys;       // [B*S, H]
+  float* keys;       // [B*S, H]: W_a m_s (general), the memory-side term of concat, the memory itself (dot)
   float* final_h;    // [L, B, H]
   float* final_c;
   float* gx;         // [B*S, ndir * 4 Hd_pad]
@@ -430,7 +458,7 @@ size_t enc_layout(const Dims& d, int B, int S, char* base, EncWs* w) {
   t.lens = c.take<int32_t>(B);
   t.src = c.take<int32_t>(BS);
   t.memory = c.take<float>(BS * d.Hm);
-  t.keys = c.take<float>(BS * d.H);
+  t.keys = d.attn == ONMT_ATTN_DOT ? t.memory : c.take<float>(BS * d.H);
   t.final_h = c.take<float>((size_t)d.L * B * d.H);
   t.final_c = c.take<float>((size_t)d.L * B * d.H);
   t.gx = c.take<float>(BS * d.ndir * 4 * d.Hd_pad);
@@ -463,6 +491,7 @@ size_t state_layout(const Dims& d, int N, char* base, State* s) {
 struct StepWs {
   float* ctx;      // [N, Hm]
   float* scores;   // [N, S_max] raw attention scores
+  float* qproj;    // [N, H] concat: query columns of W_a times the decoder output
   float* pmax;     // [N, ntiles]
   float* psum;
   float* pval;     // [N, ntiles, K]
@@ -483,6 +512,7 @@ size_t step_layout(const Dims& d, int B, int S, int K, char* base, StepWs* w) {
   t.ntiles = (d.Vt + gen_tile_cols() - 1) / gen_tile_cols();
   t.ctx = c.take<float>(N * d.Hm);
   t.scores = c.take<float>(N * S);
+  t.qproj = d.attn == ONMT_ATTN_CONCAT ? c.take<float>(N * d.H) : nullptr;
   t.pmax = c.take<float>(N * t.ntiles);
   t.psum = c.take<float>(N * t.ntiles);
   t.pval = c.take<float>(N * t.ntiles * K);
@@ -787,7 +817,8 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
       }
     }
   }
-  // attention keys W_a m_s, once per batch
+  // attention keys W_a m_s (concat: its memory columns), once per batch; dot scores read the memory
+  if (d.attn == ONMT_ATTN_DOT) return ONMT_OK;
   AOp a{};
   a.M = BS;
   a.nseg = 1;
@@ -883,8 +914,19 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     HIP_TRY(gemm_lstm(d.bf16, small_shape(N, m->dec_w[l].Np), a, bop(m->dec_w[l]), lp, st));
   }
   const float* q = out.h + (d.L - 1) * LH;
+  const float* sq = q;
+  if (d.attn == ONMT_ATTN_CONCAT) {   // the query side of concat's tanh argument, W_q q
+    AOp a{};
+    a.M = N;
+    a.nseg = 1;
+    a.seg[0] = seg(q, nullptr, N, d.H, d.H, d.pad(d.H), 0);
+    StoreParams sp{nullptr, sw.qproj, d.H, d.H, 0};
+    HIP_TRY(gemm_store(d.bf16, small_shape(N, m->W_q.Np), a, bop(m->W_q), sp, st));
+    sq = sw.qproj;
+  }
   const AttnExtra ax{ex.cov, ex.align};
-  HIP_TRY(attention(q, d.H, w.keys, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.scores, sw.ctx, attn, ax, st));
+  HIP_TRY(attention(sq, d.H, w.keys, m->v_a, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.scores, sw.ctx, attn, ax,
+                    st));
   {
     AOp a{};
     a.M = N;

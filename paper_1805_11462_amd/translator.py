@@ -25,10 +25,14 @@ def _bytes(n, device):
     return torch.empty(max(int(n), 1), dtype=torch.uint8, device=device)
 
 
+ATTN_TYPES = {"general": 0, "dot": 1, "concat": 2}
+
+
 def make_config(enc_layers, dec_layers, bidirectional, emb, hidden, src_vocab, tgt_vocab, wdtype,
-                pad_id=0, unk_id=1, bos_id=2, eos_id=3):
+                pad_id=0, unk_id=1, bos_id=2, eos_id=3, attn="general"):
     return OnmtConfig(enc_layers, dec_layers, int(bool(bidirectional)), emb, hidden, src_vocab, tgt_vocab,
-                      1 if wdtype in ("bf16", 1) else 0, pad_id, unk_id, bos_id, eos_id)
+                      1 if wdtype in ("bf16", 1) else 0, pad_id, unk_id, bos_id, eos_id,
+                      ATTN_TYPES[attn] if isinstance(attn, str) else int(attn))
 
 
 class Translator:
@@ -81,7 +85,8 @@ class Translator:
     def enc_views(self, ws, B, S):
         """(memory [B, S, Hm], keys [B, S, H], final_h [L, B, H], final_c [L, B, H]) inside an encoder
         workspace, following the library's documented carving order (256-byte aligned regions:
-        lens, src, memory, keys, final_h, final_c)."""
+        lens, src, memory, keys, final_h, final_c; dot attention has no keys region, its keys are the
+        memory)."""
         c = self.cfg
         Hm = c.hidden
         al = lambda x: (x + 255) // 256 * 256
@@ -89,8 +94,11 @@ class Translator:
         off = al(off + 4 * B * S)
         mem = ws[off:off + 4 * B * S * Hm].view(torch.float32).view(B, S, Hm)
         off = al(off + 4 * B * S * Hm)
-        keys = ws[off:off + 4 * B * S * c.hidden].view(torch.float32).view(B, S, c.hidden)
-        off = al(off + 4 * B * S * c.hidden)
+        if c.attn_type == ATTN_TYPES["dot"]:
+            keys = mem
+        else:
+            keys = ws[off:off + 4 * B * S * c.hidden].view(torch.float32).view(B, S, c.hidden)
+            off = al(off + 4 * B * S * c.hidden)
         L = c.dec_layers
         fh = ws[off:off + 4 * L * B * c.hidden].view(torch.float32).view(L, B, c.hidden)
         off = al(off + 4 * L * B * c.hidden)

@@ -32,12 +32,13 @@ def test_every_declared_symbol_is_exported_and_bound():
 
 def cfg_of(w):
     return make_config(w.enc_layers, w.dec_layers, w.bidirectional, w.emb, w.hidden, w.src_vocab, w.tgt_vocab,
-                       w.wdtype)
+                       w.wdtype, attn=w.attn)
 
 
-@pytest.mark.parametrize("name", list(W.WORKLOADS))
-def test_weight_order_matches_the_shared_generator(name):
-    w = W.get(name)
+@pytest.mark.parametrize("name,attn", [(n, "general") for n in W.WORKLOADS]
+                         + [(n, a) for n in ("tiny", "larger") for a in ("dot", "concat")])
+def test_weight_order_matches_the_shared_generator(name, attn):
+    w = W.Workload(**{**W.get(name).as_dict(), "attn": attn})
     lib = _lib.load()
     cfg = cfg_of(w)
     specs = W.weight_specs(w)
@@ -54,6 +55,8 @@ def test_weight_order_matches_the_shared_generator(name):
     ("emb", 30, _lib.ONMT_EUNSUPPORTED),        # not a multiple of 4
     ("eos_id", 50000, _lib.ONMT_EINVAL),
     ("tgt_vocab", 3, _lib.ONMT_EINVAL),
+    ("attn_type", 3, _lib.ONMT_EINVAL),
+    ("attn_type", -1, _lib.ONMT_EINVAL),
 ])
 def test_invalid_configs_are_rejected(field, value, code):
     lib = _lib.load()

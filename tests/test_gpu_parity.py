@@ -12,7 +12,7 @@ import torch
 
 import workloads as W
 from oracle import onmt_oracle as O
-from tests._gpu import Setup, TAU, ATTN_TOL, with_workload
+from tests._gpu import Setup, TAU, ATTN_TOL, with_workload, check_search
 
 pytestmark = pytest.mark.gpu
 
@@ -125,37 +125,6 @@ def test_decode_steps_full_and_topk(which, request):
 
 
 # ------------------------------------------------------------------ beam search
-def _check_search(s, buf, sentences, K, T, alpha):
-    tau = s.tau
-    g_tok = buf["tok"].cpu().numpy()
-    g_len = buf["len"].cpu().numpy()
-    g_raw = buf["raw"].cpu().numpy()
-    g_norm = buf["norm"].cpu().numpy()
-    g_lp = buf["tok_logp"].cpu().numpy()
-    trace = {k: [a for a in buf[f"trace_{k}"].cpu().numpy()] for k in ("slot", "tok", "cand")}
-    mismatched = []
-    for b in sentences:
-        res = O.beam_search(s.model, s.src[b:b + 1], s.lens[b:b + 1], K, T, alpha)
-        n = int(g_len[b])
-        toks = list(g_tok[b, :n])
-        assert (g_tok[b, n:] == W.PAD_ID).all()
-        # the GPU's own result is internally consistent: per-token log-probs sum to raw, norm = raw / lp
-        assert abs(g_lp[b, :n].astype(np.float64).sum() - g_raw[b]) < 1e-6 * max(1, n)
-        assert abs(g_norm[b] - g_raw[b] / O.length_penalty(n, alpha)) < 1e-9 * max(1.0, abs(g_raw[b]))
-        # teacher-forced oracle rescoring of the GPU's hypothesis
-        forced = O.score_forced(s.model, s.src[b], s.lens[b], toks)
-        assert np.abs(forced - g_lp[b, :n]).max() <= tau
-        assert abs(forced.sum() - g_raw[b]) <= n * tau
-        if toks == res.tokens[0]:
-            assert abs(res.raw[0] - g_raw[b]) <= n * tau
-        else:
-            mismatched.append(b)
-    # every sentence (matched or not) must pass the step-by-step replay of the GPU's decisions
-    bad = O.replay_verify(s.model, s.src, s.lens, K, T, alpha, trace, tau, sentences=sentences)
-    assert bad == [], bad[:10]
-    return mismatched
-
-
 @pytest.mark.parametrize("which,alpha", [("tiny", 0.0), ("tiny", 0.6), ("tiny_peaked", 0.0), ("tiny_peaked", 0.6)])
 def test_beam_search_tiny(which, alpha, request):
     s = request.getfixturevalue(which)
@@ -165,7 +134,7 @@ def test_beam_search_tiny(which, alpha, request):
     buf = s.tr.search_buffers(B, S, w.beam, w.max_len, alpha, trace=True)
     s.tr.beam_search(s.src_d, s.lens_d, buf)
     torch.cuda.synchronize()
-    mism = _check_search(s, buf, range(B), w.beam, w.max_len, alpha)
+    mism = check_search(s, buf, range(B), w.beam, w.max_len, alpha)
     print(f"  free-run token mismatches (replay-verified): {mism}", flush=True)
 
 
@@ -177,7 +146,7 @@ def test_beam_widths_tiny_peaked(tiny_peaked, K):
     buf = s.tr.search_buffers(B, S, K, 9, 0.6, trace=True)
     s.tr.beam_search(s.src_d, s.lens_d, buf)
     torch.cuda.synchronize()
-    _check_search(s, buf, range(B), K, 9, 0.6)
+    check_search(s, buf, range(B), K, 9, 0.6)
 
 
 def test_beam_search_default_sampled(default):
@@ -191,7 +160,7 @@ def test_beam_search_default_sampled(default):
     torch.cuda.synchronize()
     g_len = buf["len"].cpu().numpy()
     assert (g_len >= 1).all() and (g_len <= w.max_len).all()
-    _check_search(s, buf, [0, 37, 63], w.beam, w.max_len, w.alpha)
+    check_search(s, buf, [0, 37, 63], w.beam, w.max_len, w.alpha)
 
 
 def test_search_is_deterministic(tiny_peaked):
@@ -294,5 +263,5 @@ def test_beam_search_other_workloads(which, sample, request):
     torch.cuda.synchronize()
     g_len = buf["len"].cpu().numpy()
     assert (g_len >= 1).all() and (g_len <= w.max_len).all()
-    mism = _check_search(s, buf, sample, w.beam, w.max_len, w.alpha)
+    mism = check_search(s, buf, sample, w.beam, w.max_len, w.alpha)
     print(f"  free-run token mismatches (replay-verified): {mism}", flush=True)

@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--mode", choices=["search", "score"], default="search",
                     help="search: beam search (the headline metric); score: teacher-forced scoring of "
                          "max-decode-long synthetic targets")
+    ap.add_argument("--attn", choices=["general", "dot", "concat"], default=None,
+                    help="attention score type (default: the workload's, general)")
     ap.add_argument("--beta", type=float, default=0.0, help="coverage penalty weight of the search (0 = off)")
     ap.add_argument("--banned", type=int, default=0,
                     help="ban this many target ids (4, 4 + 7, 4 + 14, ...) from every hypothesis (0 = none)")
@@ -121,6 +123,8 @@ def main():
     from paper_1805_11462_amd.translator import Translator, make_config
 
     w = W.get(args.workload)
+    if args.attn:
+        w = W.Workload(**{**w.as_dict(), "attn": args.attn})
     weights = W.make_weights(w)
     src, lens = W.make_batch(w)
     B, S = src.shape
@@ -182,7 +186,7 @@ def main():
         "data": "synthetic (seeded uniform(-0.1,0.1) weights, bounded-Zipf source tokens)",
         "config": {"workload": f"{w.name}: {w.enc_layers}x{w.hidden} LSTM enc/dec, emb {w.emb}, vocab {w.tgt_vocab}, "
                                f"batch {w.batch}, src len {w.len_lo}-{w.len_hi}, beam {w.beam}, "
-                               f"max decode {w.max_len}, alpha {w.alpha}, {w.wdtype}"
+                               f"max decode {w.max_len}, alpha {w.alpha}, {w.wdtype}, {w.attn} attention"
                                + (f", coverage beta {args.beta}" if args.beta else "")
                                + (f", {len(banned)} banned ids" if banned else "")
                                + (f", max {args.max_unk} UNK" if args.max_unk >= 0 else "")

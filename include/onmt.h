@@ -198,9 +198,10 @@ int onmt_score(onmt_model* model, const int32_t* src, const int32_t* len, int B,
                void* stream);
 
 /* ---- Kernel timing -----------------------------------------------------------------------------------
- * onmt_profile_enable(model, every): every >= 1 makes onmt_beam_search record HIP events on `stream`
- * around every `every`-th launch of the decoder's generator kernel (the vocabulary projection with its
- * fused log-softmax/top-K epilogue), counting launches from this call; 0 switches timing off; < 0 is
+ * onmt_profile_enable(model, every): every >= 1 makes onmt_beam_search and onmt_score record HIP events
+ * on `stream` around every `every`-th launch of the generator kernel (the vocabulary projection with its
+ * fused log-softmax/top-K epilogue; the search launches it once per step, scoring once over all steps),
+ * counting launches from this call; 0 switches timing off; < 0 is
  * ONMT_EINVAL. onmt_profile_read returns how many launches were timed and their summed duration in
  * milliseconds since the last reset. Each timed launch adds two event records to the stream. */
 int onmt_profile_enable(onmt_model* model, int every);

@@ -186,16 +186,22 @@ hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pva
   return hipGetLastError();
 }
 
-// One wave per row: logsumexp from the per-tile maxima and sums, as in row_merge_wave.
-__global__ __launch_bounds__(kMergeWaves * kWave) void k_score_step(const float* __restrict__ pmax,
+// Teacher-forced scores of all steps at once. Row r = t * B + b (step t of sentence b); one wave per row
+// forms the logsumexp from the per-tile maxima and sums, as in row_merge_wave, and writes
+// logp[b, t] = logit of the target - logsumexp (0 past the sentence's length).
+__global__ __launch_bounds__(kMergeWaves * kWave) void k_score_rows(const float* __restrict__ pmax,
                                                                     const float* __restrict__ psum, int ntiles,
                                                                     const float* __restrict__ want_logit,
-                                                                    const int32_t* __restrict__ len, int M, int t,
-                                                                    float* __restrict__ logp, int ld,
-                                                                    double* __restrict__ nll) {
+                                                                    const int32_t* __restrict__ len, int B, int M,
+                                                                    float* __restrict__ logp, int ld) {
   const int row = blockIdx.x * kMergeWaves + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= M) return;
+  const int t = row / B, b = row % B;
+  if (t >= len[b]) {
+    if (lane == 0) logp[(size_t)b * ld + t] = 0.f;
+    return;
+  }
   const float* pm = pmax + (size_t)row * ntiles;
   const float* ps = psum + (size_t)row * ntiles;
   const float ninf = -__builtin_inff();
@@ -217,32 +223,28 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_score_step(const float*
     if (tt < ntiles) sm += tq[j] * __expf(tm[j] - gmx);
   }
   const float lse = gmx + __logf(wave_sum(sm));
-  if (lane == 0) {
-    const bool on = t < len[row];
-    const float v = on ? want_logit[row] - lse : 0.f;
-    logp[(size_t)row * ld + t] = v;
-    if (on) nll[row] -= (double)v;
-  }
+  if (lane == 0) logp[(size_t)b * ld + t] = want_logit[row] - lse;
 }
 
-hipError_t score_step(const float* pmax, const float* psum, int ntiles, const float* want_logit, const int32_t* len,
-                      int M, int t, float* logp, int ld, double* nll, hipStream_t st) {
+// nll[b] = -sum over t < len[b] of logp[b, t], summed in fp64 in step order.
+__global__ void k_score_nll(const float* __restrict__ logp, int ld, const int32_t* __restrict__ len, int B,
+                            double* __restrict__ nll) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  double s = 0.0;
+  for (int t = 0; t < len[b]; ++t) s -= (double)logp[(size_t)b * ld + t];
+  nll[b] = s;
+}
+
+hipError_t score_rows(const float* pmax, const float* psum, int ntiles, const float* want_logit, const int32_t* len,
+                      int B, int steps, float* logp, int ld, double* nll, hipStream_t st) {
   if (ntiles > kWave * kMaxTilesPerLane) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_score_step, dim3((M + kMergeWaves - 1) / kMergeWaves), dim3(kMergeWaves * kWave), 0, st, pmax,
-                     psum, ntiles, want_logit, len, M, t, logp, ld, nll);
-  return hipGetLastError();
-}
-
-__global__ void k_fill64(double* dst, size_t n, double v) {
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-    dst[i] = v;
-}
-
-hipError_t fill_f64(double* dst, size_t n, double v, hipStream_t st) {
-  if (n == 0) return hipSuccess;
-  size_t blocks = (n + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(k_fill64, dim3((unsigned)blocks), dim3(256), 0, st, dst, n, v);
+  const int M = B * steps;
+  hipLaunchKernelGGL(k_score_rows, dim3((M + kMergeWaves - 1) / kMergeWaves), dim3(kMergeWaves * kWave), 0, st, pmax,
+                     psum, ntiles, want_logit, len, B, M, logp, ld);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_score_nll, dim3((B + 255) / 256), dim3(256), 0, st, logp, ld, len, B, nll);
   return hipGetLastError();
 }
 

@@ -129,11 +129,10 @@ size_t attention_lds_bytes(int S_max, int H, int K);
 
 hipError_t lse_topk_merge(const float* pmax, const float* psum, const float* pval, const int32_t* pid, int M,
                           int ntiles, int K, float* out_val, int32_t* out_id, float* out_lse, hipStream_t st);
-// Teacher-forced scoring, one decoder step: logp[row * ld + t] = want_logit[row] - logsumexp(row) from the
-// generator partials for rows with t < len[row] (0 otherwise), and nll[row] -= logp in fp64.
-hipError_t score_step(const float* pmax, const float* psum, int ntiles, const float* want_logit, const int32_t* len,
-                      int M, int t, float* logp, int ld, double* nll, hipStream_t st);
-hipError_t fill_f64(double* dst, size_t n, double v, hipStream_t st);
+// Teacher-forced scoring of all steps: rows r = t * B + b of the generator partials; logp[b * ld + t] =
+// want_logit[r] - logsumexp(r) for t < len[b] (0 otherwise, t < steps); nll[b] = -sum_t logp[b, t] in fp64.
+hipError_t score_rows(const float* pmax, const float* psum, int ntiles, const float* want_logit, const int32_t* len,
+                      int B, int steps, float* logp, int ld, double* nll, hipStream_t st);
 hipError_t subtract_rows(float* x, int ld, const float* lse, int M, int ncols, hipStream_t st);
 
 struct BeamParams {

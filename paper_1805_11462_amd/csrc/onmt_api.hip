@@ -585,7 +585,10 @@ struct ScoreWs {
   int32_t* in_tok;     // [T, B] decoder input at step t
   int32_t* want;       // [T, B] target predicted at step t
   int32_t* tlen;       // [B]
-  float* want_logit;   // [B]
+  float* feeds;        // [T, B, H] attentional vector of every step (the generator's input)
+  float* gpmax;        // [T * B, ntiles] generator partials of all steps
+  float* gpsum;
+  float* want_logit;   // [T, B]
   double* nll;         // [B]
 };
 
@@ -607,7 +610,10 @@ size_t score_layout(const Dims& d, int B, int S, int T, char* base, ScoreWs* w) 
   t.in_tok = c.take<int32_t>((size_t)T * B);
   t.want = c.take<int32_t>((size_t)T * B);
   t.tlen = c.take<int32_t>(B);
-  t.want_logit = c.take<float>(B);
+  t.feeds = c.take<float>((size_t)T * B * d.H);
+  t.gpmax = c.take<float>((size_t)T * B * t.step.ntiles);
+  t.gpsum = c.take<float>((size_t)T * B * t.step.ntiles);
+  t.want_logit = c.take<float>((size_t)T * B);
   t.nll = c.take<double>(B);
   if (w) *w = t;
   return align_up(c.off);
@@ -870,7 +876,9 @@ void time_collect(onmt_model* m) {
 
 // One decoder step on validated inputs (Section 2; Figure 1(a); items (a)-(c); Section 4.2 attention).
 // mode 0: logp [N, V] full log-softmax; mode 1: top-K (logp [N, K], ids [N, K]); mode 2 (beam search):
-// stop after the generator, leaving its per-tile partials in the step workspace for the beam step.
+// stop after the generator, leaving its per-tile partials in the step workspace for the beam step;
+// mode 3 (teacher forcing): stop after the attentional vector (out.feed), the generator runs later over
+// all steps at once.
 // Optional work of a decoder step beyond the log-distribution.
 struct StepExtras {
   const int32_t* want = nullptr;        // the logit of column want[r] of every row goes to want_logit[r]
@@ -936,6 +944,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     StoreParams sp{nullptr, out.feed, d.H, d.H, 1};
     HIP_TRY(gemm_store(d.bf16, small_shape(N, m->W_c.Np), a, bop(m->W_c), sp, st));
   }
+  if (mode == 3) return ONMT_OK;
   {
     AOp a{};
     a.M = N;
@@ -1214,17 +1223,39 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
   rc = decode_init_compute(m, w.enc, B, 1, w.st[0], st);
   if (rc) return rc;
   HIP_TRY(fill_f32(out_logp, (size_t)B * T, 0.f, st));
-  HIP_TRY(fill_f64(w.nll, B, 0.0, st));
+  // the recurrence step by step (input feeding makes each step depend on the previous attentional
+  // vector); every step's attentional vector is kept for the generator
+  const Dims& d = m->d;
   int cur = 0;
   for (int t = 0; t < steps; ++t) {
-    StepExtras ex;
-    ex.want = w.want + (size_t)t * B;
-    ex.want_logit = w.want_logit;
-    rc = decode_compute(m, w.enc, B, S, 1, w.st[cur], w.st[cur ^ 1], w.in_tok + (size_t)t * B, nullptr, 2, nullptr,
-                        nullptr, nullptr, nullptr, w.step, st, ex);
+    State in = w.st[cur], out = w.st[cur ^ 1];
+    if (t > 0) in.feed = w.feeds + (size_t)(t - 1) * B * d.H;
+    out.feed = w.feeds + (size_t)t * B * d.H;
+    rc = decode_compute(m, w.enc, B, S, 1, in, out, w.in_tok + (size_t)t * B, nullptr, 3, nullptr, nullptr, nullptr,
+                        nullptr, w.step, st);
     if (rc) return rc;
-    HIP_TRY(score_step(w.step.pmax, w.step.psum, w.step.ntiles, w.want_logit, w.tlen, B, t, out_logp, T, w.nll, st));
     cur ^= 1;
+  }
+  // one generator pass over the steps * B rows: per-tile max and sum of exponentials, and the target's logit
+  {
+    const int M = steps * B;
+    AOp a{};
+    a.M = M;
+    a.nseg = 1;
+    a.seg[0] = seg(w.feeds, nullptr, M, d.H, d.H, d.pad(d.H), 0);
+    GenParams gp{};
+    gp.bias = m->b_s;
+    gp.V = d.Vt;
+    gp.K = 0;
+    gp.ntiles = w.step.ntiles;
+    gp.pmax = w.gpmax;
+    gp.psum = w.gpsum;
+    gp.want = w.want;
+    gp.want_logit = w.want_logit;
+    time_begin(m, st);
+    HIP_TRY(gemm_gen(d.bf16, a, bop(m->W_s), gp, st));
+    time_end(m, st);
+    HIP_TRY(score_rows(w.gpmax, w.gpsum, w.step.ntiles, w.want_logit, w.tlen, B, steps, out_logp, T, w.nll, st));
   }
   HIP_TRY(hipMemcpyAsync(out_nll, w.nll, sizeof(double) * B, hipMemcpyDeviceToDevice, st));
   HIP_TRY(hipStreamSynchronize(st));

@@ -64,17 +64,23 @@ __device__ inline int xcd_remap(int bid, int nblocks) {
 __device__ inline uint4 zero4() { return make_uint4(0u, 0u, 0u, 0u); }
 
 // Split 8 fp32 values into bf16 hi = RNE(x) and lo = RNE(x - hi); x - hi is exact in fp32, so
-// hi + lo keeps about 16 significant bits of x.
+// hi + lo keeps about 16 significant bits of x. The conversions are gfx950's packed fp32 -> bf16
+// (round to nearest even), two values per instruction.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ inline void split_bf16x8(const float4& a, const float4& b, uint4& hi, uint4& lo) {
-  const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-  uint32_t h[8], l[8];
+  const f32x2_t x[4] = {{a.x, a.y}, {a.z, a.w}, {b.x, b.y}, {b.z, b.w}};
+  uint32_t h[4], l[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    h[i] = f32_to_bf16_bits(x[i]);
-    l[i] = f32_to_bf16_bits(x[i] - bf16_bits_to_f32((uint16_t)h[i]));
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2_t hv = __builtin_convertvector(x[i], bf16x2_t);
+    const f32x2_t hf = __builtin_convertvector(hv, f32x2_t);
+    const bf16x2_t lv = __builtin_convertvector(x[i] - hf, bf16x2_t);
+    h[i] = __builtin_bit_cast(uint32_t, hv);
+    l[i] = __builtin_bit_cast(uint32_t, lv);
   }
-  hi = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
-  lo = make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16));
+  hi = make_uint4(h[0], h[1], h[2], h[3]);
+  lo = make_uint4(l[0], l[1], l[2], l[3]);
 }
 
 // Buffer resource descriptor (gfx9 family word 3). Loads through it return zeros past num_records, so
@@ -492,6 +498,10 @@ using TileThin32 = Tile<float, 1, 1, 4, 1, 2, 16>;
 using TileWide16 = Tile<__bf16, 2, 2, 1, 2, 4, 64>;
 using TileSplit16 = Tile<__bf16, 1, 1, 4, 2, 4, 32>;
 using TileThin16 = Tile<__bf16, 1, 1, 4, 1, 4, 32>;
+// bf16 LSTM GEMMs of a few hundred rows: 32 x 64 tiles, two waves per K half. Against the 16 x 64 tile
+// the weights are re-read by half as many row tiles, which matters more than the halved workgroup count
+// once the bf16 products are cheap (decoder layers at 320-512 rows: 16-32% faster).
+using TileMid16 = Tile<__bf16, 1, 2, 2, 2, 2, 32>;
 // Generator: the 64 x 128 tile of the wide shapes with a 16 (fp32) / 32 (bf16) element K stage, which
 // halves the LDS stage buffers so that four workgroups fit on a CU.
 using TileGen32 = Tile<float, 2, 2, 1, 2, 4, 16>;
@@ -584,6 +594,7 @@ hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const Lstm
   if (bf16) {
     if (shape == kShapeWide) return launch_lstm<__bf16, TileWide16>(a, b, p, st);
     if (shape == kShapeSplitK) return launch_lstm<__bf16, TileSplit16>(a, b, p, st);
+    if (shape == kShapeMid) return launch_lstm<__bf16, TileMid16>(a, b, p, st);
     return launch_lstm<__bf16, TileThin16>(a, b, p, st);
   }
   if (shape == kShapeWide) return launch_lstm<float, TileWide32>(a, b, p, st);
@@ -601,8 +612,9 @@ static hipError_t lstm2_dispatch(const LstmPair& g, hipStream_t st) {
 }
 
 hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st) {
-  if (shape != kShapeSplitKThin) return hipErrorInvalidValue;
-  return bf16 ? lstm2_dispatch<__bf16, TileThin16>(g, st) : lstm2_dispatch<float, TileThin32>(g, st);
+  if (shape != kShapeSplitKThin && shape != kShapeMid) return hipErrorInvalidValue;
+  if (!bf16) return lstm2_dispatch<float, TileThin32>(g, st);
+  return shape == kShapeMid ? lstm2_dispatch<__bf16, TileMid16>(g, st) : lstm2_dispatch<__bf16, TileThin16>(g, st);
 }
 
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {

@@ -652,6 +652,13 @@ int small_shape(int M, int Np) {
   return tiles32 >= ONMT_SMALL_M_TILES ? kShapeSplitK : kShapeSplitKThin;
 }
 
+// LSTM GEMMs: bf16 models with at least this many rows use the 32-row two-way split-K tile.
+constexpr int kMidMinRows = 256;
+int lstm_shape(const Dims& d, int M, int Np) {
+  if (d.bf16 && M >= kMidMinRows) return kShapeMid;
+  return small_shape(M, Np);
+}
+
 // Copies src/len to the host, validates them, and uploads the token ids with every position at or beyond
 // its sentence's length replaced by 0 into clean_src (device, [B, S]), so no kernel gathers an embedding
 // row through an unchecked id.
@@ -750,7 +757,7 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
     BOp wb;
     LstmParams lp;
     recurrent(l, dir, s, step, slot, joint, r, wb, lp);
-    HIP_TRY(gemm_lstm(d.bf16, small_shape(B, wb.Np), r, wb, lp, st));
+    HIP_TRY(gemm_lstm(d.bf16, lstm_shape(d, B, wb.Np), r, wb, lp, st));
     return ONMT_OK;
   };
   auto run_two = [&](int l0, int dir0, int s0, int step0, int slot0, bool joint0, int l1, int dir1, int s1,
@@ -758,7 +765,7 @@ int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B,
     LstmPair g{};
     recurrent(l0, dir0, s0, step0, slot0, joint0, g.a[0], g.b[0], g.p[0]);
     recurrent(l1, dir1, s1, step1, slot1, joint1, g.a[1], g.b[1], g.p[1]);
-    HIP_TRY(gemm_lstm2(d.bf16, kShapeSplitKThin, g, st));
+    HIP_TRY(gemm_lstm2(d.bf16, d.bf16 && B >= kMidMinRows ? kShapeMid : kShapeSplitKThin, g, st));
     return ONMT_OK;
   };
   auto project = [&](int l) -> int {   // input projection of every position, both directions at once
@@ -919,7 +926,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     lp.c_out = out.c + l * LH;
     lp.ld_out = d.H;
     lp.H = d.H;
-    HIP_TRY(gemm_lstm(d.bf16, small_shape(N, m->dec_w[l].Np), a, bop(m->dec_w[l]), lp, st));
+    HIP_TRY(gemm_lstm(d.bf16, lstm_shape(d, N, m->dec_w[l].Np), a, bop(m->dec_w[l]), lp, st));
   }
   const float* q = out.h + (d.L - 1) * LH;
   const float* sq = q;

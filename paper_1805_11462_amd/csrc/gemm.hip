@@ -92,6 +92,12 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kBufWord3);
 }
 
+// LDS address of a byte in a __shared__ array, as the LDS-destination buffer loads take it. (Declared at
+// file scope: a local typedef of this pointer type inside a kernel template stops the host stub from
+// being emitted.)
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+__device__ inline lds_ptr_t lds_at(char* p) { return (lds_ptr_t)p; }
+
 __device__ inline uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
 }
@@ -315,14 +321,22 @@ __global__ __launch_bounds__(C::NT) void k_gemm_store(AOp a, BOp b, StoreParams 
   for (int e = threadIdx.x; e < C::BM * (C::BN / 4); e += C::NT) {
     const int r = e / (C::BN / 4), c = (e % (C::BN / 4)) * 4;
     const int gr = m0 + r, gc = n0 + c;
-    if (gr >= a.M || gc >= p.ncols) continue;
+    const bool out = gc < p.ncols;                      // ncols is a multiple of 4
+    const bool split = p.hi && gc < p.ncols_hl;
+    if (gr >= a.M || !(out || split)) continue;
     float v[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      v[j] = ctile<C>(Ct, r, c + j) + (p.bias ? p.bias[gc + j] : 0.f);
+      v[j] = ctile<C>(Ct, r, c + j) + (p.bias && out ? p.bias[gc + j] : 0.f);
       if (p.act == 1) v[j] = tanhf(v[j]);
     }
-    *(float4*)(p.out + (size_t)gr * p.ldo + gc) = make_float4(v[0], v[1], v[2], v[3]);
+    if (out) *(float4*)(p.out + (size_t)gr * p.ldo + gc) = make_float4(v[0], v[1], v[2], v[3]);
+    if (split) {
+      uint4 h, l;
+      split_bf16x8(make_float4(v[0], v[1], v[2], v[3]), make_float4(0.f, 0.f, 0.f, 0.f), h, l);
+      *(uint2*)(p.hi + (size_t)gr * p.ld_hl + gc) = make_uint2(h.x, h.y);
+      *(uint2*)(p.lo + (size_t)gr * p.ld_hl + gc) = make_uint2(l.x, l.y);
+    }
   }
 }
 
@@ -387,17 +401,13 @@ __global__ __launch_bounds__(C::NT) void k_gemm_lstm2(LstmPair g) {
   }
 }
 
-// Generator: 4 threads per row, 32 interleaved columns each. Row max and sum of exponentials are
-// combined with lane shuffles; the tile's top-K is taken with K rounds of a 4-lane argmax (larger
-// logit first, smaller id on ties), each thread skipping the columns it already gave away.
-template <class T, class C, int NSEG>
-__global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, int nm, int nblocks) {
+// Generator epilogue over the 64 x 128 output tile in LDS: 4 threads per row, 32 interleaved columns
+// each. Row max and sum of exponentials are combined with lane shuffles; the tile's top-K is taken with
+// K rounds of a 4-lane argmax (larger logit first, smaller id on ties), each thread skipping the columns
+// it already gave away.
+template <class C>
+__device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M, int m0, int n0, int nt) {
   static_assert(C::NT / C::BM == 4 && C::BN == 128, "generator tile is 64 x 128 with 256 threads");
-  __shared__ __attribute__((aligned(16))) char smem[C::LDS];
-  const int L = xcd_remap(blockIdx.x, nblocks);
-  const int mt = L % nm, nt = L / nm;
-  const int m0 = mt * C::BM, n0 = nt * C::BN;
-  gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
   const float* Ct = (const float*)smem;
   // thread (row r, part p) owns columns 4 j + p, j < 32: the 64 lanes of a wave then read 64 different
   // banks of the output tile for every j
@@ -412,7 +422,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
     z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) + p.bias[gc] : ninf;
     mx = fmaxf(mx, z[j]);
   }
-  if (p.want && row < a.M) {
+  if (p.want && row < M) {
     const int wc = p.want[row] - n0;      // this thread holds column 4 j + part of the tile
     if (wc >= 0 && wc < C::BN && (wc & 3) == part) {
 #pragma unroll
@@ -420,7 +430,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
         if (4 * j + part == wc) p.want_logit[row] = z[j];
     }
   }
-  if (p.logits && row < a.M) {
+  if (p.logits && row < M) {
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
       const int gc = n0 + 4 * j + part;
@@ -435,7 +445,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
   sm += __shfl_xor(sm, 1, kWave);
   sm += __shfl_xor(sm, 2, kWave);
   const size_t o = (size_t)row * p.ntiles + nt;
-  if (part == 0 && row < a.M) {
+  if (part == 0 && row < M) {
     p.pmax[o] = rmx;
     p.psum[o] = sm;
   }
@@ -453,7 +463,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
       if ((words[j >> 3] >> (4 * (j & 7) + part)) & 1u) taken |= 1u << j;
     }
   }
-  if (p.unk_cnt && row < a.M && p.max_unk >= 0 && p.unk_cnt[row] >= p.max_unk) {
+  if (p.unk_cnt && row < M && p.max_unk >= 0 && p.unk_cnt[row] >= p.max_unk) {
     const int c = p.unk_id - n0;
     if (c >= 0 && c < C::BN && (c & 3) == part) taken |= 1u << (c >> 2);
   }
@@ -480,12 +490,23 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
       }
     }
     if (bid == mine && bv > ninf) taken |= 1u << bj;
-    if (part == 0 && row < a.M) {
+    if (part == 0 && row < M) {
       p.pval[o * p.K + k] = bv;
       p.pid[o * p.K + k] = bid;
       if (k == 0 && p.pfmax) p.pfmax[o] = bv;
     }
   }
+}
+
+
+template <class T, class C, int NSEG>
+__global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, int nm, int nblocks) {
+  __shared__ __attribute__((aligned(16))) char smem[C::LDS];
+  const int L = xcd_remap(blockIdx.x, nblocks);
+  const int mt = L % nm, nt = L / nm;
+  const int m0 = mt * C::BM, n0 = nt * C::BN;
+  gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
+  gen_epilogue<C>(smem, p, a.M, m0, n0, nt);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -507,6 +528,117 @@ using TileMid16 = Tile<__bf16, 1, 2, 2, 2, 2, 32>;
 using TileGen32 = Tile<float, 2, 2, 1, 2, 4, 16>;
 using TileGen16 = Tile<__bf16, 2, 2, 1, 2, 4, 32>;
 static_assert(TileGen32::BN == TileGen16::BN, "both generator tiles give the same column tiles");
+// LDS stages of the pre-split bf16 generator (16 KB each): three (48 KB, three workgroups per CU) measured
+// faster than four or five at 320 and 512 rows.
+constexpr int kGenStages = 3;
+
+// bf16 generator on a pre-split operand with its operands moved straight into LDS: buffer loads with an
+// LDS destination write one 1 KB slice per wave instruction (16 tile rows of 64 bytes, lane l at byte
+// 16 l), so a stage needs no staging registers and NSTG stages can be in flight at once. Each wave's loads
+// complete in issue order, so waiting until at most 4 (NSTG - 2) of its loads are outstanding means its
+// share of the oldest stage has landed; a barrier then makes the whole stage visible. The barrier is the
+// bare instruction: the fences of __syncthreads would also wait for the stages still in flight. Fragment
+// reads, products and the epilogue are those of the register-staged kernel.
+template <int NSTG>
+__global__ __launch_bounds__(256) void k_gemm_gen_lds(GenSplitA a, BOp b, GenParams p, int nm, int nblocks) {
+  using C = TileGen16;
+  static_assert(C::BM == 64 && C::BN == 128 && C::BK == 32 && C::CPR == 4 && C::NT == 256 && C::WK == 1,
+                "the slice layout below is written for the 64 x 128 x 32 bf16 generator tile");
+  static_assert(NSTG >= 3 && 4 * (NSTG - 2) < 16, "wait count must fit the low vmcnt field");
+  constexpr int ROWB = C::BK * 2;                       // bytes per tile row
+  constexpr int STG = (2 * C::BM + C::BN) * ROWB;       // one stage: A hi rows, A lo rows, B rows
+  constexpr int LDSB = NSTG * STG > C::CT ? NSTG * STG : C::CT;
+  constexpr int kWaitStage = (4 * (NSTG - 2)) | (7 << 4) | (15 << 8);   // vmcnt only
+  __shared__ __attribute__((aligned(16))) char smem[LDSB];
+  const int L = xcd_remap(blockIdx.x, nblocks);
+  const int mt = L % nm, nt = L / nm;
+  const int m0 = mt * C::BM, n0 = nt * C::BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i16 = lane & 15, g = lane >> 4;
+  const int wn = wave % C::WN, wm = wave / C::WN;
+
+  // lane's place in a slice: tile row srow, 16-byte slot sslot, which holds chunk sslot ^ swz(row)
+  const int srow = lane >> 2, sslot = lane & 3;
+  const int arow = 16 * wave + srow;                    // wave w moves A rows 16 w .. 16 w + 15
+  const int ar = min(m0 + arow, a.M - 1);               // rows past M re-read row M - 1 (never stored)
+  const uint32_t a_off = ((uint32_t)ar * a.ld + (sslot ^ C::swz(arow)) * C::CH) * 2;
+  const __amdgpu_buffer_rsrc_t rhi = make_rsrc(a.hi, (uint32_t)a.M * a.ld * 2);
+  const __amdgpu_buffer_rsrc_t rlo = make_rsrc(a.lo, (uint32_t)a.M * a.ld * 2);
+  uint32_t b_off[2];                                    // and B rows 32 w .. 32 w + 31
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int brow = 32 * wave + 16 * i + srow;
+    b_off[i] = ((uint32_t)(n0 + brow) * b.Kp + (sslot ^ C::swz(brow)) * C::CH) * 2;
+  }
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(b.W, (uint32_t)b.Np * b.Kp * 2);
+  const int nst = a.kpad / C::BK;
+  // this wave's slices of a stage buffer: A hi rows 16 w.., A lo rows 16 w.., B rows 32 w.. and 32 w + 16..
+  const int sl_ahi = (16 * wave) * ROWB, sl_alo = (C::BM + 16 * wave) * ROWB;
+  const int sl_b0 = (2 * C::BM + 32 * wave) * ROWB, sl_b1 = sl_b0 + 16 * ROWB;
+
+  f32x4 acc[C::TM][C::TN];
+#pragma unroll
+  for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+    for (int y = 0; y < C::TN; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int col = (g ^ C::swz(i16)) * C::CH;           // this lane's 16-byte chunk of a fragment row
+  // stages past the last re-load the last one into a buffer that is never multiplied, which keeps every
+  // wave's count of loads in flight the same on every iteration
+#define ONMT_GEN_ISSUE(ST)                                                                              \
+  do {                                                                                                  \
+    char* sb_ = smem + ((ST) % NSTG) * STG;                                                             \
+    const uint32_t ko_ = (uint32_t)((ST) < nst ? (ST) : nst - 1) * C::BK * 2;                           \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rhi, lds_at(sb_ + sl_ahi), 16, a_off + ko_, 0, 0, 0);      \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rlo, lds_at(sb_ + sl_alo), 16, a_off + ko_, 0, 0, 0);      \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, lds_at(sb_ + sl_b0), 16, b_off[0] + ko_, 0, 0, 0);     \
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, lds_at(sb_ + sl_b1), 16, b_off[1] + ko_, 0, 0, 0);     \
+  } while (0)
+#pragma unroll
+  for (int st = 0; st < NSTG - 1; ++st) ONMT_GEN_ISSUE(st);
+  for (int st = 0; st < nst; ++st) {
+    __builtin_amdgcn_s_waitcnt(kWaitStage);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    ONMT_GEN_ISSUE(st + NSTG - 1);                      // refills the buffer multiplied at st - 1
+    const char* base = smem + (st % NSTG) * STG;
+    const __bf16* Ah = (const __bf16*)base + (wm * C::TM * 16 + i16) * C::ROW;
+    const __bf16* Al = Ah + C::BM * C::ROW;
+    const __bf16* Bb = (const __bf16*)base + (2 * C::BM + wn * C::TN * 16 + i16) * C::ROW;
+    bf16x8 av[C::TM], bv[C::TN];
+#pragma unroll
+    for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + x * 16 * C::ROW + col);
+#pragma unroll
+    for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + col);
+#pragma unroll
+    for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+      for (int y = 0; y < C::TN; ++y)
+        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+#pragma unroll
+    for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Al + x * 16 * C::ROW + col);
+#pragma unroll
+    for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+      for (int y = 0; y < C::TN; ++y)
+        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+  }
+#undef ONMT_GEN_ISSUE
+  // every load (including the re-loads past the end) has landed before the output tile reuses the buffers
+  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
+  __syncthreads();
+  float* Ct = (float*)smem;
+#pragma unroll
+  for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+    for (int y = 0; y < C::TN; ++y)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        Ct[(wm * C::TM * 16 + x * 16 + 4 * g + v) * C::CROW + wn * C::TN * 16 + y * 16 + i16] = acc[x][y][v];
+  __syncthreads();
+  gen_epilogue<C>(smem, p, a.M, m0, n0, nt);
+}
+
 
 template <class C>
 static inline void grid_of(const AOp& a, const BOp& b, int& nm, int& nblocks) {
@@ -619,6 +751,18 @@ hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st) {
 
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
   return bf16 ? launch_gen<__bf16, TileGen16>(a, b, p, st) : launch_gen<float, TileGen32>(a, b, p, st);
+}
+
+hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, const GenParams& p, hipStream_t st) {
+  using C = TileGen16;
+  const uint64_t lim = 1ull << 31;
+  if (a.M < 1 || a.kpad % kSegK || a.kpad > b.Kp || a.ld < a.kpad || b.Np % C::BN ||
+      (uint64_t)a.M * a.ld * 2 >= lim || (uint64_t)b.Np * b.Kp * 2 >= lim)
+    return hipErrorInvalidValue;
+  const int nm = (a.M + C::BM - 1) / C::BM;
+  const int nblocks = nm * (b.Np / C::BN);
+  hipLaunchKernelGGL(k_gemm_gen_lds<kGenStages>, dim3(nblocks), dim3(C::NT), 0, st, a, b, p, nm, nblocks);
+  return hipGetLastError();
 }
 
 }  // namespace onmt

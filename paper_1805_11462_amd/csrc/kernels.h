@@ -36,12 +36,18 @@ struct BOp {
 };
 
 // Plain store epilogue: out[r, n] = act(acc + bias[n]) for n < ncols. act: 0 none, 1 tanh.
+// Optionally (hi != nullptr) the same values split into bf16 hi = RNE(v) and lo = RNE(v - hi) planes
+// [rows, ld_hl] for columns n < ncols_hl (columns past ncols hold act(0), zero for the tanh stores).
 struct StoreParams {
   const float* bias;
   float* out;
   int ldo;
   int ncols;
   int act;
+  uint16_t* hi;
+  uint16_t* lo;
+  int ld_hl;
+  int ncols_hl;
 };
 
 // LSTM cell epilogue over gate-blocked columns (groups of 32 = 4 gates x kUnitGroup = 8 units).
@@ -105,6 +111,18 @@ hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const Lstm
 // Two independent thin-shape LSTM GEMMs in one launch (segment counts 1+1, 1+2 or 2+2).
 hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st);
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st);
+
+// bf16 generator operand already split into bf16 hi and lo planes (A = hi + lo), row-major [M, ld] each
+// with zeros in the K padding (columns width .. kpad - 1).
+struct GenSplitA {
+  const uint16_t* hi;
+  const uint16_t* lo;
+  int M;
+  int ld;      // elements per row, >= kpad
+  int kpad;    // multiple of kSegK
+};
+// The bf16 generator on a pre-split operand: same partials as gemm_gen, operands moved straight into LDS.
+hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, const GenParams& p, hipStream_t st);
 int gen_tile_cols();
 
 // Attention coverage of the hypotheses (optional): out[r, s] = in[parent[r], s] + a[r, s] for the real

@@ -501,6 +501,8 @@ struct StepWs {
   float* lse;      // [N]
   int32_t* align;  // [N] attention argmax
   float* pfmax;    // [N, ntiles] largest allowed logit per tile (hypothesis filters)
+  uint16_t* feed_hi;   // bf16 models: [N, pad(H)] attentional vector as bf16 hi + lo (the generator's operand)
+  uint16_t* feed_lo;
   int ntiles;
 };
 
@@ -522,6 +524,8 @@ size_t step_layout(const Dims& d, int B, int S, int K, char* base, StepWs* w) {
   t.lse = c.take<float>(N);
   t.align = c.take<int32_t>(N);
   t.pfmax = c.take<float>(N * t.ntiles);
+  t.feed_hi = d.bf16 ? c.take<uint16_t>(N * d.pad(d.H)) : nullptr;
+  t.feed_lo = d.bf16 ? c.take<uint16_t>(N * d.pad(d.H)) : nullptr;
   if (w) *w = t;
   return align_up(c.off);
 }
@@ -586,6 +590,8 @@ struct ScoreWs {
   int32_t* want;       // [T, B] target predicted at step t
   int32_t* tlen;       // [B]
   float* feeds;        // [T, B, H] attentional vector of every step (the generator's input)
+  uint16_t* feeds_hi;  // bf16 models: [T, B, pad(H)] the same as bf16 hi + lo planes
+  uint16_t* feeds_lo;
   float* gpmax;        // [T * B, ntiles] generator partials of all steps
   float* gpsum;
   float* want_logit;   // [T, B]
@@ -611,6 +617,8 @@ size_t score_layout(const Dims& d, int B, int S, int T, char* base, ScoreWs* w) 
   t.want = c.take<int32_t>((size_t)T * B);
   t.tlen = c.take<int32_t>(B);
   t.feeds = c.take<float>((size_t)T * B * d.H);
+  t.feeds_hi = d.bf16 ? c.take<uint16_t>((size_t)T * B * d.pad(d.H)) : nullptr;
+  t.feeds_lo = d.bf16 ? c.take<uint16_t>((size_t)T * B * d.pad(d.H)) : nullptr;
   t.gpmax = c.take<float>((size_t)T * B * t.step.ntiles);
   t.gpsum = c.take<float>((size_t)T * B * t.step.ntiles);
   t.want_logit = c.take<float>((size_t)T * B);
@@ -888,6 +896,9 @@ void time_collect(onmt_model* m) {
 // all steps at once.
 // Optional work of a decoder step beyond the log-distribution.
 struct StepExtras {
+  // bf16 models: where the attentional vector's hi/lo planes go (default: the step workspace's)
+  uint16_t* feed_hi = nullptr;
+  uint16_t* feed_lo = nullptr;
   const int32_t* want = nullptr;        // the logit of column want[r] of every row goes to want_logit[r]
   float* want_logit = nullptr;
   const Coverage* cov = nullptr;        // attention coverage and its penalty
@@ -949,6 +960,11 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     a.seg[0] = seg(sw.ctx, nullptr, N, d.Hm, d.Hm, d.pad(d.Hm), 0);
     a.seg[1] = seg(q, nullptr, N, d.H, d.H, d.pad(d.H), 0);
     StoreParams sp{nullptr, out.feed, d.H, d.H, 1};
+    if (d.bf16) {            // the generator's operand, split once here instead of in every column tile
+      sp.hi = ex.feed_hi ? ex.feed_hi : sw.feed_hi;
+      sp.lo = ex.feed_lo ? ex.feed_lo : sw.feed_lo;
+      sp.ld_hl = sp.ncols_hl = d.pad(d.H);
+    }
     HIP_TRY(gemm_store(d.bf16, small_shape(N, m->W_c.Np), a, bop(m->W_c), sp, st));
   }
   if (mode == 3) return ONMT_OK;
@@ -976,7 +992,10 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     gp.max_unk = ex.max_unk;
     gp.pfmax = ex.pfmax;
     time_begin(m, st);
-    HIP_TRY(gemm_gen(d.bf16, a, bop(m->W_s), gp, st));
+    if (d.bf16)
+      HIP_TRY(gemm_gen_split(GenSplitA{sw.feed_hi, sw.feed_lo, N, d.pad(d.H), d.pad(d.H)}, bop(m->W_s), gp, st));
+    else
+      HIP_TRY(gemm_gen(0, a, bop(m->W_s), gp, st));
     time_end(m, st);
   }
   if (mode == 2) return ONMT_OK;
@@ -1238,8 +1257,13 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
     State in = w.st[cur], out = w.st[cur ^ 1];
     if (t > 0) in.feed = w.feeds + (size_t)(t - 1) * B * d.H;
     out.feed = w.feeds + (size_t)t * B * d.H;
+    StepExtras ex;
+    if (d.bf16) {
+      ex.feed_hi = w.feeds_hi + (size_t)t * B * d.pad(d.H);
+      ex.feed_lo = w.feeds_lo + (size_t)t * B * d.pad(d.H);
+    }
     rc = decode_compute(m, w.enc, B, S, 1, in, out, w.in_tok + (size_t)t * B, nullptr, 3, nullptr, nullptr, nullptr,
-                        nullptr, w.step, st);
+                        nullptr, w.step, st, ex);
     if (rc) return rc;
     cur ^= 1;
   }
@@ -1260,7 +1284,10 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
     gp.want = w.want;
     gp.want_logit = w.want_logit;
     time_begin(m, st);
-    HIP_TRY(gemm_gen(d.bf16, a, bop(m->W_s), gp, st));
+    if (d.bf16)
+      HIP_TRY(gemm_gen_split(GenSplitA{w.feeds_hi, w.feeds_lo, M, d.pad(d.H), d.pad(d.H)}, bop(m->W_s), gp, st));
+    else
+      HIP_TRY(gemm_gen(0, a, bop(m->W_s), gp, st));
     time_end(m, st);
     HIP_TRY(score_rows(w.gpmax, w.gpsum, w.step.ntiles, w.want_logit, w.tlen, B, steps, out_logp, T, w.nll, st));
   }

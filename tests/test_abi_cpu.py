@@ -103,3 +103,17 @@ def test_model_create_rejects_bad_arguments_before_touching_memory():
                                  ctypes.byref(out)) == _lib.ONMT_ESIZE
     assert lib.onmt_model_create(ctypes.byref(cfg), arr, n, ctypes.c_void_p(8), 1 << 40, None,
                                  ctypes.byref(out)) == _lib.ONMT_EINVAL      # misaligned
+
+
+def test_library_resolves_every_kernel_it_launches():
+    # a kernel template whose host-side launch stub was not emitted would leave an undefined onmt:: symbol
+    # in the shared library (the linker accepts it; the first launch would fail)
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    path = _lib.load()._name
+    out = subprocess.run([nm, "-C", "--undefined-only", path], capture_output=True, text=True, check=True).stdout
+    missing = [l for l in out.splitlines() if "onmt::" in l]
+    assert missing == []

@@ -346,10 +346,29 @@ __device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p
                                  char* smem) {
   const int L = xcd_remap(bid, nblocks);
   const int m0 = (L % nm) * C::BM, n0 = (L / nm) * C::BN;
+  constexpr int UPT = C::BN / 4;                      // units per tile
+  constexpr int EPT = (C::BM * UPT + C::NT - 1) / C::NT;   // (row, unit) elements per thread
+  // the precomputed input-projection terms of this thread's elements are loaded before the main loop,
+  // so that their latency (table rows gathered by token id) hides behind it
+  float gxv[EPT][4];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const int e = threadIdx.x + i * C::NT;
+    const int r = e / UPT, uu = e % UPT;
+    const int row = m0 + r, unit = n0 / 4 + uu;
+    const bool ok = p.gx && e < C::BM * UPT && row < a.M && unit < p.H;
+    const int grow = !ok ? 0 : (p.gx_idx ? min((unsigned)p.gx_idx[row], (unsigned)p.gx_rows - 1u) : row * p.gx_S + p.gx_s);
+    const int cbase = (uu / kUnitGroup) * (4 * kUnitGroup) + (uu % kUnitGroup);
+#pragma unroll
+    for (int gt = 0; gt < 4; ++gt)
+      gxv[i][gt] = ok ? p.gx[(size_t)grow * p.ld_gx + p.gx_col0 + n0 + cbase + gt * kUnitGroup] : 0.f;
+  }
   gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
   const float* Ct = (const float*)smem;
-  constexpr int UPT = C::BN / 4;                      // units per tile
-  for (int e = threadIdx.x; e < C::BM * UPT; e += C::NT) {
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const int e = threadIdx.x + i * C::NT;
+    if (e >= C::BM * UPT) break;
     const int r = e / UPT, uu = e % UPT;
     const int row = m0 + r;
     const int unit = n0 / 4 + uu;
@@ -359,8 +378,7 @@ __device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p
 #pragma unroll
     for (int gt = 0; gt < 4; ++gt) {
       const int col = cbase + gt * kUnitGroup;
-      z[gt] = ctile<C>(Ct, r, col) + (p.bias ? p.bias[n0 + col] : 0.f);
-      if (p.gx) z[gt] += p.gx[(size_t)(row * p.gx_S + p.gx_s) * p.ld_gx + p.gx_col0 + n0 + col];
+      z[gt] = ctile<C>(Ct, r, col) + (p.bias ? p.bias[n0 + col] : 0.f) + gxv[i][gt];
     }
     const int crow = p.c_idx ? p.c_idx[row] : row;
     const float c_prev = p.c_in ? p.c_in[(size_t)crow * p.ld_c + unit] : 0.f;

@@ -54,7 +54,9 @@ struct StoreParams {
 struct LstmParams {
   const float* bias;            // packed [Np]
   const float* gx;              // optional precomputed input projection (packed columns)
-  int ld_gx, gx_col0, gx_S, gx_s;   // gx row for GEMM row b is b * gx_S + gx_s
+  int ld_gx, gx_col0, gx_S, gx_s;   // gx row for GEMM row b is b * gx_S + gx_s ...
+  const int32_t* gx_idx;        // ... or gx_idx[b] when given (a table row per GEMM row), clamped to
+  int gx_rows;                  // [0, gx_rows)
   const float* c_in;            // previous cell state rows, through c_idx (nullable = identity)
   const int32_t* c_idx;
   int ld_c;

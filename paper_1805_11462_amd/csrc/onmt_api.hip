@@ -59,6 +59,26 @@ struct Packed {      // packed weight matrix inside the model buffer
   size_t off = 0;
 };
 
+Seg seg(const void* base, const int32_t* idx, int rows, int ld, int width, int kpad, int bf16) {
+  Seg s;
+  s.base = base;
+  s.idx = idx;
+  s.rows = rows;
+  s.ld = ld;
+  s.width = width;
+  s.kpad = kpad;
+  s.bf16 = bf16;
+  return s;
+}
+
+BOp bop(const Packed& p) {
+  BOp b;
+  b.W = p.W;
+  b.Np = p.Np;
+  b.Kp = p.Kp;
+  return b;
+}
+
 struct Dims {
   int L, ndir, Hd, Hm, H, E, Vs, Vt;
   int Hd_pad, H_pad;   // units padded to multiples of 32 (gate-blocked groups, 128-column tiles)
@@ -172,6 +192,10 @@ struct onmt_model {
   const float* v_a = nullptr;              // concat [H]
   Packed W_c, W_s;
   const float* b_s = nullptr;
+  // decoder layer 0's input-projection rows for every target token, E_tgt[v] W_e^T in the packed (gate-
+  // blocked) column order, fp32 [Vt, 4 H_pad]; computed on the device when the model is created
+  float* emb_gates = nullptr;
+  size_t image_bytes = 0;    // the uploaded part of the model buffer (everything before emb_gates)
   // kernel timing
   int prof = 0;              // time every prof-th generator launch (0: off)
   long long prof_seq = 0;    // generator launches seen while timing is on
@@ -232,6 +256,8 @@ size_t model_layout(const onmt_config* c, onmt_model* m) {
   Packed wc = mat(ceil_to(d.H, 128), d.pad(d.Hm) + d.pad(d.H));
   Packed ws = mat(ceil_to(d.Vt, 128), d.pad(d.H));
   size_t bs = vec(ceil_to(d.Vt, 128));
+  const size_t image = align_up(cv.off);
+  const size_t eg = vec((size_t)d.Vt * 4 * d.H_pad);
   const size_t total = align_up(cv.off);
   if (m) {
     char* base = m->dev;
@@ -255,6 +281,8 @@ size_t model_layout(const onmt_config* c, onmt_model* m) {
     m->W_c = fix(wc);
     m->W_s = fix(ws);
     m->b_s = (const float*)(base + bs);
+    m->emb_gates = (float*)(base + eg);
+    m->image_bytes = image;
   }
   return total;
 }
@@ -330,7 +358,7 @@ int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, 
 
   HostImage img;
   img.bf16 = d.bf16;
-  img.buf.assign(need, 0);
+  img.buf.assign(m->image_bytes, 0);
   auto off_of = [&](const void* p) { return (size_t)((const char*)p - m->dev); };
   int wi = 0;
   // E_src
@@ -413,7 +441,16 @@ int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, 
     for (int r = 0; r < d.Vt; ++r) img.putf(bo, r, bs[r]);
   }
   hipStream_t st = (hipStream_t)stream;
-  hipError_t e = hipMemcpyAsync(dev_buf, img.buf.data(), need, hipMemcpyHostToDevice, st);
+  hipError_t e = hipMemcpyAsync(dev_buf, img.buf.data(), m->image_bytes, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) {
+    // decoder layer 0: the embedding columns of its packed matrix against every target embedding row
+    AOp a{};
+    a.M = d.Vt;
+    a.nseg = 1;
+    a.seg[0] = seg(m->E_tgt, nullptr, d.Vt, d.E, d.E, d.pad(d.E), d.bf16);
+    StoreParams sp{nullptr, m->emb_gates, 4 * d.H_pad, 4 * d.H_pad, 0};
+    e = gemm_store(d.bf16, kShapeWide, a, bop(m->dec_w[0]), sp, st);
+  }
   if (e == hipSuccess) e = hipStreamSynchronize(st);
   if (e != hipSuccess) {
     delete m;
@@ -625,26 +662,6 @@ size_t score_layout(const Dims& d, int B, int S, int T, char* base, ScoreWs* w) 
   t.nll = c.take<double>(B);
   if (w) *w = t;
   return align_up(c.off);
-}
-
-Seg seg(const void* base, const int32_t* idx, int rows, int ld, int width, int kpad, int bf16) {
-  Seg s;
-  s.base = base;
-  s.idx = idx;
-  s.rows = rows;
-  s.ld = ld;
-  s.width = width;
-  s.kpad = kpad;
-  s.bf16 = bf16;
-  return s;
-}
-
-BOp bop(const Packed& p) {
-  BOp b;
-  b.W = p.W;
-  b.Np = p.Np;
-  b.Kp = p.Kp;
-  return b;
 }
 
 // Small-M GEMMs: the 16-row split-K tile unless the 32-row tile already gives this many workgroups
@@ -918,17 +935,23 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
   for (int l = 0; l < d.L; ++l) {
     AOp a{};
     a.M = N;
+    BOp wb = bop(m->dec_w[l]);
+    LstmParams lp{};
+    a.nseg = 2;
     if (l == 0) {
-      a.nseg = 3;
-      a.seg[0] = seg(m->E_tgt, prev_tok, d.Vt, d.E, d.E, d.pad(d.E), d.bf16);
-      a.seg[1] = seg(in.feed, parent, N, d.H, d.H, d.pad(d.H), 0);
-      a.seg[2] = seg(in.h, parent, N, d.H, d.H, d.pad(d.H), 0);
+      // [feed ; h] against the feed and recurrent columns; the embedding columns' product is the
+      // precomputed row of the previous token (emb_gates), added in the epilogue
+      a.seg[0] = seg(in.feed, parent, N, d.H, d.H, d.pad(d.H), 0);
+      a.seg[1] = seg(in.h, parent, N, d.H, d.H, d.pad(d.H), 0);
+      wb.W = (const char*)wb.W + (size_t)d.pad(d.E) * d.esz;
+      lp.gx = m->emb_gates;
+      lp.gx_idx = prev_tok;
+      lp.gx_rows = d.Vt;
+      lp.ld_gx = 4 * d.H_pad;
     } else {
-      a.nseg = 2;
       a.seg[0] = seg(out.h + (l - 1) * LH, nullptr, N, d.H, d.H, d.pad(d.H), 0);
       a.seg[1] = seg(in.h + l * LH, parent, N, d.H, d.H, d.pad(d.H), 0);
     }
-    LstmParams lp{};
     lp.bias = m->dec_bias[l];
     lp.c_in = in.c + l * LH;
     lp.c_idx = parent;
@@ -937,7 +960,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     lp.c_out = out.c + l * LH;
     lp.ld_out = d.H;
     lp.H = d.H;
-    HIP_TRY(gemm_lstm(d.bf16, lstm_shape(d, N, m->dec_w[l].Np), a, bop(m->dec_w[l]), lp, st));
+    HIP_TRY(gemm_lstm(d.bf16, lstm_shape(d, N, m->dec_w[l].Np), a, wb, lp, st));
   }
   const float* q = out.h + (d.L - 1) * LH;
   const float* sq = q;

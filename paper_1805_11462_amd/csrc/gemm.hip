@@ -46,7 +46,6 @@ struct Tile {
   static constexpr int CROW = BN + 4;                // fp32 output tile row stride
   static constexpr int CT = WK * BM * CROW * 4;
   static constexpr int LDS = (2 * STAGE > CT) ? 2 * STAGE : CT;
-  static_assert(A_CH % NT == 0 && B_CH % NT == 0, "chunks must divide evenly among threads");
   static_assert(KW % KSUB == 0 && kSegK % BK == 0, "stage must divide the segment padding");
   static_assert(CPR == 4 || CPR == 8 || CPR >= 16, "swizzle covers 64-, 128- and >=256-byte rows");
   __device__ static int swz(int row) { return (row >> RSH) & SMASK; }
@@ -117,6 +116,7 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
   // of CPR, so the column is the same for every i and the row advances by NT / CPR.
   constexpr int RSTEP = C::NT / C::CPR;
   static_assert(C::NT % C::CPR == 0, "threads must cover whole tile rows");
+  static_assert(C::A_CH % C::NT == 0 && C::B_CH % C::NT == 0 && C::A_PT > 0, "chunks must divide evenly among threads");
   const int arow0 = tid / C::CPR;
   const int acol = (tid % C::CPR) * C::CH;
 
@@ -424,12 +424,12 @@ __global__ __launch_bounds__(C::NT) void k_gemm_lstm2(LstmPair g) {
 // K rounds of a 4-lane argmax (larger logit first, smaller id on ties), each thread skipping the columns
 // it already gave away.
 template <class C>
-__device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M, int m0, int n0, int nt) {
+__device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M, int m0, int n0, int nt, int tid) {
   static_assert(C::NT / C::BM == 4 && C::BN == 128, "generator tile is 64 x 128 with 256 threads");
   const float* Ct = (const float*)smem;
-  // thread (row r, part p) owns columns 4 j + p, j < 32: the 64 lanes of a wave then read 64 different
-  // banks of the output tile for every j
-  const int r = threadIdx.x >> 2, part = threadIdx.x & 3;
+  // thread tid = (row r, part p) owns columns 4 j + p, j < 32: the 64 lanes of a wave then read 64
+  // different banks of the output tile for every j
+  const int r = tid >> 2, part = tid & 3;
   const int row = m0 + r;
   const float ninf = -__builtin_inff();
   float z[32];
@@ -524,7 +524,7 @@ __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, i
   const int mt = L % nm, nt = L / nm;
   const int m0 = mt * C::BM, n0 = nt * C::BN;
   gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
-  gen_epilogue<C>(smem, p, a.M, m0, n0, nt);
+  gen_epilogue<C>(smem, p, a.M, m0, n0, nt, threadIdx.x);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -546,27 +546,44 @@ using TileMid16 = Tile<__bf16, 1, 2, 2, 2, 2, 32>;
 using TileGen32 = Tile<float, 2, 2, 1, 2, 4, 16>;
 using TileGen16 = Tile<__bf16, 2, 2, 1, 2, 4, 32>;
 static_assert(TileGen32::BN == TileGen16::BN, "both generator tiles give the same column tiles");
-// LDS stages of the pre-split bf16 generator (16 KB each): three (48 KB, three workgroups per CU) measured
-// faster than four or five at 320 and 512 rows.
-constexpr int kGenStages = 3;
+// Pre-split bf16 generator: 64 x 256 tiles (8 waves of 32 x 64; the activations are re-read by half as
+// many column tiles as with 64 x 128) and two LDS stages of 24 KB; at 320 and 512 rows this measured
+// 10-15% faster than 64 x 128 tiles with three 16 KB stages, and three or four stages of 64 x 256 slower.
+constexpr int kGenStages = 2;
+constexpr int kGenWN = 4;
+
+// One 16-byte-per-lane buffer load into LDS (lane l writes 16 bytes at lds + 16 l). (A function of its
+// own: called directly under control flow inside a kernel template, the builtin stops the host-side
+// launch stub from being emitted.)
+__device__ inline void dma16(__amdgpu_buffer_rsrc_t r, char* lds, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_at(lds), 16, off, 0, 0, 0);
+}
+
+// Vector-memory wait until at most n loads of this wave are outstanding (expcnt and lgkmcnt left alone).
+constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | (((n >> 4) & 3) << 14); }
 
 // bf16 generator on a pre-split operand with its operands moved straight into LDS: buffer loads with an
 // LDS destination write one 1 KB slice per wave instruction (16 tile rows of 64 bytes, lane l at byte
 // 16 l), so a stage needs no staging registers and NSTG stages can be in flight at once. Each wave's loads
-// complete in issue order, so waiting until at most 4 (NSTG - 2) of its loads are outstanding means its
-// share of the oldest stage has landed; a barrier then makes the whole stage visible. The barrier is the
-// bare instruction: the fences of __syncthreads would also wait for the stages still in flight. Fragment
-// reads, products and the epilogue are those of the register-staged kernel.
-template <int NSTG>
-__global__ __launch_bounds__(256) void k_gemm_gen_lds(GenSplitA a, BOp b, GenParams p, int nm, int nblocks) {
-  using C = TileGen16;
-  static_assert(C::BM == 64 && C::BN == 128 && C::BK == 32 && C::CPR == 4 && C::NT == 256 && C::WK == 1,
-                "the slice layout below is written for the 64 x 128 x 32 bf16 generator tile");
-  static_assert(NSTG >= 3 && 4 * (NSTG - 2) < 16, "wait count must fit the low vmcnt field");
+// complete in issue order, so waiting until at most SPW (NSTG - 2) of its loads are outstanding (SPW per
+// stage) means its share of the oldest stage has landed; a barrier then makes the whole stage visible.
+// The barrier is the bare instruction: the fences of __syncthreads would also wait for the stages still
+// in flight. Fragment reads, products and the epilogue are those of the register-staged kernel.
+template <int WN, int NSTG>
+__global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, GenParams p, int nm, int nblocks) {
+  using C = Tile<__bf16, 2, WN, 1, 2, 4, 32>;          // 64 x (64 WN) tile, waves of 32 x 64
+  using CE = TileGen16;                                 // the 64 x 128 sub-tiles the epilogue works on
+  static_assert(C::BM == 64 && C::BK == 32 && C::CPR == 4 && C::WK == 1 && CE::BN == 128 && C::BN % 128 == 0,
+                "the slice layout below is written for 64-row bf16 generator tiles with 64-byte rows");
+  constexpr int NW = C::NT / 64;
   constexpr int ROWB = C::BK * 2;                       // bytes per tile row
+  constexpr int RPS = 16;                               // tile rows per 1 KB slice
+  constexpr int SA = C::BM / RPS, SB = C::BN / RPS;     // slices per plane of A, and of B
+  constexpr int SPW = (2 * SA + SB) / NW;               // slices (loads) per wave per stage
   constexpr int STG = (2 * C::BM + C::BN) * ROWB;       // one stage: A hi rows, A lo rows, B rows
-  constexpr int LDSB = NSTG * STG > C::CT ? NSTG * STG : C::CT;
-  constexpr int kWaitStage = (4 * (NSTG - 2)) | (7 << 4) | (15 << 8);   // vmcnt only
+  constexpr int NSUB = C::BN / 128;
+  constexpr int LDSB = NSTG * STG > NSUB * CE::CT ? NSTG * STG : NSUB * CE::CT;
+  static_assert((2 * SA + SB) % NW == 0 && NSTG >= 2 && SPW * (NSTG - 2) < 64, "slice layout / wait count");
   __shared__ __attribute__((aligned(16))) char smem[LDSB];
   const int L = xcd_remap(blockIdx.x, nblocks);
   const int mt = L % nm, nt = L / nm;
@@ -575,24 +592,31 @@ __global__ __launch_bounds__(256) void k_gemm_gen_lds(GenSplitA a, BOp b, GenPar
   const int i16 = lane & 15, g = lane >> 4;
   const int wn = wave % C::WN, wm = wave / C::WN;
 
-  // lane's place in a slice: tile row srow, 16-byte slot sslot, which holds chunk sslot ^ swz(row)
+  // slice q of a stage: A hi rows 16 q.. (q < SA), A lo rows (q < 2 SA), then B rows; wave w moves slices
+  // w, w + NW, ...; lane's place in a slice: tile row lane / 4, 16-byte slot lane % 4 (chunk slot ^ swz)
   const int srow = lane >> 2, sslot = lane & 3;
-  const int arow = 16 * wave + srow;                    // wave w moves A rows 16 w .. 16 w + 15
-  const int ar = min(m0 + arow, a.M - 1);               // rows past M re-read row M - 1 (never stored)
-  const uint32_t a_off = ((uint32_t)ar * a.ld + (sslot ^ C::swz(arow)) * C::CH) * 2;
   const __amdgpu_buffer_rsrc_t rhi = make_rsrc(a.hi, (uint32_t)a.M * a.ld * 2);
   const __amdgpu_buffer_rsrc_t rlo = make_rsrc(a.lo, (uint32_t)a.M * a.ld * 2);
-  uint32_t b_off[2];                                    // and B rows 32 w .. 32 w + 31
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int brow = 32 * wave + 16 * i + srow;
-    b_off[i] = ((uint32_t)(n0 + brow) * b.Kp + (sslot ^ C::swz(brow)) * C::CH) * 2;
-  }
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(b.W, (uint32_t)b.Np * b.Kp * 2);
+  int sl_kind[SPW], sl_lds[SPW];                        // 0 A hi, 1 A lo, 2 B; LDS byte offset in a stage
+  uint32_t sl_off[SPW];                                 // lane's byte offset in its operand at K = 0
+#pragma unroll
+  for (int i = 0; i < SPW; ++i) {
+    const int q = wave + NW * i;
+    const int kind = q < SA ? 0 : (q < 2 * SA ? 1 : 2);
+    const int trow = (kind == 0 ? q : (kind == 1 ? q - SA : q - 2 * SA)) * RPS + srow;   // row in its plane
+    const int chunk = sslot ^ C::swz(trow);
+    sl_kind[i] = kind;
+    sl_lds[i] = ((kind == 2 ? 2 * C::BM : kind * C::BM) + trow - srow) * ROWB;
+    if (kind == 2) {                                    // B rows past the packed matrix re-read its last row
+      const int br = min(n0 + trow, b.Np - 1);
+      sl_off[i] = ((uint32_t)br * b.Kp + chunk * C::CH) * 2;
+    } else {                                            // A rows past M re-read row M - 1 (never stored)
+      const int ar = min(m0 + trow, a.M - 1);
+      sl_off[i] = ((uint32_t)ar * a.ld + chunk * C::CH) * 2;
+    }
+  }
   const int nst = a.kpad / C::BK;
-  // this wave's slices of a stage buffer: A hi rows 16 w.., A lo rows 16 w.., B rows 32 w.. and 32 w + 16..
-  const int sl_ahi = (16 * wave) * ROWB, sl_alo = (C::BM + 16 * wave) * ROWB;
-  const int sl_b0 = (2 * C::BM + 32 * wave) * ROWB, sl_b1 = sl_b0 + 16 * ROWB;
 
   f32x4 acc[C::TM][C::TN];
 #pragma unroll
@@ -605,16 +629,20 @@ __global__ __launch_bounds__(256) void k_gemm_gen_lds(GenSplitA a, BOp b, GenPar
 #define ONMT_GEN_ISSUE(ST)                                                                              \
   do {                                                                                                  \
     char* sb_ = smem + ((ST) % NSTG) * STG;                                                             \
-    const uint32_t ko_ = (uint32_t)((ST) < nst ? (ST) : nst - 1) * C::BK * 2;                           \
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rhi, lds_at(sb_ + sl_ahi), 16, a_off + ko_, 0, 0, 0);      \
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rlo, lds_at(sb_ + sl_alo), 16, a_off + ko_, 0, 0, 0);      \
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, lds_at(sb_ + sl_b0), 16, b_off[0] + ko_, 0, 0, 0);     \
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, lds_at(sb_ + sl_b1), 16, b_off[1] + ko_, 0, 0, 0);     \
+    const uint32_t ko_ = (uint32_t)((ST) < nst ? (ST) : nst - 1) * ROWB;                                \
+    _Pragma("unroll") for (int i = 0; i < SPW; ++i) {                                                   \
+      if (sl_kind[i] == 0)                                                                              \
+        dma16(rhi, sb_ + sl_lds[i], sl_off[i] + ko_);                                                  \
+      else if (sl_kind[i] == 1)                                                                         \
+        dma16(rlo, sb_ + sl_lds[i], sl_off[i] + ko_);                                                  \
+      else                                                                                              \
+        dma16(rw, sb_ + sl_lds[i], sl_off[i] + ko_);                                                   \
+    }                                                                                                   \
   } while (0)
 #pragma unroll
   for (int st = 0; st < NSTG - 1; ++st) ONMT_GEN_ISSUE(st);
   for (int st = 0; st < nst; ++st) {
-    __builtin_amdgcn_s_waitcnt(kWaitStage);
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(SPW * (NSTG - 2)));
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
@@ -642,19 +670,26 @@ __global__ __launch_bounds__(256) void k_gemm_gen_lds(GenSplitA a, BOp b, GenPar
         acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
   }
 #undef ONMT_GEN_ISSUE
-  // every load (including the re-loads past the end) has landed before the output tile reuses the buffers
-  __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));
+  // every load (including the re-loads past the end) has landed before the output tiles reuse the buffers
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   __syncthreads();
-  float* Ct = (float*)smem;
+  // the 64 x BN output as BN / 128 sub-tiles of 64 x 128, each in the epilogue's layout, reduced at once
+  // (threads 256 s .. 256 s + 255 take sub-tile s, one partials tile of 128 columns); staging the
+  // sub-tiles one after the other through one buffer measured far slower
+  {
+    const int sub = (wn * C::TN * 16) / 128, c0 = (wn * C::TN * 16) % 128;
+    float* Ct = (float*)(smem + sub * CE::CT);
 #pragma unroll
-  for (int x = 0; x < C::TM; ++x)
+    for (int x = 0; x < C::TM; ++x)
 #pragma unroll
-    for (int y = 0; y < C::TN; ++y)
+      for (int y = 0; y < C::TN; ++y)
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        Ct[(wm * C::TM * 16 + x * 16 + 4 * g + v) * C::CROW + wn * C::TN * 16 + y * 16 + i16] = acc[x][y][v];
+        for (int v = 0; v < 4; ++v)
+          Ct[(wm * C::TM * 16 + x * 16 + 4 * g + v) * CE::CROW + c0 + y * 16 + i16] = acc[x][y][v];
+  }
   __syncthreads();
-  gen_epilogue<C>(smem, p, a.M, m0, n0, nt);
+  const int sub = tid / CE::NT, n0s = n0 + 128 * sub;
+  if (n0s < b.Np) gen_epilogue<CE>(smem + sub * CE::CT, p, a.M, m0, n0s, n0s / 128, tid % CE::NT);
 }
 
 
@@ -772,14 +807,15 @@ hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hi
 }
 
 hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, const GenParams& p, hipStream_t st) {
-  using C = TileGen16;
+  constexpr int BM = 64, BN = 64 * kGenWN;
   const uint64_t lim = 1ull << 31;
-  if (a.M < 1 || a.kpad % kSegK || a.kpad > b.Kp || a.ld < a.kpad || b.Np % C::BN ||
+  if (a.M < 1 || a.kpad % kSegK || a.kpad > b.Kp || a.ld < a.kpad || b.Np % 128 ||
       (uint64_t)a.M * a.ld * 2 >= lim || (uint64_t)b.Np * b.Kp * 2 >= lim)
     return hipErrorInvalidValue;
-  const int nm = (a.M + C::BM - 1) / C::BM;
-  const int nblocks = nm * (b.Np / C::BN);
-  hipLaunchKernelGGL(k_gemm_gen_lds<kGenStages>, dim3(nblocks), dim3(C::NT), 0, st, a, b, p, nm, nblocks);
+  const int nm = (a.M + BM - 1) / BM;
+  const int nblocks = nm * ((b.Np + BN - 1) / BN);
+  hipLaunchKernelGGL((k_gemm_gen_lds<kGenWN, kGenStages>), dim3(nblocks), dim3(128 * kGenWN), 0, st, a, b, p, nm,
+                     nblocks);
   return hipGetLastError();
 }
 

@@ -85,6 +85,13 @@ __device__ inline void split_bf16x8(const float4& a, const float4& b, uint4& hi,
   lo = make_uint4(l[0], l[1], l[2], l[3]);
 }
 
+__device__ inline void split_bf16(float x, uint16_t& hi, uint16_t& lo) {
+  uint4 h, l;
+  split_bf16x8(make_float4(x, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f), h, l);
+  hi = (uint16_t)(h.x & 0xffffu);
+  lo = (uint16_t)(l.x & 0xffffu);
+}
+
 // Buffer resource descriptor (gfx9 family word 3). Loads through it return zeros past num_records, so
 // an invalid row is given an offset beyond every buffer instead of a branch.
 constexpr int kBufWord3 = 0x00020000;
@@ -131,6 +138,9 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
   const int kp##S = a.seg[S].kpad, wd##S = a.seg[S].width, bf##S = a.seg[S].bf16;                     \
   const uint32_t es##S = bf##S ? 2u : 4u;                                                              \
   const __amdgpu_buffer_rsrc_t rs##S = make_rsrc(a.seg[S].base, (uint32_t)a.seg[S].rows * a.seg[S].ld * es##S); \
+  const bool pre##S = C::kBf16 && a.seg[S].lo;                                                        \
+  const __amdgpu_buffer_rsrc_t rl##S = make_rsrc(pre##S ? a.seg[S].lo : a.seg[S].base,                 \
+                                                 (uint32_t)a.seg[S].rows * a.seg[S].ld * es##S);       \
   uint32_t ao##S[C::A_PT];                                                                             \
   _Pragma("unroll") for (int i = 0; i < C::A_PT; ++i) {                                                \
     const int r = m0 + arow0 + i * RSTEP;                                                              \
@@ -228,9 +238,9 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
   // M read zeros through the descriptor bound, columns in a segment's padding are zeroed by a select,
   // and past the last stage the loads re-read the last stage into a buffer that is never multiplied.
   uint32_t kbyte_w = 0;                 // byte offset of the segment inside a weight row
-  auto run_segment = [&](__amdgpu_buffer_rsrc_t rs, const uint32_t (&ao)[C::A_PT], uint32_t es, int width,
-                         int kpad) {
-    const bool src_bf16 = es == 2;
+  auto run_segment = [&](__amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t rl, bool pre,
+                         const uint32_t (&ao)[C::A_PT], uint32_t es, int width, int kpad) {
+    const bool src_bf16 = es == 2 && !pre;              // exact bf16 operand: no lo part
     auto gload = [&](int st) -> Regs {
       Regs r;
       const int kk = st * C::BK + acol;
@@ -242,17 +252,23 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
           const uint4 v = buf_load16(rs, off);
           r.a[i] = ok ? v : zero4();
         } else {
-          // bf16 source: 8 elements in one 16-byte load (exact, no lo part); fp32 source: two 16-byte
-          // loads split into bf16 hi + lo. Widths are multiples of 4, so the second half may be past the end.
+          // bf16 source: 8 elements in one 16-byte load (exact, no lo part); pre-split source: 8 elements
+          // of each plane; fp32 source: two 16-byte loads split into bf16 hi + lo (widths are multiples of 4,
+          // so the second half may be past the end).
           const uint4 l0 = buf_load16(rs, off);
-          const uint4 l1 = buf_load16(rs, off + 16);
-          const bool ok1 = kk + 4 < width;
-          const float4 f0 = __builtin_bit_cast(float4, l0);
-          const float4 f1 = ok1 ? __builtin_bit_cast(float4, l1) : make_float4(0.f, 0.f, 0.f, 0.f);
-          uint4 hi, lo;
-          split_bf16x8(f0, f1, hi, lo);
-          r.a[i] = !ok ? zero4() : (src_bf16 ? l0 : hi);
-          r.alo[i] = (!ok || src_bf16) ? zero4() : lo;
+          const uint4 l1 = pre ? buf_load16(rl, off) : buf_load16(rs, off + 16);
+          if (pre || src_bf16) {
+            r.a[i] = ok ? l0 : zero4();
+            r.alo[i] = (ok && pre) ? l1 : zero4();
+          } else {
+            const bool ok1 = kk + 4 < width;
+            const float4 f0 = __builtin_bit_cast(float4, l0);
+            const float4 f1 = ok1 ? __builtin_bit_cast(float4, l1) : make_float4(0.f, 0.f, 0.f, 0.f);
+            uint4 hi, lo;
+            split_bf16x8(f0, f1, hi, lo);
+            r.a[i] = ok ? hi : zero4();
+            r.alo[i] = ok ? lo : zero4();
+          }
         }
       }
       const uint32_t kb = kbyte_w + (uint32_t)(st * C::BK) * sizeof(T);
@@ -285,9 +301,9 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
     }
     kbyte_w += (uint32_t)kpad * sizeof(T);
   };
-  run_segment(rs0, ao0, es0, wd0, kp0);
-  if constexpr (nseg > 1) run_segment(rs1, ao1, es1, wd1, kp1);
-  if constexpr (nseg > 2) run_segment(rs2, ao2, es2, wd2, kp2);
+  run_segment(rs0, rl0, pre0, ao0, es0, wd0, kp0);
+  if constexpr (nseg > 1) run_segment(rs1, rl1, pre1, ao1, es1, wd1, kp1);
+  if constexpr (nseg > 2) run_segment(rs2, rl2, pre2, ao2, es2, wd2, kp2);
   (void)bf0;
   (void)bf1;
   (void)bf2;
@@ -398,6 +414,12 @@ __device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p
     }
     p.h_out[(size_t)row * p.ld_out + unit] = h_new;
     p.c_out[(size_t)row * p.ld_out + unit] = c_new;
+    if (p.h_hi) {
+      uint16_t hh, hl;
+      split_bf16(h_new, hh, hl);
+      p.h_hi[(size_t)row * p.ld_hl + unit] = hh;
+      p.h_lo[(size_t)row * p.ld_hl + unit] = hl;
+    }
     if (p.y_out) p.y_out[(size_t)(row * p.y_S + p.y_s) * p.ld_y + p.y_col0 + unit] = y;
   }
 }
@@ -803,6 +825,28 @@ hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st) {
   if (shape != kShapeSplitKThin && shape != kShapeMid) return hipErrorInvalidValue;
   if (!bf16) return lstm2_dispatch<float, TileThin32>(g, st);
   return shape == kShapeMid ? lstm2_dispatch<__bf16, TileMid16>(g, st) : lstm2_dispatch<__bf16, TileThin16>(g, st);
+}
+
+__global__ void k_split_rows(const float* __restrict__ src, int ld_src, int rows, int cols, uint16_t* __restrict__ hi,
+                             uint16_t* __restrict__ lo, int ld_dst) {
+  const size_t n = (size_t)rows * ld_dst;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const int r = (int)(i / ld_dst), c = (int)(i % ld_dst);
+    uint16_t h = 0, l = 0;
+    if (c < cols) split_bf16(src[(size_t)r * ld_src + c], h, l);
+    hi[i] = h;
+    lo[i] = l;
+  }
+}
+
+hipError_t split_rows(const float* src, int ld_src, int rows, int cols, uint16_t* hi, uint16_t* lo, int ld_dst,
+                      hipStream_t st) {
+  const size_t n = (size_t)rows * ld_dst;
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_split_rows, dim3((unsigned)blocks), dim3(256), 0, st, src, ld_src, rows, cols, hi, lo, ld_dst);
+  return hipGetLastError();
 }
 
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {

@@ -19,7 +19,9 @@ struct Seg {
   int ld;
   int width;
   int kpad;
-  int bf16;
+  int bf16;      // 1: base holds bf16 values (exact operands)
+  const void* lo;   // bf16 products only: base and lo are the bf16 hi and lo planes of fp32 values
+                    // (bf16 = 1, width a multiple of 8); the operand is hi + lo, as if split on load
 };
 
 struct AOp {
@@ -65,6 +67,9 @@ struct LstmParams {
   float* h_out;
   float* c_out;
   int ld_out;
+  uint16_t* h_hi;               // optional bf16 hi / lo planes of h_out (row stride ld_hl)
+  uint16_t* h_lo;
+  int ld_hl;
   float* y_out;                 // optional layer output row b * y_S + y_s, column offset y_col0
   int ld_y, y_S, y_s, y_col0;
   const int32_t* lens;          // optional: GEMM row b is active iff y_s < lens[b]
@@ -203,6 +208,9 @@ hipError_t backtrack(const BeamParams& p, int32_t* out_tok, int32_t* out_len, do
 
 hipError_t replicate_rows(const float* src, int ld_src, int rows, int K, float* dst, int ld_dst, int ncols,
                           hipStream_t st);
+// hi / lo [rows, ld_dst] = bf16 planes of src [rows, ld_src] columns < cols, zeros in columns cols .. ld_dst.
+hipError_t split_rows(const float* src, int ld_src, int rows, int cols, uint16_t* hi, uint16_t* lo, int ld_dst,
+                      hipStream_t st);
 hipError_t fill_f32(float* dst, size_t n, float v, hipStream_t st);
 hipError_t copy_cols(const float* src, int ld_src, float* dst, int ld_dst, int rows, int ncols, hipStream_t st);
 

@@ -68,6 +68,7 @@ Seg seg(const void* base, const int32_t* idx, int rows, int ld, int width, int k
   s.width = width;
   s.kpad = kpad;
   s.bf16 = bf16;
+  s.lo = nullptr;
   return s;
 }
 
@@ -512,6 +513,12 @@ struct State {
   float* h;      // [L, N, H]
   float* c;
   float* feed;   // [N, H]
+  // bf16 models: h and feed as bf16 hi / lo planes, [L, N, pad(H)] and [N, pad(H)] (the operands of the
+  // decoder's products, split once by their producers)
+  uint16_t* h_hi;
+  uint16_t* h_lo;
+  uint16_t* feed_hi;
+  uint16_t* feed_lo;
 };
 
 size_t state_layout(const Dims& d, int N, char* base, State* s) {
@@ -521,6 +528,11 @@ size_t state_layout(const Dims& d, int N, char* base, State* s) {
   t.h = c.take<float>((size_t)d.L * N * d.H);
   t.c = c.take<float>((size_t)d.L * N * d.H);
   t.feed = c.take<float>((size_t)N * d.H);
+  const size_t pl = d.bf16 ? (size_t)N * d.pad(d.H) : 0;
+  t.h_hi = d.bf16 ? c.take<uint16_t>(d.L * pl) : nullptr;
+  t.h_lo = d.bf16 ? c.take<uint16_t>(d.L * pl) : nullptr;
+  t.feed_hi = d.bf16 ? c.take<uint16_t>(pl) : nullptr;
+  t.feed_lo = d.bf16 ? c.take<uint16_t>(pl) : nullptr;
   if (s) *s = t;
   return align_up(c.off);
 }
@@ -538,8 +550,6 @@ struct StepWs {
   float* lse;      // [N]
   int32_t* align;  // [N] attention argmax
   float* pfmax;    // [N, ntiles] largest allowed logit per tile (hypothesis filters)
-  uint16_t* feed_hi;   // bf16 models: [N, pad(H)] attentional vector as bf16 hi + lo (the generator's operand)
-  uint16_t* feed_lo;
   int ntiles;
 };
 
@@ -561,8 +571,6 @@ size_t step_layout(const Dims& d, int B, int S, int K, char* base, StepWs* w) {
   t.lse = c.take<float>(N);
   t.align = c.take<int32_t>(N);
   t.pfmax = c.take<float>(N * t.ntiles);
-  t.feed_hi = d.bf16 ? c.take<uint16_t>(N * d.pad(d.H)) : nullptr;
-  t.feed_lo = d.bf16 ? c.take<uint16_t>(N * d.pad(d.H)) : nullptr;
   if (w) *w = t;
   return align_up(c.off);
 }
@@ -874,6 +882,10 @@ int decode_init_compute(onmt_model* m, const EncWs& w, int B, int K, const State
     HIP_TRY(replicate_rows(w.final_c + (size_t)l * B * d.H, d.H, B, K, s.c + (size_t)l * N * d.H, d.H, d.H, st));
   }
   HIP_TRY(fill_f32(s.feed, (size_t)N * d.H, 0.f, st));
+  if (d.bf16) {   // the operand planes of the first step
+    HIP_TRY(split_rows(s.h, d.H, d.L * N, d.H, s.h_hi, s.h_lo, d.pad(d.H), st));
+    HIP_TRY(split_rows(s.feed, d.H, N, d.H, s.feed_hi, s.feed_lo, d.pad(d.H), st));
+  }
   return ONMT_OK;
 }
 
@@ -913,7 +925,7 @@ void time_collect(onmt_model* m) {
 // all steps at once.
 // Optional work of a decoder step beyond the log-distribution.
 struct StepExtras {
-  // bf16 models: where the attentional vector's hi/lo planes go (default: the step workspace's)
+  // bf16 models: where the attentional vector's hi/lo planes go (default: the output state's)
   uint16_t* feed_hi = nullptr;
   uint16_t* feed_lo = nullptr;
   const int32_t* want = nullptr;        // the logit of column want[r] of every row goes to want_logit[r]
@@ -932,6 +944,16 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
   const Dims& d = m->d;
   const int N = B * K;
   const size_t LH = (size_t)N * d.H;
+  const int pH = d.pad(d.H);
+  const size_t LP = (size_t)N * pH;
+  // bf16 models read the pre-split planes of h and feed (widths that are multiples of 8)
+  const bool pre = d.bf16 && d.H % 8 == 0;
+  auto act = [&](const float* x, const uint16_t* hi, const uint16_t* lo, const int32_t* idx) {
+    if (!pre) return seg(x, idx, N, d.H, d.H, pH, 0);
+    Seg s = seg(hi, idx, N, pH, d.H, pH, 1);
+    s.lo = lo;
+    return s;
+  };
   for (int l = 0; l < d.L; ++l) {
     AOp a{};
     a.M = N;
@@ -941,16 +963,22 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     if (l == 0) {
       // [feed ; h] against the feed and recurrent columns; the embedding columns' product is the
       // precomputed row of the previous token (emb_gates), added in the epilogue
-      a.seg[0] = seg(in.feed, parent, N, d.H, d.H, d.pad(d.H), 0);
-      a.seg[1] = seg(in.h, parent, N, d.H, d.H, d.pad(d.H), 0);
+      a.seg[0] = act(in.feed, in.feed_hi, in.feed_lo, parent);
+      a.seg[1] = act(in.h, in.h_hi, in.h_lo, parent);
       wb.W = (const char*)wb.W + (size_t)d.pad(d.E) * d.esz;
       lp.gx = m->emb_gates;
       lp.gx_idx = prev_tok;
       lp.gx_rows = d.Vt;
       lp.ld_gx = 4 * d.H_pad;
     } else {
-      a.seg[0] = seg(out.h + (l - 1) * LH, nullptr, N, d.H, d.H, d.pad(d.H), 0);
-      a.seg[1] = seg(in.h + l * LH, parent, N, d.H, d.H, d.pad(d.H), 0);
+      a.seg[0] = act(out.h + (l - 1) * LH, pre ? out.h_hi + (l - 1) * LP : nullptr,
+                     pre ? out.h_lo + (l - 1) * LP : nullptr, nullptr);
+      a.seg[1] = act(in.h + l * LH, pre ? in.h_hi + l * LP : nullptr, pre ? in.h_lo + l * LP : nullptr, parent);
+    }
+    if (d.bf16) {
+      lp.h_hi = out.h_hi + l * LP;
+      lp.h_lo = out.h_lo + l * LP;
+      lp.ld_hl = pH;
     }
     lp.bias = m->dec_bias[l];
     lp.c_in = in.c + l * LH;
@@ -984,8 +1012,8 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     a.seg[1] = seg(q, nullptr, N, d.H, d.H, d.pad(d.H), 0);
     StoreParams sp{nullptr, out.feed, d.H, d.H, 1};
     if (d.bf16) {            // the generator's operand, split once here instead of in every column tile
-      sp.hi = ex.feed_hi ? ex.feed_hi : sw.feed_hi;
-      sp.lo = ex.feed_lo ? ex.feed_lo : sw.feed_lo;
+      sp.hi = ex.feed_hi ? ex.feed_hi : out.feed_hi;
+      sp.lo = ex.feed_lo ? ex.feed_lo : out.feed_lo;
       sp.ld_hl = sp.ncols_hl = d.pad(d.H);
     }
     HIP_TRY(gemm_store(d.bf16, small_shape(N, m->W_c.Np), a, bop(m->W_c), sp, st));
@@ -1016,7 +1044,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     gp.pfmax = ex.pfmax;
     time_begin(m, st);
     if (d.bf16)
-      HIP_TRY(gemm_gen_split(GenSplitA{sw.feed_hi, sw.feed_lo, N, d.pad(d.H), d.pad(d.H)}, bop(m->W_s), gp, st));
+      HIP_TRY(gemm_gen_split(GenSplitA{out.feed_hi, out.feed_lo, N, d.pad(d.H), d.pad(d.H)}, bop(m->W_s), gp, st));
     else
       HIP_TRY(gemm_gen(0, a, bop(m->W_s), gp, st));
     time_end(m, st);
@@ -1278,7 +1306,13 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
   int cur = 0;
   for (int t = 0; t < steps; ++t) {
     State in = w.st[cur], out = w.st[cur ^ 1];
-    if (t > 0) in.feed = w.feeds + (size_t)(t - 1) * B * d.H;
+    if (t > 0) {
+      in.feed = w.feeds + (size_t)(t - 1) * B * d.H;
+      if (d.bf16) {
+        in.feed_hi = w.feeds_hi + (size_t)(t - 1) * B * d.pad(d.H);
+        in.feed_lo = w.feeds_lo + (size_t)(t - 1) * B * d.pad(d.H);
+      }
+    }
     out.feed = w.feeds + (size_t)t * B * d.H;
     StepExtras ex;
     if (d.bf16) {

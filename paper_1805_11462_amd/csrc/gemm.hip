@@ -559,7 +559,12 @@ using TileSplit32 = Tile<float, 1, 1, 4, 2, 4, 16>;
 // 16 x 32 tiles for GEMMs with few rows: twice the workgroups of a 16 x 64 tiling, which keeps more
 // loads in flight per CU (the decoder GEMMs at a few hundred rows are bound by that, not by MFMA).
 using TileThin32 = Tile<float, 1, 1, 4, 1, 2, 16>;
-using TileWide16 = Tile<__bf16, 2, 2, 1, 2, 4, 64>;
+// fp32 plain stores with few rows (W_c, concat's query projection): 16 x 16 tiles, twice the workgroups
+// of the 16 x 32 LSTM tile (W_c at 320 rows: 8.9 instead of 10.0 us)
+using TileStore32 = Tile<float, 1, 1, 4, 1, 1, 16>;
+// bf16 stores over many rows (encoder projections, keys, the embedding-gate table): 128 x 128 tiles of
+// 8 waves, K stages of 32 (28% faster than 64 x 128 with K stages of 64 at 20480 x 4096 x 1024).
+using TileWide16 = Tile<__bf16, 4, 2, 1, 2, 4, 32>;
 using TileSplit16 = Tile<__bf16, 1, 1, 4, 2, 4, 32>;
 using TileThin16 = Tile<__bf16, 1, 1, 4, 1, 4, 32>;
 // bf16 LSTM GEMMs of a few hundred rows: 32 x 64 tiles, two waves per K half. Against the 16 x 64 tile
@@ -797,7 +802,7 @@ hipError_t gemm_store(int bf16, int shape, const AOp& a, const BOp& b, const Sto
   }
   if (shape == kShapeWide) return launch_store<float, TileWide32>(a, b, p, st);
   if (shape == kShapeSplitK) return launch_store<float, TileSplit32>(a, b, p, st);
-  return launch_store<float, TileThin32>(a, b, p, st);
+  return launch_store<float, TileStore32>(a, b, p, st);
 }
 
 hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const LstmParams& p, hipStream_t st) {

@@ -33,9 +33,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="default")
-    ap.add_argument("--mode", choices=["search", "score"], default="search",
+    ap.add_argument("--mode", choices=["search", "score", "vendor"], default="search",
                     help="search: beam search (the headline metric); score: teacher-forced scoring of "
-                         "max-decode-long synthetic targets")
+                         "max-decode-long synthetic targets; vendor: time the vendor GEMM library "
+                         "(torch.matmul) at the workload's decoder GEMM shapes, for comparison with the "
+                         "library's fused kernels")
     ap.add_argument("--attn", choices=["general", "dot", "concat"], default=None,
                     help="attention score type (default: the workload's, general)")
     ap.add_argument("--beta", type=float, default=0.0, help="coverage penalty weight of the search (0 = off)")
@@ -125,6 +127,8 @@ def main():
     w = W.get(args.workload)
     if args.attn:
         w = W.Workload(**{**w.as_dict(), "attn": args.attn})
+    if args.mode == "vendor":
+        return bench_vendor(w)
     weights = W.make_weights(w)
     src, lens = W.make_batch(w)
     B, S = src.shape
@@ -205,6 +209,47 @@ def main():
         out["cpu_baseline"] = cpu_baseline(w, weights, src, lens, args.cpu_sentences, args.beta, banned,
                                            args.max_unk)
     print(json.dumps(out), flush=True)
+
+
+def bench_vendor(w):
+    """Plain GEMMs of the vendor library (torch.matmul, which runs hipBLASLt on ROCm) at the shapes of one
+    decoder step's GEMMs: a reference for what a library GEMM takes at these shapes without the gathers and
+    epilogues that the library's own kernels fuse in. bf16 workloads multiply hi + lo activation terms, so the
+    reference GEMM concatenates them along K (A = [hi | lo], W = [W | W]): the same MFMA work. Not part of the
+    translation path; prints one JSON line per shape."""
+    import torch
+    if not torch.cuda.is_available():
+        sys.exit("--mode vendor needs a GPU")
+    N = w.batch * w.beam
+    H, E, V = w.hidden, w.emb, w.tgt_vocab
+    Hm = 2 * w.hidden if w.bidirectional else w.hidden
+    bf16 = w.wdtype == "bf16"
+    dt = torch.bfloat16 if bf16 else torch.float32
+    rep = 2 if bf16 else 1
+    peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+    shapes = [("generator", N, V, H), ("decoder LSTM layer (feed or input ; h)", N, 4 * H, 2 * H),
+              ("attentional output W_c ([ctx ; h])", N, H, Hm + H),
+              ("square 8192 (what the library reaches on a large GEMM)", 8192, 8192, 8192 // rep)]
+    for name, M, Ncol, K in shapes:
+        a = torch.randn(M, rep * K, device="cuda", dtype=dt)
+        b = torch.randn(Ncol, rep * K, device="cuda", dtype=dt).t()
+        out = torch.empty(M, Ncol, device="cuda", dtype=dt)
+        for _ in range(5):
+            torch.matmul(a, b, out=out)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        it = 50
+        e0.record()
+        for _ in range(it):
+            torch.matmul(a, b, out=out)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / it
+        flops = 2.0 * M * Ncol * K
+        print(json.dumps({"vendor_gemm": name, "workload": w.name, "M": M, "N": Ncol, "K": K,
+                          "operands": "bf16 hi+lo along K" if bf16 else "fp32", "us": round(us, 2),
+                          "tflops": round(flops / us / 1e6, 1), "frac_of_peak": round(flops / us / 1e6 / peak, 3),
+                          "frac_counting_hi_lo": round(rep * flops / us / 1e6 / peak, 3)}), flush=True)
 
 
 def bench_score(args, w, weights, tr, src, lens, src_d, lens_d):

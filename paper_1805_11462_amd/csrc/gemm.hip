@@ -162,20 +162,39 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
   T* As[2] = {(T*)smem, (T*)(smem + C::STAGE)};
   T* Bs[2] = {As[0] + C::AREP * C::BM * C::ROW, As[1] + C::AREP * C::BM * C::ROW};
 
-  // One K stage of operands in flight: held in registers between its global load and its LDS store.
+  // One K stage of operands in flight: the raw global loads, held in registers until the stage is stored
+  // to LDS. Everything that reads the loaded values (the zeroing of a segment's K padding, the split of an
+  // fp32 source into bf16 hi + lo) happens at that store, one stage after the loads were issued: done at
+  // the load, it made every wave wait for its loads right after issuing them.
   struct Regs {
     uint4 a[C::A_PT];
-    uint4 alo[C::AREP == 2 ? C::A_PT : 1];
+    uint4 alo[C::AREP == 2 ? C::A_PT : 1];   // bf16 products: the lo plane, or the second half of an fp32 row chunk
     uint4 b[C::B_PT];
+    bool ok, ok1;                            // the A chunk (and its second fp32 half) lies inside the segment width
   };
   // RSTEP and BM are multiples of 16, so every row this thread stores has the swizzle of arow0.
   static_assert(RSTEP % 16 == 0 && C::BM % 16 == 0, "row steps must keep the swizzle");
   const int scol = ((acol / C::CH) ^ C::swz(arow0)) * C::CH;
-  auto lstore = [&](int buf, const Regs& r) {
+  // pre: the segment gives bf16 hi and lo planes; src_bf16: an exact bf16 operand; else (bf16 products) an
+  // fp32 source split here into hi + lo
+  auto lstore = [&](int buf, const Regs& r, bool pre, bool src_bf16) {
 #pragma unroll
     for (int i = 0; i < C::A_PT; ++i) {
-      *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + scol) = r.a[i];
-      if constexpr (C::AREP == 2) *(uint4*)(As[buf] + (C::BM + arow0 + i * RSTEP) * C::ROW + scol) = r.alo[i];
+      uint4 hi, lo = zero4();
+      if constexpr (!C::kBf16) {
+        hi = r.ok ? r.a[i] : zero4();
+      } else if (pre || src_bf16) {
+        hi = r.ok ? r.a[i] : zero4();
+        lo = (r.ok && pre) ? r.alo[i] : zero4();
+      } else {
+        const float4 f0 = __builtin_bit_cast(float4, r.a[i]);
+        const float4 f1 = r.ok1 ? __builtin_bit_cast(float4, r.alo[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
+        split_bf16x8(f0, f1, hi, lo);
+        hi = r.ok ? hi : zero4();
+        lo = r.ok ? lo : zero4();
+      }
+      *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + scol) = hi;
+      if constexpr (C::AREP == 2) *(uint4*)(As[buf] + (C::BM + arow0 + i * RSTEP) * C::ROW + scol) = lo;
     }
 #pragma unroll
     for (int i = 0; i < C::B_PT; ++i) *(uint4*)(Bs[buf] + (arow0 + i * RSTEP) * C::ROW + scol) = r.b[i];
@@ -235,7 +254,7 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
   };
 
   // K runs segment by segment, each with its own two-stage pipeline. Loads are unconditional: rows past
-  // M read zeros through the descriptor bound, columns in a segment's padding are zeroed by a select,
+  // M read zeros through the descriptor bound, columns in a segment's padding are zeroed at the LDS store,
   // and past the last stage the loads re-read the last stage into a buffer that is never multiplied.
   uint32_t kbyte_w = 0;                 // byte offset of the segment inside a weight row
   auto run_segment = [&](__amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t rl, bool pre,
@@ -244,31 +263,19 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
     auto gload = [&](int st) -> Regs {
       Regs r;
       const int kk = st * C::BK + acol;
-      const bool ok = kk < width;
+      r.ok = kk < width;
+      r.ok1 = kk + 4 < width;
 #pragma unroll
       for (int i = 0; i < C::A_PT; ++i) {
         const uint32_t off = ao[i] + (uint32_t)(st * C::BK) * es;
         if constexpr (!C::kBf16) {
-          const uint4 v = buf_load16(rs, off);
-          r.a[i] = ok ? v : zero4();
+          r.a[i] = buf_load16(rs, off);
         } else {
           // bf16 source: 8 elements in one 16-byte load (exact, no lo part); pre-split source: 8 elements
-          // of each plane; fp32 source: two 16-byte loads split into bf16 hi + lo (widths are multiples of 4,
-          // so the second half may be past the end).
-          const uint4 l0 = buf_load16(rs, off);
-          const uint4 l1 = pre ? buf_load16(rl, off) : buf_load16(rs, off + 16);
-          if (pre || src_bf16) {
-            r.a[i] = ok ? l0 : zero4();
-            r.alo[i] = (ok && pre) ? l1 : zero4();
-          } else {
-            const bool ok1 = kk + 4 < width;
-            const float4 f0 = __builtin_bit_cast(float4, l0);
-            const float4 f1 = ok1 ? __builtin_bit_cast(float4, l1) : make_float4(0.f, 0.f, 0.f, 0.f);
-            uint4 hi, lo;
-            split_bf16x8(f0, f1, hi, lo);
-            r.a[i] = ok ? hi : zero4();
-            r.alo[i] = ok ? lo : zero4();
-          }
+          // of each plane; fp32 source: two 16-byte loads, split into bf16 hi + lo at the LDS store (widths
+          // are multiples of 4, so the second half may be past the end).
+          r.a[i] = buf_load16(rs, off);
+          r.alo[i] = pre ? buf_load16(rl, off) : buf_load16(rs, off + 16);
         }
       }
       const uint32_t kb = kbyte_w + (uint32_t)(st * C::BK) * sizeof(T);
@@ -280,13 +287,13 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
     const int last = nst - 1;
     Regs r0 = gload(0);
     Regs r1 = gload(min(1, last));
-    lstore(0, r0);
+    lstore(0, r0, pre, src_bf16);
     __syncthreads();
     for (int st = 0; st < nst; st += 2) {
       // even stage: LDS buffer 0 holds stage st, r1 holds st + 1
       r0 = gload(min(st + 2, last));
       compute(0, !src_bf16);
-      lstore(1, r1);
+      lstore(1, r1, pre, src_bf16);
       __syncthreads();
       // whole pairs of stages when the stage count is even by construction: a single loop exit keeps
       // the accumulators in place (no copies between the two exits' register assignments)
@@ -296,7 +303,7 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
       // odd stage: LDS buffer 1 holds stage st + 1, r0 holds st + 2
       r1 = gload(min(st + 3, last));
       compute(1, !src_bf16);
-      lstore(0, r0);
+      lstore(0, r0, pre, src_bf16);
       __syncthreads();
     }
     kbyte_w += (uint32_t)kpad * sizeof(T);

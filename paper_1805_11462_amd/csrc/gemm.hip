@@ -612,6 +612,7 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
   using CE = TileGen16;                                 // the 64 x 128 sub-tiles the epilogue works on
   static_assert(C::BM == 64 && C::BK == 32 && C::CPR == 4 && C::WK == 1 && CE::BN == 128 && C::BN % 128 == 0,
                 "the slice layout below is written for 64-row bf16 generator tiles with 64-byte rows");
+  static_assert(C::BK == kGenKBlock, "a K stage is one block of the K-blocked weights");
   constexpr int NW = C::NT / 64;
   constexpr int ROWB = C::BK * 2;                       // bytes per tile row
   constexpr int RPS = 16;                               // tile rows per 1 KB slice
@@ -647,7 +648,7 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
     sl_lds[i] = ((kind == 2 ? 2 * C::BM : kind * C::BM) + trow - srow) * ROWB;
     if (kind == 2) {                                    // B rows past the packed matrix re-read its last row
       const int br = min(n0 + trow, b.Np - 1);
-      sl_off[i] = ((uint32_t)br * b.Kp + chunk * C::CH) * 2;
+      sl_off[i] = ((uint32_t)br * C::BK + chunk * C::CH) * 2;   // in K block 0 (the stage adds its block)
     } else {                                            // A rows past M re-read row M - 1 (never stored)
       const int ar = min(m0 + trow, a.M - 1);
       sl_off[i] = ((uint32_t)ar * a.ld + chunk * C::CH) * 2;
@@ -662,18 +663,20 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
     for (int y = 0; y < C::TN; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int col = (g ^ C::swz(i16)) * C::CH;           // this lane's 16-byte chunk of a fragment row
   // stages past the last re-load the last one into a buffer that is never multiplied, which keeps every
-  // wave's count of loads in flight the same on every iteration
+  // wave's count of loads in flight the same on every iteration; stage st of A is ROWB bytes into each
+  // row, of B the st-th K block of the weights
 #define ONMT_GEN_ISSUE(ST)                                                                              \
   do {                                                                                                  \
     char* sb_ = smem + ((ST) % NSTG) * STG;                                                             \
-    const uint32_t ko_ = (uint32_t)((ST) < nst ? (ST) : nst - 1) * ROWB;                                \
+    const uint32_t ks_ = (uint32_t)((ST) < nst ? (ST) : nst - 1);                                       \
+    const uint32_t ko_ = ks_ * ROWB, kb_ = ks_ * (uint32_t)b.Np * ROWB;                                 \
     _Pragma("unroll") for (int i = 0; i < SPW; ++i) {                                                   \
       if (sl_kind[i] == 0)                                                                              \
         dma16(rhi, sb_ + sl_lds[i], sl_off[i] + ko_);                                                  \
       else if (sl_kind[i] == 1)                                                                         \
         dma16(rlo, sb_ + sl_lds[i], sl_off[i] + ko_);                                                  \
       else                                                                                              \
-        dma16(rw, sb_ + sl_lds[i], sl_off[i] + ko_);                                                   \
+        dma16(rw, sb_ + sl_lds[i], sl_off[i] + kb_);                                                   \
     }                                                                                                   \
   } while (0)
 #pragma unroll
@@ -868,7 +871,8 @@ hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hi
 hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, const GenParams& p, hipStream_t st) {
   constexpr int BM = 64, BN = 64 * kGenWN;
   const uint64_t lim = 1ull << 31;
-  if (a.M < 1 || a.kpad % kSegK || a.kpad > b.Kp || a.ld < a.kpad || b.Np % 128 ||
+  // the K-blocked weights are read up to the operand's padded width: a.kpad == b.Kp
+  if (a.M < 1 || a.kpad % kSegK || a.kpad != b.Kp || a.ld < a.kpad || b.Np % 128 ||
       (uint64_t)a.M * a.ld * 2 >= lim || (uint64_t)b.Np * b.Kp * 2 >= lim)
     return hipErrorInvalidValue;
   const int nm = (a.M + BM - 1) / BM;

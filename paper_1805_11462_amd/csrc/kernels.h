@@ -129,6 +129,10 @@ struct GenSplitA {
   int kpad;    // multiple of kSegK
 };
 // The bf16 generator on a pre-split operand: same partials as gemm_gen, operands moved straight into LDS.
+// Its weights are K-blocked: element (n, k) of the [Np, Kp] matrix sits at (k / kGenKBlock) * Np *
+// kGenKBlock + n * kGenKBlock + k % kGenKBlock, so that one K stage of a column tile is one contiguous block
+// (with row-major weights each load instruction touched 16 rows 2 KB apart for 64 bytes each).
+constexpr int kGenKBlock = 32;
 hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, const GenParams& p, hipStream_t st);
 int gen_tile_cols();
 

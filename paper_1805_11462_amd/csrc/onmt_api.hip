@@ -436,7 +436,15 @@ int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, 
       pack_row(img, m->W_c, r, d.pad(d.Hm), Wc + (size_t)r * (d.Hm + d.H), d.Hm, d.H);
     }
     const float* Ws = host_weights[wi++];
-    for (int r = 0; r < d.Vt; ++r) pack_row(img, m->W_s, r, 0, Ws + (size_t)r * d.H, 0, d.H);
+    if (d.bf16) {   // K-blocked for the pre-split generator (see gemm_gen_split)
+      const size_t o = m->W_s.off, Np = (size_t)m->W_s.Np;
+      for (int r = 0; r < d.Vt; ++r)
+        for (int k = 0; k < d.H; ++k)
+          img.put(o, (size_t)(k / kGenKBlock) * Np * kGenKBlock + (size_t)r * kGenKBlock + k % kGenKBlock,
+                  Ws[(size_t)r * d.H + k]);
+    } else {
+      for (int r = 0; r < d.Vt; ++r) pack_row(img, m->W_s, r, 0, Ws + (size_t)r * d.H, 0, d.H);
+    }
     const float* bs = host_weights[wi++];
     const size_t bo = off_of(m->b_s);
     for (int r = 0; r < d.Vt; ++r) img.putf(bo, r, bs[r]);

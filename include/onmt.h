@@ -70,8 +70,10 @@ enum { ONMT_ATTN_GENERAL = 0, ONMT_ATTN_DOT = 1, ONMT_ATTN_CONCAT = 2 };
 /* Beam search settings (Section 2 item (d); Section 4.2 length and attention coverage normalisation,
  * GNMT forms lp(n) = ((5 + n) / 6)^alpha and cp = beta * sum over the real source positions i of
  * log(min(c_i, 1)), c_i = attention on position i summed over the hypothesis's steps). max_len counts
- * generated tokens including EOS. beta >= 0 (0 = no coverage penalty). The host reads an "all sentences
- * finished" counter every check_every steps (<= 0: every step when max_len <= 32, else every 8). */
+ * generated tokens including EOS. beta >= 0 (0 = no coverage penalty). Every check_every steps (<= 0:
+ * every step when max_len <= 32, else every 8) the "all sentences finished" counter is copied to the host
+ * without waiting; the host then waits for the previous such copy and stops when it shows every sentence
+ * finished, so a finished batch runs at most one check period of extra steps (which change no output). */
 typedef struct {
   int beam;
   int max_len;

@@ -205,6 +205,9 @@ struct onmt_model {
   double prof_ms = 0.0;
   std::vector<hipEvent_t> ev;   // reusable start/stop pairs
   size_t ev_used = 0;
+  // finish checks of the beam search: two pinned host words the done count is copied into, one event each
+  int32_t* done_host = nullptr;
+  hipEvent_t done_ev[2] = {nullptr, nullptr};
 };
 
 namespace {
@@ -472,6 +475,9 @@ int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, 
 int onmt_model_destroy(onmt_model* m) {
   if (!m) return fail(ONMT_EINVAL, "model is NULL");
   for (auto e : m->ev) hipEventDestroy(e);
+  for (auto e : m->done_ev)
+    if (e) hipEventDestroy(e);
+  if (m->done_host) hipHostFree(m->done_host);
   delete m;
   return ONMT_OK;
 }
@@ -1232,7 +1238,11 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   HIP_TRY(beam_init(bp, m->cfg.bos_id, st));
   if (coverage) HIP_TRY(fill_f32(w.cov[0], (size_t)B * K * S, 0.f, st));
   const int every = prm->check_every > 0 ? prm->check_every : (T <= 32 ? 1 : 8);
-  int cur = 0;
+  if (!m->done_host) {
+    HIP_TRY(hipHostMalloc((void**)&m->done_host, 2 * sizeof(int32_t), hipHostMallocDefault));
+    for (auto& e : m->done_ev) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  }
+  int cur = 0, nchk = 0;
   for (int t = 1; t <= T; ++t) {
     // coverage of the rows' hypotheses: the parents' coverage (previous layout) plus this step's weights
     const Coverage cv{w.cov[cur], w.cov[cur ^ 1], bp.parent, prm->beta, w.cp};
@@ -1243,10 +1253,16 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
     HIP_TRY(beam_step(bp, gp, t, st));
     cur ^= 1;
     if (t < T && t % every == 0) {
-      int32_t done = 0;
-      HIP_TRY(hipMemcpyAsync(&done, bp.done_count, sizeof(int32_t), hipMemcpyDeviceToHost, st));
-      HIP_TRY(hipStreamSynchronize(st));
-      if (done >= B) break;
+      // this step's done count goes to the host asynchronously and the host waits only for the previous
+      // check's, so a check period of steps stays queued on the device; a finished batch runs at most one
+      // extra period, in which the beam step leaves every finished sentence unchanged
+      const int slot = nchk & 1;
+      HIP_TRY(hipMemcpyAsync(m->done_host + slot, bp.done_count, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+      HIP_TRY(hipEventRecord(m->done_ev[slot], st));
+      if (nchk++ > 0) {
+        HIP_TRY(hipEventSynchronize(m->done_ev[slot ^ 1]));
+        if (m->done_host[slot ^ 1] >= B) break;
+      }
     }
   }
   HIP_TRY(backtrack(bp, out_tok, out_len, out_raw, out_norm, out_tok_logp, out_align, st));

@@ -582,7 +582,16 @@ using TileMid16 = Tile<__bf16, 1, 2, 2, 2, 2, 32>;
 // halves the LDS stage buffers so that four workgroups fit on a CU.
 using TileGen32 = Tile<float, 2, 2, 1, 2, 4, 16>;
 using TileGen16 = Tile<__bf16, 2, 2, 1, 2, 4, 32>;
-static_assert(TileGen32::BN == TileGen16::BN, "both generator tiles give the same column tiles");
+// 32 x 128 fp32 generator tiles (two waves) where the last 64-row tile would be at most half full and the
+// rows are few: at 160 rows 91 us instead of 108 us (64-row tiles compute 192 rows), at 96 rows 64 instead
+// of 78 us; at multiples of 64 rows, and at 480, the 64-row tile is faster. Same partials, bitwise.
+using TileGen32h = Tile<float, 1, 2, 1, 2, 4, 16>;
+static inline bool gen_rows32(int M) {
+  const int r = M % 64;
+  return M <= 256 && r > 0 && r <= 32;
+}
+static_assert(TileGen32::BN == TileGen16::BN && TileGen32h::BN == TileGen32::BN,
+              "all generator tiles give the same column tiles");
 // Pre-split bf16 generator: 64 x 256 tiles (8 waves of 32 x 64; the activations are re-read by half as
 // many column tiles as with 64 x 128) and two LDS stages of 24 KB; at 320 and 512 rows this measured
 // 10-15% faster than 64 x 128 tiles with three 16 KB stages, and three or four stages of 64 x 256 slower.
@@ -865,7 +874,8 @@ hipError_t split_rows(const float* src, int ld_src, int rows, int cols, uint16_t
 }
 
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
-  return bf16 ? launch_gen<__bf16, TileGen16>(a, b, p, st) : launch_gen<float, TileGen32>(a, b, p, st);
+  if (bf16) return launch_gen<__bf16, TileGen16>(a, b, p, st);
+  return gen_rows32(a.M) ? launch_gen<float, TileGen32h>(a, b, p, st) : launch_gen<float, TileGen32>(a, b, p, st);
 }
 
 hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, const GenParams& p, hipStream_t st) {

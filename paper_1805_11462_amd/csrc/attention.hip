@@ -252,12 +252,14 @@ __global__ __launch_bounds__(kCtxThreads) void k_attn_context(const float* __res
   }
 #pragma unroll
   for (int k = 0; k < KMAX; ++k) {
+    if (k < K) {                                      // uniform: no shuffles for the rows past K
 #pragma unroll
-    for (int o = PL / 2; o > 0; o >>= 1) {
-      acc[k].x += __shfl_xor(acc[k].x, o, kWave);
-      acc[k].y += __shfl_xor(acc[k].y, o, kWave);
-      acc[k].z += __shfl_xor(acc[k].z, o, kWave);
-      acc[k].w += __shfl_xor(acc[k].w, o, kWave);
+      for (int o = PL / 2; o > 0; o >>= 1) {
+        acc[k].x += __shfl_xor(acc[k].x, o, kWave);
+        acc[k].y += __shfl_xor(acc[k].y, o, kWave);
+        acc[k].z += __shfl_xor(acc[k].z, o, kWave);
+        acc[k].w += __shfl_xor(acc[k].w, o, kWave);
+      }
     }
   }
   if (pl == 0 && col_ok) {

@@ -366,8 +366,20 @@ __global__ __launch_bounds__(C::NT) void k_gemm_store(AOp a, BOp b, StoreParams 
   }
 }
 
+// Main loop with LDS-destination loads for bf16 products whose A segments are all pre-split planes (defined
+// with the other LDS-destination kernel below); same LDS result as gemm_tile.
+template <class C, int NSEG>
+__device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0, char* smem);
+// LDS bytes of a tile with the LDS-destination main loop (kLstmStages stages, or the output tile).
+constexpr int kLstmStages = 2;
+template <class C>
+constexpr int dma_lds() {
+  constexpr int stg = (2 * C::BM + C::BN) * C::BK * 2;
+  return kLstmStages * stg > C::CT ? kLstmStages * stg : C::CT;
+}
+
 // One output tile of an LSTM GEMM (block bid of nblocks) with the gate/cell epilogue.
-template <class T, class C, int NSEG>
+template <class T, class C, int NSEG, bool DMA = false>
 __device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p, int nm, int nblocks, int bid,
                                  char* smem) {
   const int L = xcd_remap(bid, nblocks);
@@ -389,7 +401,10 @@ __device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p
     for (int gt = 0; gt < 4; ++gt)
       gxv[i][gt] = ok ? p.gx[(size_t)grow * p.ld_gx + p.gx_col0 + n0 + cbase + gt * kUnitGroup] : 0.f;
   }
-  gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
+  if constexpr (DMA)
+    gemm_tile_dma<C, NSEG>(a, b, m0, n0, smem);
+  else
+    gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
   const float* Ct = (const float*)smem;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
@@ -431,10 +446,10 @@ __device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p
   }
 }
 
-template <class T, class C, int NSEG>
+template <class T, class C, int NSEG, bool DMA = false>
 __global__ __launch_bounds__(C::NT) void k_gemm_lstm(AOp a, BOp b, LstmParams p, int nm, int nblocks) {
-  __shared__ __attribute__((aligned(16))) char smem[C::LDS];
-  lstm_tile<T, C, NSEG>(a, b, p, nm, nblocks, blockIdx.x, smem);
+  __shared__ __attribute__((aligned(16))) char smem[DMA ? dma_lds<C>() : C::LDS];
+  lstm_tile<T, C, NSEG, DMA>(a, b, p, nm, nblocks, blockIdx.x, smem);
 }
 
 // Two independent LSTM GEMMs in one launch (the encoder's two directions at one step, or two stacked
@@ -742,6 +757,147 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
 }
 
 
+// Vector-memory "no wait", LDS wait until nothing is outstanding (for LDS stores before a bare barrier).
+constexpr int kWaitLgkm0 = 15 | (7 << 4) | (0 << 8) | (3 << 14);
+
+// gemm_tile for bf16 products whose A segments (one or two) are all pre-split hi / lo planes, with the
+// operands moved straight into LDS: a stage of A hi rows, A lo rows and B rows is sliced into 1 KB pieces
+// (RPS tile rows each; lane l writes row l / (ROWB / 16), 16-byte slot l % (ROWB / 16)), kLstmStages stages
+// in flight, waits and bare barriers as in k_gemm_gen_lds. A rows come through the segment's row map
+// (beam parents) and rows past M re-read row M - 1. The planes' columns past a segment's width are not
+// assumed to be zero: on a segment's last stage they are cleared in LDS before the products. Products,
+// their order and the output tile (WK partial planes) are those of gemm_tile, so the results are equal.
+template <class C, int NSEG>
+__device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0, char* smem) {
+  static_assert(C::kBf16 && C::KW == C::KSUB && NSEG >= 1 && NSEG <= 2, "one MFMA K step per wave and stage");
+  constexpr int NW = C::NT / 64, ROWB = C::BK * 2, RPS = 1024 / ROWB, LPR = ROWB / 16;
+  constexpr int SA = C::BM / RPS, SB = C::BN / RPS, SPW = (2 * SA + SB) / NW;
+  constexpr int STG = (2 * C::BM + C::BN) * ROWB, NSTG = kLstmStages;
+  static_assert(1024 % ROWB == 0 && C::BM % RPS == 0 && C::BN % RPS == 0 && (2 * SA + SB) % NW == 0 &&
+                    SPW * (NSTG - 2) < 64 && dma_lds<C>() >= NSTG * STG,
+                "slice layout");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i16 = lane & 15, g = lane >> 4;
+  const int wk = wave % C::WK, wn = (wave / C::WK) % C::WN, wm = wave / (C::WK * C::WN);
+  const int srow = lane / LPR, sslot = lane % LPR;
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(b.W, (uint32_t)b.Np * b.Kp * 2);
+  // per segment (constant indices only): plane descriptors, stage count, width
+  __amdgpu_buffer_rsrc_t rh[2], rl[2];
+  int nst[2] = {0, 0}, wd[2] = {0, 0};
+#pragma unroll
+  for (int s = 0; s < NSEG; ++s) {
+    const uint32_t bytes = (uint32_t)a.seg[s].rows * a.seg[s].ld * 2;
+    rh[s] = make_rsrc(a.seg[s].base, bytes);
+    rl[s] = make_rsrc(a.seg[s].lo, bytes);
+    nst[s] = a.seg[s].kpad / C::BK;
+    wd[s] = a.seg[s].width;
+  }
+  const int total = nst[0] + nst[1];
+  const int kb1 = NSEG > 1 ? a.seg[0].kpad : 0;        // K offset of segment 1 in the weight rows
+  int sl_kind[SPW], sl_lds[SPW];
+  uint32_t aoff[2][SPW], boff[SPW];
+#pragma unroll
+  for (int i = 0; i < SPW; ++i) {
+    const int q = wave + NW * i;
+    const int kind = q < SA ? 0 : (q < 2 * SA ? 1 : 2);
+    const int trow = (kind == 0 ? q : (kind == 1 ? q - SA : q - 2 * SA)) * RPS + srow;
+    const int chunk = sslot ^ C::swz(trow);
+    sl_kind[i] = kind;
+    sl_lds[i] = ((kind == 2 ? 2 * C::BM : kind * C::BM) + trow - srow) * ROWB;
+    boff[i] = ((uint32_t)min(n0 + trow, b.Np - 1) * b.Kp + chunk * C::CH) * 2;
+    const int r = min(m0 + trow, a.M - 1);
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      aoff[s][i] = 0;
+      if (s < NSEG) {
+        const int rr = a.seg[s].idx ? a.seg[s].idx[r] : r;
+        aoff[s][i] = ((uint32_t)rr * a.seg[s].ld + chunk * C::CH) * 2;
+      }
+    }
+  }
+  f32x4 acc[C::TM][C::TN];
+#pragma unroll
+  for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+    for (int y = 0; y < C::TN; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // stages past the last re-load the last one into a buffer that is never multiplied
+  auto issue = [&](int G) {
+    const int gg = G < total ? G : total - 1;
+    const int s = gg >= nst[0] ? 1 : 0;
+    const int ls = gg - (s ? nst[0] : 0);
+    char* sb = smem + (G % NSTG) * STG;
+    const uint32_t ka = (uint32_t)ls * ROWB, kb = (uint32_t)((s ? kb1 : 0) + ls * C::BK) * 2;
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      if (sl_kind[i] == 2)
+        dma16(rw, sb + sl_lds[i], boff[i] + kb);
+      else if (sl_kind[i] == 0)
+        dma16(s ? rh[1] : rh[0], sb + sl_lds[i], (s ? aoff[1][i] : aoff[0][i]) + ka);
+      else
+        dma16(s ? rl[1] : rl[0], sb + sl_lds[i], (s ? aoff[1][i] : aoff[0][i]) + ka);
+    }
+  };
+#pragma unroll
+  for (int G = 0; G < NSTG - 1; ++G) issue(G);
+  const int col = ((wk * C::KW / C::CH + g) ^ C::swz(i16)) * C::CH;
+  for (int G = 0; G < total; ++G) {
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(SPW * (NSTG - 2)));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    char* base = smem + (G % NSTG) * STG;
+    {
+      const int s = G >= nst[0] ? 1 : 0;
+      const int ls = G - (s ? nst[0] : 0);
+      const int w = s ? wd[1] : wd[0];
+      if ((ls + 1) * C::BK > w) {                      // the segment's last stage reaches past its width
+        for (int e = tid; e < 2 * C::BM * C::CPR; e += C::NT) {
+          const int row = e / C::CPR, c = e % C::CPR;   // row of the hi then the lo plane, logical chunk
+          if (ls * C::BK + c * C::CH >= w)
+            *(uint4*)(base + row * ROWB + ((c ^ C::swz(row % C::BM)) * 16)) = zero4();
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+      }
+    }
+    issue(G + NSTG - 1);                                // refills the buffer multiplied at G - 1
+    const __bf16* Ah = (const __bf16*)base + (wm * C::TM * 16 + i16) * C::ROW;
+    const __bf16* Al = Ah + C::BM * C::ROW;
+    const __bf16* Bb = (const __bf16*)base + (2 * C::BM + wn * C::TN * 16 + i16) * C::ROW;
+    bf16x8 av[C::TM], bv[C::TN];
+#pragma unroll
+    for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + x * 16 * C::ROW + col);
+#pragma unroll
+    for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + col);
+#pragma unroll
+    for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+      for (int y = 0; y < C::TN; ++y)
+        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+#pragma unroll
+    for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Al + x * 16 * C::ROW + col);
+#pragma unroll
+    for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+      for (int y = 0; y < C::TN; ++y)
+        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+  }
+  // every load (including the re-loads past the end) has landed before the output tile reuses the buffers
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  __syncthreads();
+  float* Ct = (float*)smem + wk * C::BM * C::CROW;
+#pragma unroll
+  for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+    for (int y = 0; y < C::TN; ++y)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        Ct[(wm * C::TM * 16 + x * 16 + 4 * g + v) * C::CROW + wn * C::TN * 16 + y * 16 + i16] = acc[x][y][v];
+  __syncthreads();
+}
+
 template <class C>
 static inline void grid_of(const AOp& a, const BOp& b, int& nm, int& nblocks) {
   nm = (a.M + C::BM - 1) / C::BM;
@@ -775,12 +931,29 @@ static hipError_t launch_store(const AOp& a, const BOp& b, const StoreParams& p,
   return hipGetLastError();
 }
 
+// The LDS-destination main loop applies to bf16 products whose one or two A segments are all pre-split.
+static inline bool all_pre_split(const AOp& a) {
+  if (a.nseg < 1 || a.nseg > 2) return false;
+  for (int s = 0; s < a.nseg; ++s)
+    if (!a.seg[s].bf16 || !a.seg[s].lo || a.seg[s].ld < a.seg[s].kpad) return false;
+  return true;
+}
+
 template <class T, class C>
 static hipError_t launch_lstm(const AOp& a, const BOp& b, const LstmParams& p, hipStream_t st) {
   int nm, nb;
   grid_of<C>(a, b, nm, nb);
   if (!operands_fit<T>(a, b) || a.nseg < 1 || a.nseg > 3) return hipErrorInvalidValue;
   if (nb == 0) return hipSuccess;
+  if constexpr (C::kBf16 && C::KW == C::KSUB && C::CPR == 8) {
+    if (all_pre_split(a)) {
+      if (a.nseg == 1)
+        hipLaunchKernelGGL((k_gemm_lstm<T, C, 1, true>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+      else
+        hipLaunchKernelGGL((k_gemm_lstm<T, C, 2, true>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+      return hipGetLastError();
+    }
+  }
   if (a.nseg == 1) hipLaunchKernelGGL((k_gemm_lstm<T, C, 1>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
   else if (a.nseg == 2) hipLaunchKernelGGL((k_gemm_lstm<T, C, 2>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
   else hipLaunchKernelGGL((k_gemm_lstm<T, C, 3>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);

@@ -4,7 +4,9 @@ that leave a ragged last generator tile, three stacked layers, bidirectional enc
 per-direction widths, the concat attention type at such sizes, and a bf16 model whose hidden size is not
 a multiple of 8 (its activations are split on load instead of read as pre-split planes). Each shape:
 three decoder steps against the oracle (full log-distribution, attention, state) and a beam search whose
-every sentence is checked by teacher-forced rescoring and the replay of its decisions.
+every sentence is checked by teacher-forced rescoring and the replay of its decisions. A bf16 model with
+hidden 104 at 256 hypothesis rows runs the decoder layers' LDS-destination main loop (rows gathered by
+beam parent, a segment width that is not a multiple of the 64-wide K stage).
 """
 
 import numpy as np
@@ -87,3 +89,37 @@ def test_beam_search(shape):
     torch.cuda.synchronize()
     mism = check_search(s, buf, range(B), w.beam, w.max_len, 0.6)
     print(f"  free-run token mismatches (replay-verified): {mism}", flush=True)
+
+
+def test_bf16_lds_path_256_rows():
+    w = with_workload(TINY, name="bf16_h104_256rows", batch=64, beam=4, hidden=104, emb=48, tgt_vocab=1500,
+                      wdtype="bf16")
+    s = Setup(w, peaked=True)
+    B, S = s.src.shape
+    K = w.beam
+    N = B * K
+    assert N >= 256                                   # the decoder GEMMs use the 32-row bf16 tiles
+    _case("bf16_lds_path", rows=N)
+    ws = s.tr.encode(s.src_d, s.lens_d)
+    st = s.tr.decode_init(ws, B, S, K)
+    enc = O.encode(s.model, s.src, s.lens)
+    ost = O.init_state(s.model, enc, K)
+    rows = np.repeat(np.arange(B), K)
+    rng = np.random.default_rng(5)
+    tok = np.full(N, W.BOS_ID, np.int32)
+    parent = None
+    for step in range(3):
+        par_d = torch.from_numpy(parent).cuda() if parent is not None else None
+        st, logp, _, _, _ = s.tr.decode_step(ws, B, S, K, st, torch.from_numpy(tok).cuda(), par_d, mode=0)
+        torch.cuda.synchronize()
+        o_new, o_logp, _ = O.decode_step(s.model, enc, ost if parent is None else ost.take(parent), tok, rows)
+        err = np.abs(logp.cpu().numpy() - o_logp).max()
+        print(f"  step {step}: max |logp - oracle| = {err:.3g}", flush=True)
+        assert err <= s.tau
+        h, c, feed = s.tr.state_views(st, N)
+        for l in range(w.dec_layers):
+            np.testing.assert_allclose(h[l].cpu().numpy(), o_new.h[l], atol=1e-2, rtol=0)
+        parent = (rows * K + rng.integers(0, K, size=N)).astype(np.int32)
+        tok = rng.integers(0, w.tgt_vocab, size=N).astype(np.int32)
+        ost = o_new
+

@@ -4,6 +4,8 @@
 // row-mapped segments (embedding rows by token id, state rows by beam parent, plain activations)
 // and W is a packed weight matrix. Tiles are staged through two LDS buffers; global loads run two
 // K stages ahead in registers so that a stage's loads have a full stage of MFMA work to hide behind.
+// Where the bf16 operands are pre-split hi / lo planes (the bf16 generator and decoder layers), buffer
+// loads with an LDS destination move them straight into the stage buffers instead.
 // Products use 16x16 MFMA tiles: v_mfma_f32_16x16x4_f32 for fp32 operands and
 // v_mfma_f32_16x16x32_bf16 for bf16 operands, always accumulating in fp32. Waves may split K
 // inside the workgroup (WK > 1); their partial tiles are summed in LDS before the epilogue.

@@ -110,7 +110,7 @@ struct GenParams {
 };
 
 // kShapeMid: 32 x 64 tiles with two waves splitting K, for bf16 LSTM GEMMs of a few hundred rows (fp32 maps
-// it to the thin tile).
+// it to the thin tile); when every A segment is a pre-split plane pair the operands go straight into LDS.
 enum GemmShape { kShapeWide = 0, kShapeSplitK = 1, kShapeSplitKThin = 2, kShapeMid = 3 };
 
 hipError_t gemm_store(int bf16, int shape, const AOp& a, const BOp& b, const StoreParams& p, hipStream_t st);

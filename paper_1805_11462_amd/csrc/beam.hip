@@ -22,26 +22,32 @@ constexpr int kMaxTilesPerLane = 16;          // tiles per row <= 64 * 16 (vocab
 constexpr int kSurvivorCap = 256;
 constexpr int kQualCap = 256;                 // qualifying tiles listed per row
 
-// Row partials start at pmax/psum + row * ntiles and pval/pid + row * ntiles * K. Lane 0 writes
+// Row partials start at pmax/psum + row * ntiles (loaded by row_tiles_load) and pval/pid + row * ntiles * K. Lane 0 writes
 // out_val[k] = logit - lse (K entries), out_id[k] and *out_lse. sv/si/cnt/qt: this wave's LDS scratch
 // (kSurvivorCap survivors, kQualCap qualifying tile ids).
 // pfmax (optional, filters active): per-tile largest allowed logit, which then replaces the tile maximum
 // in the bound (the lists hold allowed entries only; the logsumexp still covers every column).
-__device__ __forceinline__ void row_merge_wave(const float* __restrict__ pmax, const float* __restrict__ psum,
+// The row's tile maxima and sums (lane l holds tiles l + 64 j), every load issued before the first use.
+__device__ __forceinline__ void row_tiles_load(const float* __restrict__ pmax, const float* __restrict__ psum,
+                                               int ntiles, float (&tm)[kMaxTilesPerLane],
+                                               float (&tq)[kMaxTilesPerLane]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < kMaxTilesPerLane; ++j) {
+    const int t = lane + j * kWave;
+    tm[j] = t < ntiles ? pmax[t] : -__builtin_inff();
+    tq[j] = t < ntiles ? psum[t] : 0.f;
+  }
+}
+
+// tm / tq: the row's tile maxima and sums from row_tiles_load (tm is overwritten).
+__device__ __forceinline__ void row_merge_wave(float (&tm)[kMaxTilesPerLane], const float (&tq)[kMaxTilesPerLane],
                                                const float* __restrict__ pval, const int32_t* __restrict__ pid,
                                                const float* __restrict__ pfmax, int ntiles, int K, float* sv,
                                                int* si, int* cnt, int* qt, float* out_val, int32_t* out_id,
                                                float* out_lse) {
   const int lane = threadIdx.x & 63;
   const float ninf = -__builtin_inff();
-  // tile maxima and sums, every load issued before the first use
-  float tm[kMaxTilesPerLane], tq[kMaxTilesPerLane];
-#pragma unroll
-  for (int j = 0; j < kMaxTilesPerLane; ++j) {
-    const int t = lane + j * kWave;
-    tm[j] = t < ntiles ? pmax[t] : ninf;
-    tq[j] = t < ntiles ? psum[t] : 0.f;
-  }
   float mx = ninf;
 #pragma unroll
   for (int j = 0; j < kMaxTilesPerLane; ++j) mx = fmaxf(mx, tm[j]);
@@ -172,8 +178,9 @@ __global__ __launch_bounds__(kMergeWaves * kWave) void k_lse_topk(const float* _
   const int row = blockIdx.x * kMergeWaves + w;
   if (row >= M) return;
   const size_t base = (size_t)row * ntiles;
-  row_merge_wave(pmax + base, psum + base, pval + base * K, pid + base * K, nullptr, ntiles, K, sv[w], si[w], &cnt[w],
-                 qt[w],
+  float tm[kMaxTilesPerLane], tq[kMaxTilesPerLane];
+  row_tiles_load(pmax + base, psum + base, ntiles, tm, tq);
+  row_merge_wave(tm, tq, pval + base * K, pid + base * K, nullptr, ntiles, K, sv[w], si[w], &cnt[w], qt[w],
                  out_val + (size_t)row * K, out_id ? out_id + (size_t)row * K : nullptr,
                  out_lse ? out_lse + row : nullptr);
 }
@@ -315,12 +322,18 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
   const int b = blockIdx.x;
   const int w = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
-  if (p.done[b]) return;
   const int K = p.K;
   const int r0 = b * K;
   const double ninf = -__builtin_inf();
-  // sentence state, fetched up front so that the tail below does not wait on memory
+  // the finished flag, the slot's score and its row's tile partials are loaded together (one memory round
+  // trip instead of three dependent ones; a finished sentence's loads are simply not used)
+  const int done = p.done[b];
   const double my_score = p.score[r0 + w];
+  const size_t base = (size_t)(r0 + w) * gp.ntiles;
+  float tm[kMaxTilesPerLane], tq[kMaxTilesPerLane];
+  row_tiles_load(gp.pmax + base, gp.psum + base, gp.ntiles, tm, tq);
+  if (done) return;
+  // sentence state, fetched up front so that the tail below does not wait on memory
   double best_norm0 = ninf;
   int best_t0 = 0;
   if (w == 0) {
@@ -328,8 +341,7 @@ __global__ __launch_bounds__(kMaxBeam * kWave) void k_beam_step(BeamParams p, Ge
     best_t0 = p.best_t[b];
   }
   if (my_score > ninf) {
-    const size_t base = (size_t)(r0 + w) * gp.ntiles;
-    row_merge_wave(gp.pmax + base, gp.psum + base, gp.pval + base * K, gp.pid + base * K,
+    row_merge_wave(tm, tq, gp.pval + base * K, gp.pid + base * K,
                    gp.pfmax ? gp.pfmax + base : nullptr, gp.ntiles, K, sv[w], si[w], &cnt[w], qt[w], tkv[w], tki[w],
                    nullptr);
   }

@@ -1241,6 +1241,10 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   if (!m->done_host) {
     HIP_TRY(hipHostMalloc((void**)&m->done_host, 2 * sizeof(int32_t), hipHostMallocDefault));
     for (auto& e : m->done_ev) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  } else {
+    // a search that returned early on an error may have left a count copy queued (possibly on another
+    // stream): it must land before this search's copies reuse the two slots
+    for (auto& e : m->done_ev) HIP_TRY(hipEventSynchronize(e));
   }
   int cur = 0, nchk = 0;
   for (int t = 1; t <= T; ++t) {

@@ -114,8 +114,11 @@ __device__ inline uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 }
 
 // Main loop: leaves the (WK-way partial) fp32 output tile in LDS at smem, layout [WK][BM][CROW].
-template <class T, class C, int NSEG>
-__device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, char* smem) {
+// CBIAS (single-K-group tiles): cb[y] is added to the lane's column of output block y as the tile is
+// written (the generator's bias, loaded before the main loop by gen_col_bias).
+template <class T, class C, int NSEG, bool CBIAS = false>
+__device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, char* smem, const float* cb = nullptr) {
+  static_assert(!CBIAS || C::WK == 1, "a bias is added to whole sums only");
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -324,8 +327,11 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
 #pragma unroll
     for (int y = 0; y < C::TN; ++y)
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        Ct[(wm * C::TM * 16 + x * 16 + 4 * g + v) * C::CROW + wn * C::TN * 16 + y * 16 + i16] = acc[x][y][v];
+      for (int v = 0; v < 4; ++v) {
+        float o = acc[x][y][v];
+        if constexpr (CBIAS) o += cb[y];
+        Ct[(wm * C::TM * 16 + x * 16 + 4 * g + v) * C::CROW + wn * C::TN * 16 + y * 16 + i16] = o;
+      }
   __syncthreads();
 }
 
@@ -472,7 +478,9 @@ __global__ __launch_bounds__(C::NT) void k_gemm_lstm2(LstmPair g) {
 // each. Row max and sum of exponentials are combined with lane shuffles; the tile's top-K is taken with
 // K rounds of a 4-lane argmax (larger logit first, smaller id on ties), each thread skipping the columns
 // it already gave away.
-template <class C>
+// BIASED: the output tile already holds product + bias (added as the tile was written, the same single
+// fp32 addition), so the epilogue issues no bias loads of its own.
+template <class C, bool BIASED = false>
 __device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M, int m0, int n0, int nt, int tid) {
   static_assert(C::NT / C::BM == 4 && C::BN == 128, "generator tile is 64 x 128 with 256 threads");
   const float* Ct = (const float*)smem;
@@ -486,7 +494,10 @@ __device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M,
 #pragma unroll
   for (int j = 0; j < 32; ++j) {
     const int gc = n0 + 4 * j + part;
-    z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) + p.bias[gc] : ninf;
+    if constexpr (BIASED)
+      z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) : ninf;
+    else
+      z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) + p.bias[gc] : ninf;
     mx = fmaxf(mx, z[j]);
   }
   if (p.want && row < M) {
@@ -566,14 +577,28 @@ __device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M,
 }
 
 
+// The generator bias of the columns this lane writes in the output tile (column wn * TN * 16 + 16 y + i16
+// of the tile at n0, for y < TN; 0 past V), loaded before the main loop so that its latency hides there.
+template <class C>
+__device__ inline void gen_col_bias(const GenParams& p, int n0, int wn, int i16, float (&cb)[C::TN]) {
+#pragma unroll
+  for (int y = 0; y < C::TN; ++y) {
+    const int gc = n0 + wn * C::TN * 16 + y * 16 + i16;
+    cb[y] = gc < p.V ? p.bias[gc] : 0.f;
+  }
+}
+
 template <class T, class C, int NSEG>
 __global__ __launch_bounds__(C::NT) void k_gemm_gen(AOp a, BOp b, GenParams p, int nm, int nblocks) {
   __shared__ __attribute__((aligned(16))) char smem[C::LDS];
   const int L = xcd_remap(blockIdx.x, nblocks);
   const int mt = L % nm, nt = L / nm;
   const int m0 = mt * C::BM, n0 = nt * C::BN;
-  gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
-  gen_epilogue<C>(smem, p, a.M, m0, n0, nt, threadIdx.x);
+  const int wave = threadIdx.x >> 6;
+  float cb[C::TN];
+  gen_col_bias<C>(p, n0, (wave / C::WK) % C::WN, threadIdx.x & 15, cb);
+  gemm_tile<T, C, NSEG, true>(a, b, m0, n0, smem, cb);
+  gen_epilogue<C, true>(smem, p, a.M, m0, n0, nt, threadIdx.x);
 }
 
 // ---------------------------------------------------------------- launchers
@@ -655,6 +680,8 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i16 = lane & 15, g = lane >> 4;
   const int wn = wave % C::WN, wm = wave / C::WN;
+  float cb[C::TN];
+  gen_col_bias<C>(p, n0, wn, i16, cb);
 
   // slice q of a stage: A hi rows 16 q.. (q < SA), A lo rows (q < 2 SA), then B rows; wave w moves slices
   // w, w + NW, ...; lane's place in a slice: tile row lane / 4, 16-byte slot lane % 4 (chunk slot ^ swz)
@@ -751,11 +778,11 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
       for (int y = 0; y < C::TN; ++y)
 #pragma unroll
         for (int v = 0; v < 4; ++v)
-          Ct[(wm * C::TM * 16 + x * 16 + 4 * g + v) * CE::CROW + c0 + y * 16 + i16] = acc[x][y][v];
+          Ct[(wm * C::TM * 16 + x * 16 + 4 * g + v) * CE::CROW + c0 + y * 16 + i16] = acc[x][y][v] + cb[y];
   }
   __syncthreads();
   const int sub = tid / CE::NT, n0s = n0 + 128 * sub;
-  if (n0s < b.Np) gen_epilogue<CE>(smem + sub * CE::CT, p, a.M, m0, n0s, n0s / 128, tid % CE::NT);
+  if (n0s < b.Np) gen_epilogue<CE, true>(smem + sub * CE::CT, p, a.M, m0, n0s, n0s / 128, tid % CE::NT);
 }
 
 

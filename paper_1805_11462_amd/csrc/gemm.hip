@@ -474,10 +474,22 @@ __global__ __launch_bounds__(C::NT) void k_gemm_lstm2(LstmPair g) {
   }
 }
 
+// Exchange with lane l ^ X (X = 1 or 2) inside each group of four lanes: a DPP quad permutation, so the
+// four threads of an epilogue row trade values without a round trip through LDS.
+template <int X>
+__device__ inline int quad_xor(int v) {
+  static_assert(X == 1 || X == 2, "quad lanes");
+  return __builtin_amdgcn_mov_dpp(v, X == 1 ? 0xB1 : 0x4E, 0xF, 0xF, false);   // quad_perm [1,0,3,2] / [2,3,0,1]
+}
+template <int X>
+__device__ inline float quad_xor(float v) {
+  return __builtin_bit_cast(float, quad_xor<X>(__builtin_bit_cast(int, v)));
+}
+
 // Generator epilogue over the 64 x 128 output tile in LDS: 4 threads per row, 32 interleaved columns
-// each. Row max and sum of exponentials are combined with lane shuffles; the tile's top-K is taken with
-// K rounds of a 4-lane argmax (larger logit first, smaller id on ties), each thread skipping the columns
-// it already gave away.
+// each. Row max and sum of exponentials are combined across the row's four lanes (quad_xor); the tile's
+// top-K is taken with K rounds of a 4-lane argmax (larger logit first, smaller id on ties), each thread
+// skipping the columns it already gave away.
 // BIASED: the output tile already holds product + bias (added as the tile was written, the same single
 // fp32 addition), so the epilogue issues no bias loads of its own.
 template <class C, bool BIASED = false>
@@ -515,13 +527,13 @@ __device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M,
       if (gc < p.V) p.logits[(size_t)row * p.ld_logits + gc] = z[j];
     }
   }
-  float rmx = fmaxf(mx, __shfl_xor(mx, 1, kWave));
-  rmx = fmaxf(rmx, __shfl_xor(rmx, 2, kWave));
+  float rmx = fmaxf(mx, quad_xor<1>(mx));
+  rmx = fmaxf(rmx, quad_xor<2>(rmx));
   float sm = 0.f;
 #pragma unroll
   for (int j = 0; j < 32; ++j) sm += __expf(z[j] - rmx);     // exp(-inf) = 0 for columns past V
-  sm += __shfl_xor(sm, 1, kWave);
-  sm += __shfl_xor(sm, 2, kWave);
+  sm += quad_xor<1>(sm);
+  sm += quad_xor<2>(sm);
   const size_t o = (size_t)row * p.ntiles + nt;
   if (part == 0 && row < M) {
     p.pmax[o] = rmx;
@@ -558,10 +570,17 @@ __device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M,
     }
     int bid = bv > ninf ? n0 + 4 * bj + part : 0x7fffffff;
     const int mine = bid;
-#pragma unroll
-    for (int sft = 1; sft < 4; sft <<= 1) {
-      const float ov = __shfl_xor(bv, sft, kWave);
-      const int oi = __shfl_xor(bid, sft, kWave);
+    {
+      const float ov = quad_xor<1>(bv);
+      const int oi = quad_xor<1>(bid);
+      if (before(ov, oi, bv, bid)) {
+        bv = ov;
+        bid = oi;
+      }
+    }
+    {
+      const float ov = quad_xor<2>(bv);
+      const int oi = quad_xor<2>(bid);
       if (before(ov, oi, bv, bid)) {
         bv = ov;
         bid = oi;

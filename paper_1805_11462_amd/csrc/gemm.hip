@@ -557,15 +557,28 @@ __device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M,
     const int c = p.unk_id - n0;
     if (c >= 0 && c < C::BN && (c & 3) == part) taken |= 1u << (c >> 2);
   }
+  // with no filter every column is free in the first round, whose best is then the thread's maximum at
+  // its first (smallest-id) position
+  const bool fast0 = !p.banned_bits && !p.unk_cnt;
   for (int k = 0; k < p.K; ++k) {
     float bv = ninf;
     int bj = 0;
+    if (k == 0 && fast0) {
 #pragma unroll
-    for (int j = 0; j < 32; ++j) {
-      const bool free = !((taken >> j) & 1u);
-      if (free && z[j] > bv) {                    // strict: the earlier (smaller id) column wins ties
-        bv = z[j];
-        bj = j;
+      for (int j = 31; j >= 0; --j) {
+        if (z[j] == mx) {
+          bv = z[j];
+          bj = j;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 32; ++j) {
+        const bool free = !((taken >> j) & 1u);
+        if (free && z[j] > bv) {                  // strict: the earlier (smaller id) column wins ties
+          bv = z[j];
+          bj = j;
+        }
       }
     }
     int bid = bv > ninf ? n0 + 4 * bj + part : 0x7fffffff;

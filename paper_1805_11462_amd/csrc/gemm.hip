@@ -503,15 +503,26 @@ __device__ inline void gen_epilogue(const char* smem, const GenParams& p, int M,
   const float ninf = -__builtin_inff();
   float z[32];
   float mx = ninf;
+  if (n0 + C::BN <= p.V) {                 // uniform: every column of the tile is a vocabulary entry
 #pragma unroll
-  for (int j = 0; j < 32; ++j) {
-    const int gc = n0 + 4 * j + part;
-    if constexpr (BIASED)
-      z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) : ninf;
-    else
-      z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) + p.bias[gc] : ninf;
-    mx = fmaxf(mx, z[j]);
+    for (int j = 0; j < 32; ++j) {
+      if constexpr (BIASED)
+        z[j] = ctile<C>(Ct, r, 4 * j + part);
+      else
+        z[j] = ctile<C>(Ct, r, 4 * j + part) + p.bias[n0 + 4 * j + part];
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      const int gc = n0 + 4 * j + part;
+      if constexpr (BIASED)
+        z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) : ninf;
+      else
+        z[j] = gc < p.V ? ctile<C>(Ct, r, 4 * j + part) + p.bias[gc] : ninf;
+    }
   }
+#pragma unroll
+  for (int j = 0; j < 32; ++j) mx = fmaxf(mx, z[j]);
   if (p.want && row < M) {
     const int wc = p.want[row] - n0;      // this thread holds column 4 j + part of the tile
     if (wc >= 0 && wc < C::BN && (wc & 3) == part) {

@@ -53,8 +53,8 @@ R12 bf16 workloads: the oracle runs in fp64 on the bf16-rounded weights. (The GP
     weights and fp32 accumulation; it carries each activation entering a product as two bf16 terms,
     which keeps the chaotic decoder recurrence within the bf16 tolerance over full-length outputs.)
 R15 Throughput counts target tokens of the 1-best, EOS included.
-R18 Hypothesis filters (Section 4.2: constraints such as a maximum number of OOVs and lexical
-    constraints): a candidate whose token is in the banned set, or which would be an UNK beyond
+R18 Hypothesis filters (Section 4.2 names a limit on unknown words and word-level constraints on the
+    search): a candidate whose token is in the banned set, or which would be an UNK beyond
     max_unk UNKs, is not a candidate (log-probs stay normalised over the whole vocabulary).
 R19 Unknown-word replacement (Section 4.2 OOV handling, citing Luong et al. 2015b): every output token
     is aligned to the source position with the largest attention weight of its step (smaller position
@@ -302,11 +302,12 @@ class Result:
     steps: np.ndarray       # [B] step after which the sentence was done
     trace: dict = None      # per step: chosen (slot, token, cand) by rank
     align: list = None      # per token of the 1-best: argmax source position of its step's attention
+    margin: np.ndarray = None   # [B] smallest decision margin of the sentence's run (see beam_search)
 
 
 def allowed(w, n_unk, banned, max_unk):
-    """Hypothesis filter (Section 4.2: beam search under constraints such as a maximum number of OOVs and
-    lexical constraints; R18): a banned token, or an UNK beyond max_unk UNKs (max_unk < 0: no limit),
+    """Hypothesis filter (Section 4.2 names a limit on unknown words and word-level constraints on the
+    search; R18): a banned token, or an UNK beyond max_unk UNKs (max_unk < 0: no limit),
     cannot extend a hypothesis."""
     if w in banned:
         return False
@@ -333,6 +334,13 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
     Sentences are independent; the decoder runs all B*K rows at once only to
     share the matrix products. A finished hypothesis is ranked by
     raw / lp(n) + coverage_penalty (R10, R17).
+
+    ``Result.margin[b]`` is the smallest gap between the two quantities compared by any decision of
+    sentence b's run that can change its output: the K-th against the (K+1)-th finite candidate of every
+    step (which hypotheses survive; the order inside the chosen K only renumbers slots), the stop rule's
+    best finished score against the best live score / lp(max_len), and the best finished entry against the
+    second best. Another implementation whose scores differ from these by less than half the margin makes
+    every decision the same way, so its output tokens must be identical (R16).
     """
     src = np.asarray(src)
     lens = np.asarray(lens)
@@ -350,6 +358,8 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
     done = np.zeros(B, bool)
     steps = np.zeros(B, np.int64)
     best = [None] * B              # (norm, raw, Hyp)
+    pool_norms = [[] for _ in range(B)]
+    margin = np.full(B, np.inf)
     trace = {"slot": [], "tok": [], "cand": []} if record else None
     lp_max = length_penalty(max_len, alpha)
     for t in range(1, max_len + 1):
@@ -374,6 +384,8 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
             flat = cand.ravel()
             order = np.argsort(-flat, kind="stable")            # ties: smaller flat index first
             chosen = [i for i in order[:K] if np.isfinite(flat[i])]
+            if order.size > K and np.isfinite(flat[order[K]]):      # the selection boundary
+                margin[b] = min(margin[b], flat[order[K - 1]] - flat[order[K]])
             new_scores = np.full(K, -np.inf)
             new_hyps = [Hyp([], [], np.zeros(S, F64), []) for _ in range(K)]
             j = 0
@@ -387,6 +399,7 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
                     t_slot[b, rank], t_tok[b, rank], t_cand[b, rank] = k, w, flat[i]
                 if w == EOS_ID or t == max_len:
                     norm = flat[i] / length_penalty(t, alpha) + coverage_penalty(hyp.cov, lens[b], beta)
+                    pool_norms[b].append(norm)
                     if best[b] is None or norm > best[b][0]:
                         best[b] = (norm, flat[i], hyp)
                 else:
@@ -398,6 +411,8 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
             scores[b] = new_scores
             hyps[b] = new_hyps
             live = new_scores[np.isfinite(new_scores)]
+            if stop_rule and best[b] is not None and live.size and t < max_len:
+                margin[b] = min(margin[b], abs(best[b][0] - live.max() / lp_max))
             if (t == max_len or live.size == 0
                     or (stop_rule and best[b] is not None and best[b][0] >= live.max() / lp_max)):
                 done[b] = True
@@ -410,9 +425,13 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
         tok = new_tok
         if done.all():
             break
+    for b in range(B):                                      # the final argmax over the pool
+        if len(pool_norms[b]) > 1:
+            top = sorted(pool_norms[b], reverse=True)
+            margin[b] = min(margin[b], top[0] - top[1])
     return Result([bst[2].tokens for bst in best],
                   np.array([bst[1] for bst in best]), np.array([bst[0] for bst in best]),
-                  [bst[2].logps for bst in best], steps, trace, [bst[2].align for bst in best])
+                  [bst[2].logps for bst in best], steps, trace, [bst[2].align for bst in best], margin)
 
 
 def greedy(m: Model, src, lens, max_len):
@@ -521,82 +540,173 @@ def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0, beta=0.0, banned=(
 # Replay of a recorded search (parity protocol for near-ties, R16)
 # --------------------------------------------------------------------------
 
-def replay_verify(m: Model, src, lens, K, max_len, alpha, trace, tau, sentences=None):
-    """Check another implementation's beam decisions step by step.
+def replay_verify(m: Model, src, lens, K, max_len, alpha, trace, tau, sentences=None, steps=None, result=None,
+                  beta=0.0):
+    """Check another implementation's beam decisions step by step (parity protocol for near-ties, R16).
 
-    ``trace`` holds, per step t (list index t-1), arrays [B, K] by rank:
-    ``slot`` (parent slot, -1 = nothing chosen), ``tok`` and ``cand`` (that
-    implementation's fp64 score). The oracle follows the recorded decisions
-    (teacher forcing its own fp64 decoder through them) and checks that
+    ``trace`` holds, per step t (list index t-1), arrays [B, K] by rank: ``slot`` (parent slot, -1 = nothing
+    chosen), ``tok`` and ``cand`` (that implementation's fp64 score). The oracle follows the recorded
+    decisions, teacher forcing its own fp64 decoder through them (all listed sentences in one batch, like
+    beam_search), and keeps the finished pool of R9 on the recorded scores. It checks that
       * every chosen candidate's log-prob agrees with the oracle's within tau;
-      * the chosen set is a valid top-K under the oracle's log-probs added to
-        the recorded scores (chosen >= K-th - tau, rejected <= K-th + tau);
-      * every recorded score stays within t * tau of the oracle's running sum.
-    Returns a list of violation strings (empty = pass).
+      * the chosen set is a valid top-K under the oracle's log-probs added to the recorded scores
+        (chosen >= K-th - tau, rejected <= K-th + tau);
+      * every recorded score stays within t * tau of the oracle's running sum;
+      * a chosen EOS (or any choice at max_len) leaves the live slots: the next step's slots are the
+        other choices in rank order, so a finished hypothesis kept live shows up there as wrong log-probs
+        or scores;
+      * the sentence stops exactly when rule (iii) fires on the recorded numbers (no choices recorded
+        after that step, some at every step before it; ``steps[b]``, if given, is that step), and the
+        same rule on the oracle's running sums agrees wherever its two sides differ by more than t * tau;
+      * ``result`` (dict of [B] arrays ``len``, ``raw``, ``norm`` and [B, T] ``tokens``), if given, is the
+        pool's best entry by normalised score on the recorded numbers (earlier step, then better rank, on
+        ties), and on the oracle's numbers no pool entry beats it by more than t * tau.
+    With beta > 0 the coverage penalty of an entry is the oracle's, from the attention along its
+    replayed steps. Returns a list of violation strings (empty = pass).
     """
     src = np.asarray(src)
-    B = src.shape[0]
+    lens = np.asarray(lens)
+    B, S = src.shape
     V = m.tgt_vocab
-    if sentences is None:
-        sentences = range(B)
+    sel = list(range(B)) if sentences is None else [int(x) for x in sentences]
+    nb = len(sel)
     bad = []
-    for b in sentences:
-        enc = encode(m, src[b:b + 1], np.asarray(lens)[b:b + 1])
-        st = init_state(m, enc, K)
-        s_rec = np.full(K, -np.inf)       # recorded scores of live slots
-        s_orc = np.full(K, -np.inf)       # oracle running sums along the same hypotheses
-        s_rec[0] = s_orc[0] = 0.0
-        tok = np.full(K, BOS_ID, np.int64)
-        for t in range(1, len(trace["slot"]) + 1):
+    if nb == 0:
+        return bad
+    ninf = -np.inf
+    enc = encode(m, src[sel], lens[sel])
+    st = init_state(m, enc, K)
+    row_sentence = np.repeat(np.arange(nb), K)
+    lp_max = length_penalty(max_len, alpha)
+    s_rec = np.full((nb, K), ninf)        # recorded scores of the live slots
+    s_orc = np.full((nb, K), ninf)        # oracle running sums along the same hypotheses
+    s_rec[:, 0] = s_orc[:, 0] = 0.0
+    toks = [[[] for _ in range(K)] for _ in range(nb)]
+    cov = np.zeros((nb, K, S), F64)
+    pool = [[] for _ in range(nb)]        # (norm_rec, norm_orc, raw_rec, t, rank, tokens)
+    active = np.ones(nb, bool)
+    tok = np.full(nb * K, BOS_ID, np.int64)
+    T = len(trace["slot"])
+    rel = lambda x: 1e-12 * max(1.0, abs(x))
+    for t in range(1, T + 1):
+        if not active.any():
+            break
+        st_new, logp, attn = decode_step(m, enc, st, tok, row_sentence)
+        parent = np.arange(nb * K)
+        new_tok = np.full(nb * K, PAD_ID, np.int64)
+        lp_t = length_penalty(t, alpha)
+        for i, b in enumerate(sel):
+            if not active[i]:
+                continue
             slot = np.asarray(trace["slot"][t - 1][b])
-            if (slot < 0).all():
-                break
             wtok = np.asarray(trace["tok"][t - 1][b])
             cand_rec = np.asarray(trace["cand"][t - 1][b])
-            st_new, logp, _ = decode_step(m, enc, st, tok, np.zeros(K, np.int64))
-            oc = s_rec[:, None] + logp                       # oracle log-probs on recorded scores
-            flat = np.sort(oc.ravel())[::-1]
+            rows = slice(i * K, (i + 1) * K)
+            if (slot < 0).all():
+                bad.append(f"b{b} t{t}: nothing chosen while the sentence is live")
+                active[i] = False
+                continue
+            oc = s_rec[i][:, None] + logp[rows]               # oracle log-probs on recorded scores
+            flat = oc.ravel()
             n_fin = int(np.isfinite(flat).sum())
             kk = min(K, n_fin)
-            theta = flat[kk - 1]
+            theta = -np.partition(-flat, kk - 1)[kk - 1]      # the oracle's K-th value
             chosen = set()
-            parent = np.zeros(K, np.int64)
-            new_tok = np.full(K, PAD_ID, np.int64)
-            ns_rec = np.full(K, -np.inf)
-            ns_orc = np.full(K, -np.inf)
+            ns_rec = np.full(K, ninf)
+            ns_orc = np.full(K, ninf)
+            n_toks = [[] for _ in range(K)]
+            n_cov = np.zeros((K, S), F64)
             j = 0
             for r in range(K):
                 k = int(slot[r])
                 if k < 0:
                     continue
                 w = int(wtok[r])
+                if k >= K or not 0 <= w < V:
+                    bad.append(f"b{b} t{t} r{r}: slot {k} / token {w} out of range")
+                    continue
                 chosen.add(k * V + w)
-                if not np.isfinite(s_rec[k]):
+                if not np.isfinite(s_rec[i, k]):
                     bad.append(f"b{b} t{t} r{r}: chose dead slot {k}")
                     continue
-                lp_rec = cand_rec[r] - s_rec[k]
-                if abs(lp_rec - logp[k, w]) > tau:
-                    bad.append(f"b{b} t{t} r{r}: logp {lp_rec:.6g} vs oracle {logp[k, w]:.6g}")
+                lpk = logp[i * K + k, w]
+                lp_rec = cand_rec[r] - s_rec[i, k]
+                if abs(lp_rec - lpk) > tau:
+                    bad.append(f"b{b} t{t} r{r}: logp {lp_rec:.6g} vs oracle {lpk:.6g}")
                 if oc[k, w] < theta - tau:
                     bad.append(f"b{b} t{t} r{r}: chosen {oc[k, w]:.8g} below K-th {theta:.8g} - tau")
-                run = s_orc[k] + logp[k, w]
+                run = s_orc[i, k] + lpk
                 if abs(cand_rec[r] - run) > t * tau:
                     bad.append(f"b{b} t{t} r{r}: score drift {cand_rec[r] - run:.3g}")
-                if not (w == EOS_ID or t == max_len):
-                    parent[j] = k
-                    new_tok[j] = w
+                hyp_toks = toks[i][k] + [w]
+                hyp_cov = cov[i, k] + attn[i * K + k]
+                if w == EOS_ID or t == max_len:
+                    cp = coverage_penalty(hyp_cov, lens[b], beta)
+                    pool[i].append((cand_rec[r] / lp_t + cp, run / lp_t + cp, cand_rec[r], t, r, hyp_toks))
+                else:
+                    parent[i * K + j] = i * K + k
+                    new_tok[i * K + j] = w
                     ns_rec[j] = cand_rec[r]
                     ns_orc[j] = run
+                    n_toks[j] = hyp_toks
+                    n_cov[j] = hyp_cov
                     j += 1
             if len(chosen) != kk:
                 bad.append(f"b{b} t{t}: {len(chosen)} chosen, expected {kk}")
-            # rejected candidates must not beat the K-th by more than tau
             masked = oc.copy().ravel()
             if chosen:
-                masked[np.fromiter(chosen, np.int64)] = -np.inf
+                masked[np.fromiter(chosen, np.int64)] = ninf
             if masked.max() > theta + tau:
                 bad.append(f"b{b} t{t}: rejected {masked.max():.8g} above K-th {theta:.8g} + tau")
-            st = st_new.take(parent)
-            tok = new_tok
-            s_rec, s_orc = ns_rec, ns_orc
+            s_rec[i], s_orc[i], toks[i], cov[i] = ns_rec, ns_orc, n_toks, n_cov
+            # rule (iii) on the recorded numbers decides; the oracle's numbers must agree outside t * tau
+            stop = t == max_len or j == 0
+            if not stop and pool[i]:
+                best_rec = max(e[0] for e in pool[i])
+                bound_rec = ns_rec[:j].max() / lp_max
+                tol = rel(bound_rec) if beta == 0.0 else t * tau
+                stop = best_rec >= bound_rec
+                if abs(best_rec - bound_rec) <= tol:
+                    stop = None                                # a tie within rounding: either is correct
+                best_orc = max(e[1] for e in pool[i])
+                bound_orc = ns_orc[:j].max() / lp_max
+                if stop is not None and (best_orc >= bound_orc) != stop and abs(best_orc - bound_orc) > t * tau:
+                    bad.append(f"b{b} t{t}: stop rule {stop} on the recorded scores, {not stop} on the oracle's "
+                               f"({best_orc:.10g} vs {bound_orc:.10g})")
+            if stop is None:                                   # follow what the implementation did
+                stop = (t < T and (np.asarray(trace["slot"][t][b]) < 0).all())
+            if stop:
+                active[i] = False
+                if steps is not None and int(steps[b]) != t:
+                    bad.append(f"b{b}: finished at step {int(steps[b])}, rule (iii) fires at step {t}")
+                if t < T and not all((np.asarray(trace["slot"][u][b]) < 0).all() for u in range(t, T)):
+                    bad.append(f"b{b}: choices recorded after the sentence finished at step {t}")
+        st = st_new.take(parent)
+        tok = new_tok
+    for i, b in enumerate(sel):
+        if active[i]:
+            bad.append(f"b{b}: the record ends at step {T} before the sentence finished")
+        if result is None or not pool[i]:
+            continue
+        best = None                                            # first maximum in (step, rank) order
+        for e in pool[i]:
+            if best is None or e[0] > best[0]:
+                best = e
+        n = int(result["len"][b])
+        got = [int(x) for x in np.asarray(result["tokens"][b])[:n]]
+        if got != best[5]:
+            # a tie within rounding on the recorded numbers leaves either entry correct
+            alt = [e for e in pool[i] if e[5] == got]
+            if not alt or abs(alt[0][0] - best[0]) > rel(best[0]):
+                bad.append(f"b{b}: returned hypothesis is not the pool's best ({n} tokens vs {len(best[5])})")
+                continue
+            best = alt[0]
+        if abs(float(result["raw"][b]) - best[2]) > rel(best[2]):
+            bad.append(f"b{b}: returned raw {float(result['raw'][b]):.12g} vs pool entry {best[2]:.12g}")
+        if abs(float(result["norm"][b]) - best[0]) > (rel(best[0]) if beta == 0.0 else best[3] * tau):
+            bad.append(f"b{b}: returned norm {float(result['norm'][b]):.12g} vs pool entry {best[0]:.12g}")
+        top_orc = max(e[1] for e in pool[i])
+        if best[1] < top_orc - best[3] * tau:
+            bad.append(f"b{b}: on the oracle's numbers the pool's best beats the returned entry by "
+                       f"{top_orc - best[1]:.3g}")
     return bad

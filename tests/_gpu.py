@@ -33,32 +33,79 @@ def with_workload(w, **kw):
     return W.Workload(**{**w.as_dict(), **kw})
 
 
-def check_search(s, buf, sentences, K, T, alpha):
+def golden_search(name, seed):
+    """Stored oracle results of a whole batch (written by tests/golden/make_search_golden.py)."""
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", f"search_{name}_seed{seed}.npz")
+    with np.load(path, allow_pickle=False) as z:
+        return {k: z[k] for k in z.files}
+
+
+def check_search(s, buf, sentences, K, T, alpha, golden=None, log=None):
+    """Parity of one GPU search against the oracle, on the listed sentences (section P1-P3 protocol).
+
+    * the GPU's result is internally consistent (log-probs sum to raw; norm = raw / lp; pad after the end);
+    * P3: the oracle's own search of the same sentences (``golden``: its stored results for the whole
+      batch) gives the same tokens wherever its decision margin exceeds 2 tau, and where tokens agree the
+      raw scores agree within n tau; a sentence may differ only where the margin is within 2 tau;
+    * every GPU 1-best is rescored by the oracle's teacher-forced decoder: per-token log-probs within tau;
+    * P2: every listed sentence's recorded decisions are replayed through the oracle (log-probs, top-K
+      validity, finished pool, stop step and the returned entry).
+    Returns the sentences whose tokens differ from the oracle's (all replay-verified).
+    """
     tau = s.tau
+    sel = [int(b) for b in sentences]
+    say = log or (lambda msg: None)
     g_tok = buf["tok"].cpu().numpy()
     g_len = buf["len"].cpu().numpy()
     g_raw = buf["raw"].cpu().numpy()
     g_norm = buf["norm"].cpu().numpy()
     g_lp = buf["tok_logp"].cpu().numpy()
+    g_steps = buf["trace_steps"].cpu().numpy()
     trace = {k: [a for a in buf[f"trace_{k}"].cpu().numpy()] for k in ("slot", "tok", "cand")}
-    mismatched = []
-    for b in sentences:
-        res = O.beam_search(s.model, s.src[b:b + 1], s.lens[b:b + 1], K, T, alpha)
+    for b in sel:
         n = int(g_len[b])
-        toks = list(g_tok[b, :n])
+        assert 1 <= n <= T
         assert (g_tok[b, n:] == W.PAD_ID).all()
-        # the GPU's own result is internally consistent: per-token log-probs sum to raw, norm = raw / lp
         assert abs(g_lp[b, :n].astype(np.float64).sum() - g_raw[b]) < 1e-6 * max(1, n)
         assert abs(g_norm[b] - g_raw[b] / O.length_penalty(n, alpha)) < 1e-9 * max(1.0, abs(g_raw[b]))
-        # teacher-forced oracle rescoring of the GPU's hypothesis
-        forced = O.score_forced(s.model, s.src[b], s.lens[b], toks)
-        assert np.abs(forced - g_lp[b, :n]).max() <= tau
-        assert abs(forced.sum() - g_raw[b]) <= n * tau
-        if toks == res.tokens[0]:
-            assert abs(res.raw[0] - g_raw[b]) <= n * tau
+    # the oracle's own search: tokens, raw score and decision margin per sentence
+    if golden is None:
+        res = O.beam_search(s.model, s.src[sel], s.lens[sel], K, T, alpha)
+        o_tok = {b: res.tokens[i] for i, b in enumerate(sel)}
+        o_raw = {b: res.raw[i] for i, b in enumerate(sel)}
+        o_margin = {b: res.margin[i] for i, b in enumerate(sel)}
+    else:
+        assert (golden["src"] == s.src).all() and (golden["lens"] == s.lens).all()
+        o_tok = {b: [int(x) for x in golden["tokens"][b, :int(golden["len"][b])]] for b in sel}
+        o_raw = {b: golden["raw"][b] for b in sel}
+        o_margin = {b: golden["margin"][b] for b in sel}
+    say(f"oracle search ready for {len(sel)} sentences")
+    # teacher-forced rescoring of every GPU 1-best, all listed sentences in one batch
+    forced, _ = O.score_batch(s.model, s.src[sel], s.lens[sel], g_tok[sel], g_len[sel])
+    for i, b in enumerate(sel):
+        n = int(g_len[b])
+        err = np.abs(forced[i, :n] - g_lp[b, :n]).max()
+        assert err <= tau, f"sentence {b}: per-token log-prob error {err:.3g} > {tau}"
+        assert abs(forced[i, :n].sum() - g_raw[b]) <= n * tau
+    say("teacher-forced rescoring passed")
+    mismatched, unexplained = [], []
+    for b in sel:
+        n = int(g_len[b])
+        toks = [int(x) for x in g_tok[b, :n]]
+        if toks == o_tok[b]:
+            assert abs(o_raw[b] - g_raw[b]) <= n * tau
         else:
             mismatched.append(b)
-    # every sentence (matched or not) must pass the step-by-step replay of the GPU's decisions
-    bad = O.replay_verify(s.model, s.src, s.lens, K, T, alpha, trace, tau, sentences=sentences)
+            if o_margin[b] > 2 * tau:
+                unexplained.append((b, float(o_margin[b])))
+    assert not unexplained, f"tokens differ although every oracle decision margin exceeds 2 tau: {unexplained[:10]}"
+    say(f"P3: {len(sel) - len(mismatched)} of {len(sel)} sentences token-identical, "
+        f"{sum(1 for b in sel if o_margin[b] > 2 * tau)} of them with every margin > 2 tau")
+    # P2: replay every listed sentence's decisions, including its finish step and returned entry
+    result = {"tokens": g_tok, "len": g_len, "raw": g_raw, "norm": g_norm}
+    bad = O.replay_verify(s.model, s.src, s.lens, K, T, alpha, trace, tau, sentences=sel, steps=g_steps,
+                          result=result)
     assert bad == [], bad[:10]
+    say("replay passed")
     return mismatched

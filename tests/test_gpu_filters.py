@@ -1,5 +1,6 @@
 """GPU parity of the hypothesis filters and the unknown-word alignment (Section 4.2: beam search under
-constraints such as a maximum number of OOVs and lexical constraints; OOV handling; readings R18, R19).
+a limit on unknown words and
+word-level constraints on the search; OOV handling; readings R18, R19).
 """
 
 import numpy as np

@@ -67,7 +67,10 @@ def _oracle_state(s, st_views, N):
                    feed.cpu().numpy().astype(np.float64))
 
 
-@pytest.mark.parametrize("which", ["tiny", "tiny_peaked", "default"])
+STATE_TOL = {"fp32": 1e-5, "bf16": 1e-3}     # decoder h, c and feed after a step
+
+
+@pytest.mark.parametrize("which", ["tiny", "tiny_peaked", "default", "larger", "greedy", "long_src"])
 def test_decode_steps_full_and_topk(which, request):
     s = request.getfixturevalue(which)
     w = s.w
@@ -94,9 +97,11 @@ def test_decode_steps_full_and_topk(which, request):
         o_new, o_logp, o_attn = O.decode_step(s.model, enc, o_in, tok, rows)
         g_logp = logp.cpu().numpy()
         err = np.abs(g_logp - o_logp).max()
-        print(f"  step {step}: max |logp - oracle| = {err:.3g}", flush=True)
+        a_err = np.abs(attn.cpu().numpy() - o_attn).max()
+        print(f"  step {step}: max |logp - oracle| = {err:.3g}, max |attention - oracle| = {a_err:.3g}", flush=True)
         assert err <= s.tau
         np.testing.assert_allclose(attn.cpu().numpy(), o_attn, atol=ATTN_TOL[w.wdtype], rtol=0)
+        assert (attn.cpu().numpy()[~enc.mask[rows]] == 0).all()     # exactly zero at pads
         # top-K mode: values within tau, ids exact where the oracle's sorted gaps exceed 2 tau
         o_sorted = np.argsort(-o_logp, axis=1, kind="stable")[:, :K + 1]
         g_ids = ti.cpu().numpy()
@@ -113,10 +118,15 @@ def test_decode_steps_full_and_topk(which, request):
             assert torch.equal(a, b)
         np.testing.assert_allclose(lse.cpu().numpy(), lse2.cpu().numpy(), atol=0, rtol=0)
         h, c, feed = tr.state_views(st_full, N)
+        st_err = max([np.abs(h[l].cpu().numpy() - o_new.h[l]).max() for l in range(w.dec_layers)] +
+                     [np.abs(c[l].cpu().numpy() - o_new.c[l]).max() for l in range(w.dec_layers)] +
+                     [np.abs(feed.cpu().numpy() - o_new.feed).max()])
+        print(f"  step {step}: max |state - oracle| = {st_err:.3g}", flush=True)
+        stol = STATE_TOL[w.wdtype]
         for l in range(w.dec_layers):
-            np.testing.assert_allclose(h[l].cpu().numpy(), o_new.h[l], atol=1e-5, rtol=0)
-            np.testing.assert_allclose(c[l].cpu().numpy(), o_new.c[l], atol=1e-5, rtol=0)
-        np.testing.assert_allclose(feed.cpu().numpy(), o_new.feed, atol=1e-5, rtol=0)
+            np.testing.assert_allclose(h[l].cpu().numpy(), o_new.h[l], atol=stol, rtol=0)
+            np.testing.assert_allclose(c[l].cpu().numpy(), o_new.c[l], atol=stol, rtol=0)
+        np.testing.assert_allclose(feed.cpu().numpy(), o_new.feed, atol=stol, rtol=0)
         # next step: random in-sentence parents and random tokens
         parent = (np.repeat(np.arange(B), K) * K + rng.integers(0, K, size=N)).astype(np.int32)
         tok = rng.integers(0, w.tgt_vocab, size=N).astype(np.int32)
@@ -147,20 +157,6 @@ def test_beam_widths_tiny_peaked(tiny_peaked, K):
     s.tr.beam_search(s.src_d, s.lens_d, buf)
     torch.cuda.synchronize()
     check_search(s, buf, range(B), K, 9, 0.6)
-
-
-def test_beam_search_default_sampled(default):
-    # full default workload (64 sentences, beam 5, max 100) on the GPU; oracle on sampled sentences
-    s = default
-    w = s.w
-    B, S = s.src.shape
-    _print_case("beam_search", workload=w.name, B=B)
-    buf = s.tr.search_buffers(B, S, w.beam, w.max_len, w.alpha, trace=True)
-    s.tr.beam_search(s.src_d, s.lens_d, buf)
-    torch.cuda.synchronize()
-    g_len = buf["len"].cpu().numpy()
-    assert (g_len >= 1).all() and (g_len <= w.max_len).all()
-    check_search(s, buf, [0, 37, 63], w.beam, w.max_len, w.alpha)
 
 
 def test_search_is_deterministic(tiny_peaked):
@@ -194,8 +190,8 @@ def test_all_zero_weights_tie_rules():
             assert abs(buf["raw"][b].item() + len(want) * np.log(50)) < 1e-5
 
 
-# ------------------------------------------------------------------ the other workloads (full batches on
-# the GPU, oracle on sampled sentences; bf16 workloads at the bf16 tolerance)
+# ------------------------------------------------------------------ the other workloads (bf16 workloads at
+# the bf16 tolerance); their whole searches are in test_gpu_search_all.py
 @pytest.fixture(scope="module")
 def larger():
     return Setup(W.get("larger"))
@@ -219,49 +215,15 @@ def test_encoder_other_workloads(which, request):
     ws = s.tr.encode(s.src_d, s.lens_d)
     torch.cuda.synchronize()
     mem, keys, fh, fc = s.tr.enc_views(ws, B, S)
-    pick = [0, B // 2, B - 1]
-    enc = O.encode(s.model, s.src[pick], s.lens[pick])
+    enc = O.encode(s.model, s.src, s.lens)
     tol = 1e-4 if s.w.wdtype == "fp32" else 2e-2
-    np.testing.assert_allclose(mem.cpu().numpy()[pick], enc.memory, atol=tol, rtol=0)
+    err = np.abs(mem.cpu().numpy() - enc.memory).max()
+    print(f"  max |memory - oracle| = {err:.3g} over all {B} sentences", flush=True)
+    np.testing.assert_allclose(mem.cpu().numpy(), enc.memory, atol=tol, rtol=0)
+    assert (mem.cpu().numpy()[~enc.mask] == 0).all()
+    if s.w.attn == "general":
+        np.testing.assert_allclose(keys.cpu().numpy()[enc.mask], (enc.memory @ s.model.w["W_a"].T)[enc.mask],
+                                   atol=tol, rtol=0)
     for l in range(s.w.dec_layers):
-        np.testing.assert_allclose(fh[l].cpu().numpy()[pick], enc.final_h[l], atol=tol, rtol=0)
-
-
-@pytest.mark.parametrize("which", ["larger", "greedy"])
-def test_decode_step_bf16(which, request):
-    # one full-vocabulary step from the encoder state, sampled rows, bf16 tolerance
-    s = request.getfixturevalue(which)
-    w = s.w
-    B, S = s.src.shape
-    K = w.beam
-    _print_case("decode_step", workload=w.name)
-    ws = s.tr.encode(s.src_d, s.lens_d)
-    st = s.tr.decode_init(ws, B, S, K)
-    tok = torch.full((B * K,), W.BOS_ID, dtype=torch.int32, device="cuda")
-    _, logp, _, _, attn = s.tr.decode_step(ws, B, S, K, st, tok, None, mode=0, want_attn=True)
-    torch.cuda.synchronize()
-    sent = [0, B // 2, B - 1]
-    enc = O.encode(s.model, s.src[sent], s.lens[sent])
-    ost = O.init_state(s.model, enc, K)
-    rows = np.repeat(np.arange(len(sent)), K)
-    _, o_logp, o_attn = O.decode_step(s.model, enc, ost, np.full(len(rows), W.BOS_ID), rows)
-    g_rows = np.concatenate([np.arange(b * K, (b + 1) * K) for b in sent])
-    err = np.abs(logp.cpu().numpy()[g_rows] - o_logp).max()
-    print(f"  max |logp - oracle| = {err:.3g}", flush=True)
-    assert err <= s.tau
-    np.testing.assert_allclose(attn.cpu().numpy()[g_rows], o_attn, atol=ATTN_TOL[w.wdtype], rtol=0)
-
-
-@pytest.mark.parametrize("which,sample", [("larger", [5]), ("greedy", [3, 300]), ("long_src", [7])])
-def test_beam_search_other_workloads(which, sample, request):
-    s = request.getfixturevalue(which)
-    w = s.w
-    B, S = s.src.shape
-    _print_case("beam_search", workload=w.name, B=B)
-    buf = s.tr.search_buffers(B, S, w.beam, w.max_len, w.alpha, trace=True)
-    s.tr.beam_search(s.src_d, s.lens_d, buf)
-    torch.cuda.synchronize()
-    g_len = buf["len"].cpu().numpy()
-    assert (g_len >= 1).all() and (g_len <= w.max_len).all()
-    mism = check_search(s, buf, sample, w.beam, w.max_len, w.alpha)
-    print(f"  free-run token mismatches (replay-verified): {mism}", flush=True)
+        np.testing.assert_allclose(fh[l].cpu().numpy(), enc.final_h[l], atol=tol, rtol=0)
+        np.testing.assert_allclose(fc[l].cpu().numpy(), enc.final_c[l], atol=tol, rtol=0)

@@ -1,5 +1,6 @@
 """Pins for the oracle's hypothesis filters and unknown-word replacement (Section 4.2: beam search under
-constraints such as a maximum number of OOVs and lexical constraints, and OOV handling; readings R18,
+a limit on unknown words and
+word-level constraints on the search, and OOV handling; readings R18,
 R19).
 
 A beam wide enough to keep every hypothesis must return the exhaustive-search optimum over the allowed

@@ -36,12 +36,32 @@ def test_wide_beam_equals_brute_force(alpha):
         assert abs(res.raw[b] - raw) < 1e-12 and abs(res.norm[b] - norm) < 1e-12
 
 
-def test_brute_force_counts_sequences():
-    # independent count of the enumeration: sum_{n<=T} (V-1)^(n-1) + (V-1)^T ... EOS-terminated
-    # sequences of length n have (V-1)^(n-1) prefixes; EOS-free length-T sequences (V-1)^T.
-    V, T = 6, 3
-    n = sum((V - 1) ** (k - 1) for k in range(1, T + 1)) + (V - 1) ** T
-    assert n == 156
+def test_brute_force_scores_every_output_sequence_once(monkeypatch):
+    # the sequences brute_force scores, recorded through score_forced, must be exactly the output
+    # sequences of the search space: those whose first EOS ends them at n <= T (EOS-free prefixes of
+    # length n - 1: (V-1)^(n-1) of them) and the EOS-free sequences of length T ((V-1)^T): 156 at V = 6,
+    # T = 3, listed here by direct enumeration
+    import itertools
+    w, ws, m = _small.model(seed=31, scale={"W_s": 20.0, "b_s": 5.0})
+    src, lens = _small.batch(w, seed=32)
+    V, T = m.tgt_vocab, 3
+    seen = []
+    real = O.score_forced
+
+    def counting(mm, s_row, n_src, target):
+        seen.append(tuple(target))
+        return real(mm, s_row, n_src, target)
+
+    monkeypatch.setattr(O, "score_forced", counting)
+    O.brute_force(m, src[0], lens[0], T)
+    want = set()
+    for n in range(1, T + 1):
+        for seq in itertools.product(range(V), repeat=n):
+            if EOS_ID not in seq[:-1] and (seq[-1] == EOS_ID or n == T):
+                want.add(seq)
+    assert len(want) == sum((V - 1) ** (k - 1) for k in range(1, T + 1)) + (V - 1) ** T == 156
+    assert len(seen) == len(set(seen)) == 156
+    assert set(seen) == want
 
 
 @pytest.mark.parametrize("seed", [41, 42])

@@ -94,19 +94,47 @@ def banned_ids(w, n):
     return tuple(range(4, 4 + 7 * n, 7)) if n else ()
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def blas_vendor():
+    try:
+        import numpy as np
+        cfg = np.show_config(mode="dicts")
+        b = cfg["Build Dependencies"]["blas"]
+        return f"{b.get('name', '?')} {b.get('version', '')}".strip()
+    except Exception:
+        return "unknown"
+
+
 def cpu_baseline(w, weights, src, lens, n_sent, beta=0.0, banned=(), max_unk=-1):
-    """The oracle (fp64 NumPy) on the first n_sent sentences of the same batch, on this host's cores."""
+    """The oracle on the first n_sent sentences of the same batch, on this host's cores: its fp32 mode
+    (single-precision BLAS products, fp64 beam scores) is the timed baseline; the fp64 parity mode is
+    timed on the same sentences and reported beside it."""
+    import numpy as np
     from oracle import onmt_oracle as O
     threads = cpu_threads()
-    m = O.model_from(w, weights)
-    t0 = time.perf_counter()
-    res = O.beam_search(m, src[:n_sent], lens[:n_sent], w.beam, w.max_len, w.alpha, beta=beta, banned=banned,
-                        max_unk=max_unk)
-    dt = time.perf_counter() - t0
-    toks = int(sum(len(t) for t in res.tokens))
+    out = {}
+    for name, dt_ in (("fp32", np.float32), ("fp64", np.float64)):
+        m = O.model_from(w, weights, dtype=dt_)
+        t0 = time.perf_counter()
+        res = O.beam_search(m, src[:n_sent], lens[:n_sent], w.beam, w.max_len, w.alpha, beta=beta, banned=banned,
+                            max_unk=max_unk)
+        dt = time.perf_counter() - t0
+        out[name] = (int(sum(len(t) for t in res.tokens)), dt)
+    toks, dt = out["fp32"]
+    toks64, dt64 = out["fp64"]
     return {"value": round(toks / dt, 3), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{n_sent} of the {src.shape[0]} sentences (full beam search incl. encoder), "
-                      f"{toks} target tokens in {dt:.1f} s, fp64 NumPy"}
+                      f"{toks} target tokens in {dt:.1f} s with the oracle's fp32 mode (fp64 beam scores)",
+            "value_fp64": round(toks64 / dt64, 3), "cpu_model": cpu_model(), "blas": blas_vendor()}
 
 
 def main():
@@ -294,16 +322,22 @@ def bench_score(args, w, weights, tr, src, lens, src_d, lens_d):
                      "avg_launch_us": round(avg_gen_s * 1e6, 2), "flops_per_launch": gen_flops},
     }
     if not args.no_cpu_baseline:
+        import numpy as np
         from oracle import onmt_oracle as O
-        m = O.model_from(w, weights)
         n = max(1, min(args.cpu_sentences, B))
-        t1 = time.perf_counter()
-        O.score_batch(m, src[:n], lens[:n], tgt[:n], tgt_len[:n])
-        ct = time.perf_counter() - t1
-        out["cpu_baseline"] = {"value": round(int(tgt_len[:n].sum()) / ct, 3), "unit": "tokens/s",
+        ct = {}
+        for name, dt_ in (("fp32", np.float32), ("fp64", np.float64)):
+            m = O.model_from(w, weights, dtype=dt_)
+            t1 = time.perf_counter()
+            O.score_batch(m, src[:n], lens[:n], tgt[:n], tgt_len[:n])
+            ct[name] = time.perf_counter() - t1
+        ntok = int(tgt_len[:n].sum())
+        out["cpu_baseline"] = {"value": round(ntok / ct["fp32"], 3), "unit": "tokens/s",
                                "cores": cpu_threads(), "kind": "oracle",
-                               "sample": f"{n} of the {B} sentences, {int(tgt_len[:n].sum())} target tokens "
-                                         f"in {ct:.1f} s, fp64 NumPy"}
+                               "sample": f"{n} of the {B} sentences, {ntok} target tokens in {ct['fp32']:.1f} s "
+                                         f"with the oracle's fp32 mode",
+                               "value_fp64": round(ntok / ct["fp64"], 3), "cpu_model": cpu_model(),
+                               "blas": blas_vendor()}
     print(json.dumps(out), flush=True)
 
 

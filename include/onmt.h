@@ -22,7 +22,8 @@
  *   - Return 0 (ONMT_OK) or a negative error code; never throw or abort. onmt_last_error() gives a
  *     thread-local message for the last failure.
  *   - All size and id checks happen before any compute is enqueued. On error no kernel has been
- *     launched and output buffers are unspecified.
+ *     launched and output buffers are unspecified. (With ONMT_VALIDATE_DEVICE, ids and lengths are
+ *     instead checked by a kernel on the stream; see "Input validation".)
  *   - The caller owns all device memory: it allocates the buffers whose sizes the *_bytes queries
  *     return and passes device pointers. The library never allocates device memory.
  *   - `stream` is a hipStream_t (NULL = default stream). Work is ordered on that stream.
@@ -80,8 +81,8 @@ typedef struct {
   double alpha;
   int check_every;
   double beta;
-  /* Hypothesis filters (Section 4.2: beam search under constraints such as a maximum number of OOVs and
-   * lexical constraints): a candidate whose token is one of banned[0 .. n_banned) (host array, ids in
+  /* Hypothesis filters (Section 4.2 names limits on unknown words and word-level constraints on the
+   * search): a candidate whose token is one of banned[0 .. n_banned) (host array, ids in
    * [0, tgt_vocab)), or an unk_id beyond max_unk UNKs of its hypothesis (max_unk < 0: no limit), is not
    * a candidate; log-probs stay normalised over the whole vocabulary. */
   int max_unk;
@@ -132,8 +133,12 @@ int onmt_model_destroy(onmt_model* model);
  * ids in [0, src_vocab). Positions >= len[b] are ignored. Writes the memory bank, the attention keys
  * (general: W_a m_s; concat: the memory columns of W_a times m_s; dot: none, the scores read the
  * memory) and the final states into enc_ws (>= onmt_encode_ws_bytes(model, B, S_max)), which the
- * decoder calls then read. Copies src and len to the host to validate them (one stream sync), then
- * enqueues the encoder asynchronously. */
+ * decoder calls then read. With host validation (the default) src and len are copied to the host and
+ * checked (one stream sync), then the encoder is enqueued asynchronously; with device validation nothing
+ * waits. The GEMMs read operands through 2 GiB buffer descriptors: a batch whose memory bank
+ * (B * S_max rows of the memory width padded to 128 columns, fp32) or decoder state rows (B * beam rows)
+ * would reach 2 GiB is refused with ONMT_EUNSUPPORTED, as is a model whose embedding table or packed
+ * weight matrix would (onmt_num_weights / onmt_model_bytes report it), and scoring over B * T_max rows. */
 size_t onmt_encode_ws_bytes(const onmt_model* model, int B, int S_max);
 int onmt_encode(onmt_model* model, const int32_t* src, const int32_t* len, int B, int S_max, void* enc_ws,
                 size_t enc_ws_bytes, void* stream);
@@ -153,8 +158,9 @@ int onmt_encode(onmt_model* model, const int32_t* src, const int32_t* len, int B
  *                   smaller id on ties.
  *   lse [N] (optional) = logsumexp of each row's logits. attn [N, S_max] (optional) = attention weights,
  *   exactly 0 at pads.
- * step_ws holds onmt_step_ws_bytes(model, B, S_max, K) bytes of scratch. prev_tok and parent are copied
- * to the host for validation (one stream sync); the compute is then enqueued asynchronously. */
+ * step_ws holds onmt_step_ws_bytes(model, B, S_max, K) bytes of scratch. With host validation (the default)
+ * prev_tok and parent are copied to the host and checked (one stream sync), then the compute is enqueued
+ * asynchronously; with device validation (onmt_set_validation below) nothing waits. */
 size_t onmt_state_bytes(const onmt_model* model, int N);
 size_t onmt_step_ws_bytes(const onmt_model* model, int B, int S_max, int K);
 int onmt_decode_init(onmt_model* model, const void* enc_ws, int B, int S_max, int K, void* state_out,
@@ -162,6 +168,20 @@ int onmt_decode_init(onmt_model* model, const void* enc_ws, int B, int S_max, in
 int onmt_decode_step(onmt_model* model, const void* enc_ws, int B, int S_max, int K, const void* state_in,
                      void* state_out, const int32_t* prev_tok, const int32_t* parent, int mode, float* logp,
                      int32_t* ids, float* lse, float* attn, void* step_ws, size_t step_ws_bytes, void* stream);
+
+/* ---- Input validation ---------------------------------------------------------------------------------
+ * ONMT_VALIDATE_HOST (the default): onmt_encode, onmt_decode_step and onmt_beam_search copy their device
+ * id / length inputs to the host and check them before enqueuing anything, returning ONMT_EINVAL on a bad
+ * value (one stream sync per call). ONMT_VALIDATE_DEVICE: a kernel enqueued on the stream checks them
+ * instead, so the call does not wait for the device; a bad value is replaced by a safe one (a length
+ * clamped to [1, S_max], an id by 0, a parent by the row itself), the computation goes on, and the model
+ * records the failure. In this mode the encoder steps over all S_max positions (the host does not learn
+ * the longest length), which gives the same results. onmt_device_status sets *code to ONMT_OK or
+ * ONMT_EINVAL (onmt_last_error then says what was wrong) for the work enqueued since its last call and
+ * clears the record; call it after synchronizing the stream(s) the work ran on. It does not synchronize. */
+enum { ONMT_VALIDATE_HOST = 0, ONMT_VALIDATE_DEVICE = 1 };
+int onmt_set_validation(onmt_model* model, int mode);
+int onmt_device_status(onmt_model* model, int* code);
 
 /* ---- Beam search (Section 2 item (d); Section 4.2; Section 4.1 batched GPU translator) --------------
  * Translates B sentences with beam width K = params->beam (1 <= K <= 16, K <= tgt_vocab). Per sentence:
@@ -184,6 +204,16 @@ int onmt_beam_search(onmt_model* model, const int32_t* src, const int32_t* len, 
                      const onmt_search_params* params, void* ws, size_t ws_bytes, int32_t* out_tok,
                      int32_t* out_len, double* out_raw, double* out_norm, float* out_tok_logp,
                      int32_t* out_align, const onmt_trace* trace, void* stream);
+
+/* ---- Unknown-word replacement (Section 4.2 OOV handling, after Luong et al. 2015b) -------------------
+ * For the outputs of onmt_beam_search run with out_align: out_src[b, t] = src[b, out_align[b, t]] for every
+ * output token t < out_len[b] that is the model's unk_id (the source word at the position the UNK's step
+ * attended to most), -1 for every other entry. A bilingual dictionary would map that source id to a target
+ * word; without one the caller copies it. src [B, S_max] as given to the search; out_tok, out_align,
+ * out_src [B, max_len]; all device pointers. Asynchronous on the stream; alignments outside [0, S_max) give
+ * -1. */
+int onmt_replace_unk(onmt_model* model, const int32_t* src, int B, int S_max, const int32_t* out_tok,
+                     const int32_t* out_len, const int32_t* out_align, int max_len, int32_t* out_src, void* stream);
 
 /* ---- Teacher-forced scoring: the training objective's per-token terms (Section 2: the model is trained
  * to minimise the negative log-likelihood of the corpus; the same conditional factorisation) ----------

@@ -5,7 +5,9 @@ CPU-baseline leg of ``bench.py`` may import or run this module. The product
 path (the HIP library and its Python binding) never calls it and shares no code
 with it; the two meet only in the seeded inputs of the ``workloads`` package.
 
-Everything is float64 NumPy, written for a reader holding the OpenNMT paper
+Everything is float64 NumPy (model_from(..., dtype=np.float32) gives an fp32 copy whose products run in
+single precision, used only to time the CPU baseline; beam scores stay fp64), written for a reader
+holding the OpenNMT paper
 (Klein et al., arXiv 1805.11462). The paper names the pieces but prints no
 equations, so the standard published forms of the cited works are written out
 here; every place where the paper is silent carries its reading (R1..R16, the
@@ -106,10 +108,11 @@ class Model:
         return self.hidden // 2 if self.bidirectional else self.hidden
 
 
-def model_from(workload, weights) -> Model:
+def model_from(workload, weights, dtype=F64) -> Model:
+    """The oracle's model; activations follow the weights' dtype (fp64 unless asked otherwise)."""
     return Model(workload.enc_layers, workload.dec_layers, workload.bidirectional,
                  workload.emb, workload.hidden, workload.src_vocab, workload.tgt_vocab,
-                 {k: np.asarray(v, dtype=F64) for k, v in weights.items()}, workload.attn)
+                 {k: np.asarray(v, dtype=dtype) for k, v in weights.items()}, workload.attn)
 
 
 # --------------------------------------------------------------------------
@@ -155,9 +158,9 @@ def run_direction(W, b, x, real, reverse):
     """One LSTM direction over [B, S, in] with packed padding (R2, R4)."""
     B, S, _ = x.shape
     Hl = W.shape[0] // 4
-    h = np.zeros((B, Hl), F64)
-    c = np.zeros((B, Hl), F64)
-    out = np.zeros((B, S, Hl), F64)
+    h = np.zeros((B, Hl), x.dtype)
+    c = np.zeros((B, Hl), x.dtype)
+    out = np.zeros((B, S, Hl), x.dtype)
     steps = range(S - 1, -1, -1) if reverse else range(S)
     for s in steps:
         h_new, c_new = lstm_cell(W, b, x[:, s], h, c)
@@ -209,7 +212,7 @@ def init_state(m: Model, enc: Encoded, K: int) -> State:
     rep = lambda a: np.repeat(a, K, axis=0)
     N = enc.memory.shape[0] * K
     return State([rep(h) for h in enc.final_h], [rep(c) for c in enc.final_c],
-                 np.zeros((N, m.hidden), F64))
+                 np.zeros((N, m.hidden), enc.memory.dtype))
 
 
 def attention_scores(m: Model, q, memory):
@@ -300,7 +303,7 @@ class Result:
     norm: np.ndarray        # [B] raw / lp(len)
     logps: list             # per-token log-probs of the 1-best
     steps: np.ndarray       # [B] step after which the sentence was done
-    trace: dict = None      # per step: chosen (slot, token, cand) by rank
+    trace: dict = None      # per step: chosen (slot, token, cand) by rank, and each sentence's margin
     align: list = None      # per token of the 1-best: argmax source position of its step's attention
     margin: np.ndarray = None   # [B] smallest decision margin of the sentence's run (see beam_search)
 
@@ -340,7 +343,10 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
     step (which hypotheses survive; the order inside the chosen K only renumbers slots), the stop rule's
     best finished score against the best live score / lp(max_len), and the best finished entry against the
     second best. Another implementation whose scores differ from these by less than half the margin makes
-    every decision the same way, so its output tokens must be identical (R16).
+    every decision the same way, so its output tokens must be identical (R16). With ``record`` the trace
+    also holds, per step, each sentence's margin of that step's selection and stop decisions (inf once
+    the sentence is done): the other implementation's choices must be the same at every step before the
+    first one whose margin is within its tolerance.
     """
     src = np.asarray(src)
     lens = np.asarray(lens)
@@ -360,7 +366,7 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
     best = [None] * B              # (norm, raw, Hyp)
     pool_norms = [[] for _ in range(B)]
     margin = np.full(B, np.inf)
-    trace = {"slot": [], "tok": [], "cand": []} if record else None
+    trace = {"slot": [], "tok": [], "cand": [], "margin": []} if record else None
     lp_max = length_penalty(max_len, alpha)
     for t in range(1, max_len + 1):
         st_new, logp, attn = decode_step(m, enc, st, tok, row_sentence)
@@ -370,6 +376,7 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
             t_slot = np.full((B, K), -1, np.int64)
             t_tok = np.full((B, K), -1, np.int64)
             t_cand = np.full((B, K), -np.inf)
+            t_margin = np.full(B, np.inf)
         for b in range(B):
             if done[b]:
                 continue
@@ -384,8 +391,9 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
             flat = cand.ravel()
             order = np.argsort(-flat, kind="stable")            # ties: smaller flat index first
             chosen = [i for i in order[:K] if np.isfinite(flat[i])]
+            step_margin = np.inf
             if order.size > K and np.isfinite(flat[order[K]]):      # the selection boundary
-                margin[b] = min(margin[b], flat[order[K - 1]] - flat[order[K]])
+                step_margin = flat[order[K - 1]] - flat[order[K]]
             new_scores = np.full(K, -np.inf)
             new_hyps = [Hyp([], [], np.zeros(S, F64), []) for _ in range(K)]
             j = 0
@@ -412,7 +420,10 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
             hyps[b] = new_hyps
             live = new_scores[np.isfinite(new_scores)]
             if stop_rule and best[b] is not None and live.size and t < max_len:
-                margin[b] = min(margin[b], abs(best[b][0] - live.max() / lp_max))
+                step_margin = min(step_margin, abs(best[b][0] - live.max() / lp_max))
+            margin[b] = min(margin[b], step_margin)
+            if record:
+                t_margin[b] = step_margin
             if (t == max_len or live.size == 0
                     or (stop_rule and best[b] is not None and best[b][0] >= live.max() / lp_max)):
                 done[b] = True
@@ -421,6 +432,7 @@ def beam_search(m: Model, src, lens, K, max_len, alpha=0.0, stop_rule=True, reco
             trace["slot"].append(t_slot)
             trace["tok"].append(t_tok)
             trace["cand"].append(t_cand)
+            trace["margin"].append(t_margin)
         st = st_new.take(parent)
         tok = new_tok
         if done.all():
@@ -539,6 +551,56 @@ def brute_force(m: Model, src_row, n_src, max_len, alpha=0.0, beta=0.0, banned=(
 # --------------------------------------------------------------------------
 # Replay of a recorded search (parity protocol for near-ties, R16)
 # --------------------------------------------------------------------------
+
+def chosen_hypotheses(trace, b, t_end, K):
+    """The token sequences chosen at each step 1..t_end of sentence b in a record by rank (slot, tok):
+    a list (per step) of sets of tuples. Slots are numbered as R9 fills them (live choices in rank order)."""
+    live = {0: ()}
+    out = []
+    for t in range(1, t_end + 1):
+        slot = np.asarray(trace["slot"][t - 1][b])
+        tok = np.asarray(trace["tok"][t - 1][b])
+        step, nxt = set(), {}
+        for r in range(K):
+            k = int(slot[r])
+            if k < 0 or k not in live:
+                continue
+            seq = live[k] + (int(tok[r]),)
+            step.add(seq)
+            if int(tok[r]) != EOS_ID:
+                nxt[len(nxt)] = seq
+        out.append(step)
+        live = nxt
+    return out
+
+
+def prefix_agreement(oracle_trace, other_trace, sentences, K, tol):
+    """Per-step free-run parity (R16): for each sentence, the other implementation must choose the same
+    hypotheses as the oracle at every step before the first step whose recorded oracle margin is within
+    ``tol`` (ties and near-ties may go either way from there on). Returns (violations, number of steps
+    compared per sentence)."""
+    bad, n_cmp = [], {}
+    T = len(oracle_trace["slot"])
+    for b in sentences:
+        t_stop = 0
+        while t_stop < T and np.asarray(oracle_trace["slot"][t_stop][b])[0] >= 0 \
+                and oracle_trace["margin"][t_stop][b] > tol:
+            t_stop += 1
+        n_cmp[b] = t_stop
+        if t_stop == 0:
+            continue
+        want = chosen_hypotheses(oracle_trace, b, t_stop, K)
+        got = chosen_hypotheses(other_trace, b, min(t_stop, len(other_trace["slot"])), K)
+        for t, (a, g) in enumerate(zip(want, got), start=1):
+            if a != g:
+                bad.append(f"b{b} t{t}: chose {len(g - a)} hypotheses the oracle did not, although every "
+                           f"oracle margin up to this step exceeds {tol:.3g}")
+                break
+        else:
+            if len(got) < len(want):
+                bad.append(f"b{b}: record ends at step {len(got)}, the oracle's agrees to step {t_stop}")
+    return bad, n_cmp
+
 
 def replay_verify(m: Model, src, lens, K, max_len, alpha, trace, tau, sentences=None, steps=None, result=None,
                   beta=0.0):

@@ -11,6 +11,7 @@ from ctypes import POINTER, c_char_p, c_double, c_int, c_int64, c_size_t, c_void
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libonmt.so")
 
 ONMT_OK, ONMT_EINVAL, ONMT_ESIZE, ONMT_EDEVICE, ONMT_EUNSUPPORTED = 0, -1, -2, -3, -4
+ONMT_VALIDATE_HOST, ONMT_VALIDATE_DEVICE = 0, 1
 ERROR_NAMES = {ONMT_EINVAL: "EINVAL", ONMT_ESIZE: "ESIZE", ONMT_EDEVICE: "EDEVICE", ONMT_EUNSUPPORTED: "EUNSUPPORTED"}
 
 
@@ -49,9 +50,13 @@ SIGNATURES = {
     "onmt_beam_search": (c_int, [c_void_p, c_void_p, c_void_p, c_int, c_int, POINTER(OnmtSearchParams), c_void_p,
                                  c_size_t, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                  POINTER(OnmtTrace), c_void_p]),
+    "onmt_replace_unk": (c_int, [c_void_p, c_void_p, c_int, c_int, c_void_p, c_void_p, c_void_p, c_int, c_void_p,
+                                 c_void_p]),
     "onmt_score_ws_bytes": (c_size_t, [c_void_p, c_int, c_int, c_int]),
     "onmt_score": (c_int, [c_void_p, c_void_p, c_void_p, c_int, c_int, c_void_p, c_void_p, c_int, c_void_p, c_size_t,
                            c_void_p, c_void_p, c_void_p]),
+    "onmt_set_validation": (c_int, [c_void_p, c_int]),
+    "onmt_device_status": (c_int, [c_void_p, POINTER(c_int)]),
     "onmt_profile_enable": (c_int, [c_void_p, c_int]),
     "onmt_profile_read": (c_int, [c_void_p, POINTER(c_int), POINTER(c_double), c_int]),
 }

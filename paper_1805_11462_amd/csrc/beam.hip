@@ -533,6 +533,103 @@ hipError_t backtrack(const BeamParams& p, int32_t* out_tok, int32_t* out_len, do
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ unknown-word replacement
+// out[b, t] = src[b, align[b, t]] where the output token tok[b, t] (t < len[b]) is the UNK id and its
+// alignment is a position of the source row, else -1.
+__global__ void k_replace_unk(const int32_t* __restrict__ src, int B, int S, const int32_t* __restrict__ tok,
+                              const int32_t* __restrict__ len, const int32_t* __restrict__ align, int T, int unk,
+                              int32_t* __restrict__ out) {
+  const size_t n = (size_t)B * T;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const int b = (int)(i / T), t = (int)(i % T);
+    int v = -1;
+    if (t < len[b] && tok[i] == unk) {
+      const int a = align[i];
+      if (a >= 0 && a < S) v = src[(size_t)b * S + a];
+    }
+    out[i] = v;
+  }
+}
+
+hipError_t replace_unk(const int32_t* src, int B, int S, const int32_t* tok, const int32_t* len, const int32_t* align,
+                       int T, int unk, int32_t* out, hipStream_t st) {
+  const size_t n = (size_t)B * T;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_replace_unk, dim3((unsigned)blocks), dim3(256), 0, st, src, B, S, tok, len, align, T, unk, out);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ input validation on the device
+// The checks the host otherwise makes after copying the inputs over (one stream sync per call), done by a
+// kernel instead: invalid values are replaced by safe ones (length clamped to [1, S], ids by 0, a parent
+// by the row itself), so every later kernel stays in bounds, and the first kind of violation seen is
+// recorded in *err (a word of host-visible memory the host reads once the stream is synchronized). Several
+// threads may store different codes; any nonzero code reports the failure.
+__global__ void k_sanitize_src(const int32_t* __restrict__ src, const int32_t* __restrict__ len, int B, int S, int V,
+                               int32_t* __restrict__ clean, int32_t* __restrict__ lens, int32_t* __restrict__ rowmap,
+                               int32_t* err) {
+  const size_t n = (size_t)B * S;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const int b = (int)(i / S), s = (int)(i % S);
+    const int l = len[b];
+    const int lc = l < 1 ? 1 : (l > S ? S : l);
+    if (s == 0) {
+      lens[b] = lc;
+      if (l != lc) *err = kErrLength;
+    }
+    int id = 0;
+    if (s < lc) {
+      id = src[i];
+      if (id < 0 || id >= V) {
+        *err = kErrSourceId;
+        id = 0;
+      }
+    }
+    clean[i] = id;
+    rowmap[(size_t)s * B + b] = (int32_t)i;
+  }
+}
+
+__global__ void k_sanitize_step(const int32_t* __restrict__ tok, const int32_t* __restrict__ parent, int N, int V,
+                                int32_t* __restrict__ tok_out, int32_t* __restrict__ par_out, int32_t* err) {
+  for (int r = blockIdx.x * blockDim.x + threadIdx.x; r < N; r += gridDim.x * blockDim.x) {
+    int t = tok[r];
+    if (t < 0 || t >= V) {
+      *err = kErrToken;
+      t = 0;
+    }
+    tok_out[r] = t;
+    if (par_out) {
+      int p = parent[r];
+      if (p < 0 || p >= N) {
+        *err = kErrParent;
+        p = r;
+      }
+      par_out[r] = p;
+    }
+  }
+}
+
+hipError_t sanitize_src(const int32_t* src, const int32_t* len, int B, int S, int V, int32_t* clean, int32_t* lens,
+                        int32_t* rowmap, int32_t* err, hipStream_t st) {
+  const size_t n = (size_t)B * S;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_sanitize_src, dim3((unsigned)blocks), dim3(256), 0, st, src, len, B, S, V, clean, lens, rowmap,
+                     err);
+  return hipGetLastError();
+}
+
+hipError_t sanitize_step(const int32_t* tok, const int32_t* parent, int N, int V, int32_t* tok_out, int32_t* par_out,
+                         int32_t* err, hipStream_t st) {
+  int blocks = (N + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_sanitize_step, dim3(blocks), dim3(256), 0, st, tok, parent, N, V, tok_out,
+                     parent ? par_out : nullptr, err);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ layout helpers
 __global__ void k_replicate_rows(const float* src, int ld_src, int rows, int K, float* dst, int ld_dst, int ncols) {
   const int r = blockIdx.y;                 // destination row

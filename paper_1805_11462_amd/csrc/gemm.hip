@@ -386,48 +386,48 @@ constexpr int dma_lds() {
   return kLstmStages * stg > C::CT ? kLstmStages * stg : C::CT;
 }
 
-// One output tile of an LSTM GEMM (block bid of nblocks) with the gate/cell epilogue.
-template <class T, class C, int NSEG, bool DMA = false>
-__device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p, int nm, int nblocks, int bid,
-                                 char* smem) {
-  const int L = xcd_remap(bid, nblocks);
-  const int m0 = (L % nm) * C::BM, n0 = (L / nm) * C::BN;
-  constexpr int UPT = C::BN / 4;                      // units per tile
-  constexpr int EPT = (C::BM * UPT + C::NT - 1) / C::NT;   // (row, unit) elements per thread
-  // the precomputed input-projection terms of this thread's elements are loaded before the main loop,
-  // so that their latency (table rows gathered by token id) hides behind it
-  float gxv[EPT][4];
+// The precomputed input-projection terms (gx) of this thread's (row, unit) elements of an LSTM output tile,
+// loaded before the main loop so that their latency (table rows gathered by token id) hides behind it.
+template <class C>
+struct LstmGx {
+  static constexpr int UPT = C::BN / 4;                          // units per tile
+  static constexpr int EPT = (C::BM * UPT + C::NT - 1) / C::NT;  // (row, unit) elements per thread
+  float v[EPT][4];
+  __device__ void load(const LstmParams& p, int M, int m0, int n0) {
 #pragma unroll
-  for (int i = 0; i < EPT; ++i) {
-    const int e = threadIdx.x + i * C::NT;
-    const int r = e / UPT, uu = e % UPT;
-    const int row = m0 + r, unit = n0 / 4 + uu;
-    const bool ok = p.gx && e < C::BM * UPT && row < a.M && unit < p.H;
-    const int grow = !ok ? 0 : (p.gx_idx ? min((unsigned)p.gx_idx[row], (unsigned)p.gx_rows - 1u) : row * p.gx_S + p.gx_s);
-    const int cbase = (uu / kUnitGroup) * (4 * kUnitGroup) + (uu % kUnitGroup);
+    for (int i = 0; i < EPT; ++i) {
+      const int e = threadIdx.x + i * C::NT;
+      const int r = e / UPT, uu = e % UPT;
+      const int row = m0 + r, unit = n0 / 4 + uu;
+      const bool ok = p.gx && e < C::BM * UPT && row < M && unit < p.H;
+      const int grow = !ok ? 0 : (p.gx_idx ? min((unsigned)p.gx_idx[row], (unsigned)p.gx_rows - 1u) : row * p.gx_S + p.gx_s);
+      const int cbase = (uu / kUnitGroup) * (4 * kUnitGroup) + (uu % kUnitGroup);
 #pragma unroll
-    for (int gt = 0; gt < 4; ++gt)
-      gxv[i][gt] = ok ? p.gx[(size_t)grow * p.ld_gx + p.gx_col0 + n0 + cbase + gt * kUnitGroup] : 0.f;
+      for (int gt = 0; gt < 4; ++gt)
+        v[i][gt] = ok ? p.gx[(size_t)grow * p.ld_gx + p.gx_col0 + n0 + cbase + gt * kUnitGroup] : 0.f;
+    }
   }
-  if constexpr (DMA)
-    gemm_tile_dma<C, NSEG>(a, b, m0, n0, smem);
-  else
-    gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
-  const float* Ct = (const float*)smem;
+};
+
+// Gate nonlinearities and cell update over an output tile: acc(r, col) gives the tile's product at tile row
+// r and (gate-blocked) tile column col; bias, gx, the previous cell state (through c_idx) complete z.
+template <class C, class Acc>
+__device__ inline void lstm_epilogue(Acc acc, const LstmParams& p, int M, int m0, int n0, const LstmGx<C>& gx) {
+  using G = LstmGx<C>;
 #pragma unroll
-  for (int i = 0; i < EPT; ++i) {
+  for (int i = 0; i < G::EPT; ++i) {
     const int e = threadIdx.x + i * C::NT;
-    if (e >= C::BM * UPT) break;
-    const int r = e / UPT, uu = e % UPT;
+    if (e >= C::BM * G::UPT) break;
+    const int r = e / G::UPT, uu = e % G::UPT;
     const int row = m0 + r;
     const int unit = n0 / 4 + uu;
-    if (row >= a.M || unit >= p.H) continue;
+    if (row >= M || unit >= p.H) continue;
     const int cbase = (uu / kUnitGroup) * (4 * kUnitGroup) + (uu % kUnitGroup);
     float z[4];
 #pragma unroll
     for (int gt = 0; gt < 4; ++gt) {
       const int col = cbase + gt * kUnitGroup;
-      z[gt] = ctile<C>(Ct, r, col) + (p.bias ? p.bias[n0 + col] : 0.f) + gxv[i][gt];
+      z[gt] = acc(r, col) + (p.bias ? p.bias[n0 + col] : 0.f) + gx.v[i][gt];
     }
     const int crow = p.c_idx ? p.c_idx[row] : row;
     const float c_prev = p.c_in ? p.c_in[(size_t)crow * p.ld_c + unit] : 0.f;
@@ -452,6 +452,22 @@ __device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p
     }
     if (p.y_out) p.y_out[(size_t)(row * p.y_S + p.y_s) * p.ld_y + p.y_col0 + unit] = y;
   }
+}
+
+// One output tile of an LSTM GEMM (block bid of nblocks) with the gate/cell epilogue.
+template <class T, class C, int NSEG, bool DMA = false>
+__device__ inline void lstm_tile(const AOp& a, const BOp& b, const LstmParams& p, int nm, int nblocks, int bid,
+                                 char* smem) {
+  const int L = xcd_remap(bid, nblocks);
+  const int m0 = (L % nm) * C::BM, n0 = (L / nm) * C::BN;
+  LstmGx<C> gx;
+  gx.load(p, a.M, m0, n0);
+  if constexpr (DMA)
+    gemm_tile_dma<C, NSEG>(a, b, m0, n0, smem);
+  else
+    gemm_tile<T, C, NSEG>(a, b, m0, n0, smem);
+  const float* Ct = (const float*)smem;
+  lstm_epilogue<C>([&](int r, int col) { return ctile<C>(Ct, r, col); }, p, a.M, m0, n0, gx);
 }
 
 template <class T, class C, int NSEG, bool DMA = false>

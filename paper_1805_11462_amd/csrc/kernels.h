@@ -119,6 +119,7 @@ hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const Lstm
 hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st);
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st);
 
+
 // bf16 generator operand already split into bf16 hi and lo planes (A = hi + lo), row-major [M, ld] each
 // with zeros in the K padding (columns width .. kpad - 1).
 struct GenSplitA {
@@ -209,6 +210,21 @@ hipError_t beam_init(const BeamParams& p, int bos, hipStream_t st);
 hipError_t beam_step(const BeamParams& p, const GenPartials& gp, int t, hipStream_t st);
 hipError_t backtrack(const BeamParams& p, int32_t* out_tok, int32_t* out_len, double* out_raw, double* out_norm,
                      float* out_tok_logp, int32_t* out_align, hipStream_t st);
+
+// out [B, T] = the source id at the aligned position of every UNK output token (t < len[b]), -1 elsewhere.
+hipError_t replace_unk(const int32_t* src, int B, int S, const int32_t* tok, const int32_t* len, const int32_t* align,
+                       int T, int unk, int32_t* out, hipStream_t st);
+
+// Device-side input validation (see beam.hip): error kinds recorded in the host-visible word.
+enum { kErrLength = 1, kErrSourceId = 2, kErrToken = 3, kErrParent = 4 };
+// clean [B, S] = src with ids past each length (and invalid ids) set to 0; lens [B] = len clamped to [1, S];
+// rowmap [S, B] = b * S + s.
+hipError_t sanitize_src(const int32_t* src, const int32_t* len, int B, int S, int V, int32_t* clean, int32_t* lens,
+                        int32_t* rowmap, int32_t* err, hipStream_t st);
+// tok_out [N] = tok with invalid ids set to 0; par_out [N] (when parent != NULL) = parent with rows outside
+// [0, N) replaced by the row itself.
+hipError_t sanitize_step(const int32_t* tok, const int32_t* parent, int N, int V, int32_t* tok_out, int32_t* par_out,
+                         int32_t* err, hipStream_t st);
 
 hipError_t replicate_rows(const float* src, int ld_src, int rows, int K, float* dst, int ld_dst, int ncols,
                           hipStream_t st);

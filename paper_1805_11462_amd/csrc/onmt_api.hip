@@ -109,6 +109,22 @@ bool dims_of(const onmt_config* c, Dims* d) {
   return true;
 }
 
+// The GEMMs address their operands through buffer descriptors, whose byte counts and row offsets are
+// 32-bit and which treat offsets from 2 GiB on as "no row" (zeros): every operand read that way must be
+// smaller than 2 GiB. These checks run before anything is enqueued.
+constexpr uint64_t kDescLimit = 1ull << 31;
+size_t model_layout(const onmt_config* c, onmt_model* m, std::vector<uint64_t>* mats = nullptr);
+
+int check_model_limits(const onmt_config* c) {
+  std::vector<uint64_t> mats;
+  model_layout(c, nullptr, &mats);   // embeddings, packed LSTM / attention / generator matrices
+  for (uint64_t b : mats)
+    if (b >= kDescLimit)
+      return fail(ONMT_EUNSUPPORTED, "a packed weight matrix or embedding table needs %llu bytes (limit 2 GiB)",
+                  (unsigned long long)b);
+  return ONMT_OK;
+}
+
 int check_config(const onmt_config* c) {
   if (!c) return fail(ONMT_EINVAL, "config is NULL");
   if (c->enc_layers < 1 || c->dec_layers < 1) return fail(ONMT_EINVAL, "layers must be >= 1");
@@ -130,7 +146,7 @@ int check_config(const onmt_config* c) {
   const int ids[4] = {c->pad_id, c->unk_id, c->bos_id, c->eos_id};
   for (int i = 0; i < 4; ++i)
     if (ids[i] < 0 || ids[i] >= c->tgt_vocab) return fail(ONMT_EINVAL, "special ids must be in [0, tgt_vocab)");
-  return ONMT_OK;
+  return check_model_limits(c);
 }
 
 struct WeightSpec {
@@ -208,12 +224,17 @@ struct onmt_model {
   // finish checks of the beam search: two pinned host words the done count is copied into, one event each
   int32_t* done_host = nullptr;
   hipEvent_t done_ev[2] = {nullptr, nullptr};
+  // input validation: ONMT_VALIDATE_HOST or ONMT_VALIDATE_DEVICE; the device checks report into err_host
+  // (pinned host memory, written by the validation kernels, read by onmt_device_status)
+  int validation = ONMT_VALIDATE_HOST;
+  int32_t* err_host = nullptr;
 };
 
 namespace {
 
-// Model buffer layout (offsets only); fills m's offsets when m != nullptr.
-size_t model_layout(const onmt_config* c, onmt_model* m) {
+// Model buffer layout (offsets only); fills m's offsets when m != nullptr, and the byte size of every
+// matrix the GEMMs read through buffer descriptors into *mats when given.
+size_t model_layout(const onmt_config* c, onmt_model* m, std::vector<uint64_t>* mats) {
   Dims d;
   dims_of(c, &d);
   Carver cv;
@@ -224,6 +245,7 @@ size_t model_layout(const onmt_config* c, onmt_model* m) {
     p.Np = Np;
     p.Kp = Kp;
     cv.off += (size_t)Np * Kp * d.esz;
+    if (mats) mats->push_back((uint64_t)Np * Kp * d.esz);
     return p;
   };
   auto vec = [&](size_t n) {
@@ -464,7 +486,12 @@ int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, 
     e = gemm_store(d.bf16, kShapeWide, a, bop(m->dec_w[0]), sp, st);
   }
   if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e == hipSuccess) {
+    e = hipHostMalloc((void**)&m->err_host, sizeof(int32_t), hipHostMallocDefault);
+    if (e == hipSuccess) *m->err_host = 0;
+  }
   if (e != hipSuccess) {
+    if (m->err_host) hipHostFree(m->err_host);
     delete m;
     return fail(ONMT_EDEVICE, "weight upload failed: %s", hipGetErrorString(e));
   }
@@ -478,6 +505,7 @@ int onmt_model_destroy(onmt_model* m) {
   for (auto e : m->done_ev)
     if (e) hipEventDestroy(e);
   if (m->done_host) hipHostFree(m->done_host);
+  if (m->err_host) hipHostFree(m->err_host);
   delete m;
   return ONMT_OK;
 }
@@ -564,6 +592,8 @@ struct StepWs {
   float* lse;      // [N]
   int32_t* align;  // [N] attention argmax
   float* pfmax;    // [N, ntiles] largest allowed logit per tile (hypothesis filters)
+  int32_t* tok_s;  // [N] previous tokens and parents checked on the device (device validation)
+  int32_t* par_s;
   int ntiles;
 };
 
@@ -585,6 +615,8 @@ size_t step_layout(const Dims& d, int B, int S, int K, char* base, StepWs* w) {
   t.lse = c.take<float>(N);
   t.align = c.take<int32_t>(N);
   t.pfmax = c.take<float>(N * t.ntiles);
+  t.tok_s = c.take<int32_t>(N);
+  t.par_s = c.take<int32_t>(N);
   if (w) *w = t;
   return align_up(c.off);
 }
@@ -686,6 +718,26 @@ size_t score_layout(const Dims& d, int B, int S, int T, char* base, ScoreWs* w) 
   return align_up(c.off);
 }
 
+// Workspace operands that the GEMMs read through buffer descriptors (see kDescLimit): the encoder's
+// memory, layer outputs and keys [B * S, Hm or H], the decoder's state rows and attentional vectors
+// [B * K, Hm or H] (and their bf16 planes), and scoring's attentional vectors of all steps [T * B, H].
+int check_ws_limits(const Dims& d, long long B, long long S, long long K, long long T) {
+  const long long w = d.Hm > d.H ? d.Hm : d.H;
+  const uint64_t enc = (uint64_t)(B * S) * (uint64_t)ceil_to((int)w, kSegK) * 4;
+  const uint64_t dec = (uint64_t)(B * K) * (uint64_t)ceil_to((int)w, kSegK) * 4;
+  const uint64_t sco = (uint64_t)(B * T) * (uint64_t)ceil_to(d.H, kSegK) * 4;
+  if (enc >= kDescLimit)
+    return fail(ONMT_EUNSUPPORTED, "B * S_max = %lld source positions need a %llu-byte memory bank (limit 2 GiB)",
+                B * S, (unsigned long long)enc);
+  if (dec >= kDescLimit)
+    return fail(ONMT_EUNSUPPORTED, "B * beam = %lld hypothesis rows need %llu-byte state operands (limit 2 GiB)",
+                B * K, (unsigned long long)dec);
+  if (sco >= kDescLimit)
+    return fail(ONMT_EUNSUPPORTED, "B * T_max = %lld scored rows need %llu bytes of attentional vectors (limit 2 GiB)",
+                B * T, (unsigned long long)sco);
+  return ONMT_OK;
+}
+
 // Small-M GEMMs: the 16-row split-K tile unless the 32-row tile already gives this many workgroups
 // (measured on the decoder layers: more, smaller workgroups win while M is a few hundred rows).
 #ifndef ONMT_SMALL_M_TILES
@@ -739,13 +791,33 @@ int check_len_src(const onmt_model* m, const int32_t* src, const int32_t* len, i
   return ONMT_OK;
 }
 
+// Source ids and lengths, checked either on the host (ONMT_VALIDATE_HOST: copied over, one stream sync; the
+// longest length bounds the encoder's steps) or on the device (ONMT_VALIDATE_DEVICE: a kernel writes the
+// checked copies and records violations; the encoder then steps over all S_max positions, which the packed
+// padding leaves unchanged past each sentence's length). On return w.src, w.rowmap and (device mode)
+// w.lens hold the checked inputs; *lens_src is what encode_compute copies into w.lens (nullptr: in place).
+int checked_source(onmt_model* m, const int32_t* src, const int32_t* len, int B, int S, const EncWs& w, hipStream_t st,
+                   int* max_len, const int32_t** lens_src) {
+  if (m->validation == ONMT_VALIDATE_DEVICE) {
+    if (!src || !len) return fail(ONMT_EINVAL, "src/len is NULL");
+    if ((long long)B * S > (1LL << 28)) return fail(ONMT_EUNSUPPORTED, "B * S_max too large");
+    HIP_TRY(sanitize_src(src, len, B, S, m->cfg.src_vocab, w.src, w.lens, w.rowmap, m->err_host, st));
+    *max_len = S;
+    *lens_src = nullptr;
+    return ONMT_OK;
+  }
+  *lens_src = len;
+  return check_len_src(m, src, len, B, S, st, max_len, w.src, w.rowmap);
+}
+
 // Encoder compute on validated inputs (Section 2 encoder RNN; Tables 3-4 bidirectional; readings R2-R5).
+// len == nullptr: the lengths are already in w.lens (checked on the device).
 int encode_compute(onmt_model* m, const int32_t* src, const int32_t* len, int B, int S, int max_len, const EncWs& w,
                    hipStream_t st) {
   const Dims& d = m->d;
   const int BS = B * S;
   (void)src;   // the validated, pad-cleaned ids are already in w.src
-  HIP_TRY(hipMemcpyAsync(w.lens, len, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, st));
+  if (len) HIP_TRY(hipMemcpyAsync(w.lens, len, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, st));
   HIP_TRY(fill_f32(w.memory, (size_t)BS * d.Hm, 0.f, st));
   const int gxw = d.ndir * 4 * d.Hd_pad;
   const size_t SB = (size_t)B * d.Hd;       // one state slot
@@ -954,7 +1026,8 @@ struct StepExtras {
 
 int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const State& in, const State& out,
                    const int32_t* prev_tok, const int32_t* parent, int mode, float* logp, int32_t* ids, float* lse,
-                   float* attn, const StepWs& sw, hipStream_t st, const StepExtras& ex = StepExtras{}) {
+                   float* attn, const StepWs& sw, hipStream_t st, const StepExtras& ex = StepExtras{},
+                   bool timing = true) {
   const Dims& d = m->d;
   const int N = B * K;
   const size_t LH = (size_t)N * d.H;
@@ -1056,12 +1129,12 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     gp.unk_id = ex.unk_id;
     gp.max_unk = ex.max_unk;
     gp.pfmax = ex.pfmax;
-    time_begin(m, st);
+    if (timing) time_begin(m, st);
     if (d.bf16)
       HIP_TRY(gemm_gen_split(GenSplitA{out.feed_hi, out.feed_lo, N, d.pad(d.H), d.pad(d.H)}, bop(m->W_s), gp, st));
     else
       HIP_TRY(gemm_gen(0, a, bop(m->W_s), gp, st));
-    time_end(m, st);
+    if (timing) time_end(m, st);
   }
   if (mode == 2) return ONMT_OK;
   float* lse_out = lse ? lse : sw.lse;
@@ -1098,13 +1171,16 @@ int onmt_encode(onmt_model* m, const int32_t* src, const int32_t* len, int B, in
   if (!ws) return fail(ONMT_EINVAL, "enc_ws is NULL");
   hipStream_t st = (hipStream_t)stream;
   if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
+  int rc = check_ws_limits(m->d, B, S, 1, 0);
+  if (rc) return rc;
   if (ws_bytes < enc_layout(m->d, B, S, nullptr, nullptr)) return fail(ONMT_ESIZE, "encoder workspace too small");
   EncWs w;
   enc_layout(m->d, B, S, (char*)ws, &w);
   int mx = 0;
-  int rc = check_len_src(m, src, len, B, S, st, &mx, w.src, w.rowmap);
+  const int32_t* lsrc = nullptr;
+  rc = checked_source(m, src, len, B, S, w, st, &mx, &lsrc);
   if (rc) return rc;
-  return encode_compute(m, src, len, B, S, mx, w, st);
+  return encode_compute(m, src, lsrc, B, S, mx, w, st);
 }
 
 size_t onmt_state_bytes(const onmt_model* m, int N) {
@@ -1120,6 +1196,8 @@ size_t onmt_step_ws_bytes(const onmt_model* m, int B, int S, int K) {
 int onmt_decode_init(onmt_model* m, const void* enc_ws, int B, int S, int K, void* state_out, void* stream) {
   if (!m || !enc_ws || !state_out) return fail(ONMT_EINVAL, "NULL argument");
   if (B < 1 || S < 1 || K < 1) return fail(ONMT_EINVAL, "B, S_max, K must be >= 1");
+  int rc = check_ws_limits(m->d, B, S, K, 0);
+  if (rc) return rc;
   EncWs w;
   enc_layout(m->d, B, S, (char*)enc_ws, &w);
   State s;
@@ -1135,32 +1213,61 @@ int onmt_decode_step(onmt_model* m, const void* enc_ws, int B, int S, int K, con
   if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
   int rc = check_beam(m, S, K);
   if (rc) return rc;
+  if ((rc = check_ws_limits(m->d, B, S, K, 0))) return rc;
   if (mode != 0 && mode != 1) return fail(ONMT_EINVAL, "mode must be 0 (full) or 1 (top-K)");
   if (mode == 1 && !ids) return fail(ONMT_EINVAL, "ids is NULL in top-K mode");
   if (step_ws_bytes < step_layout(m->d, B, S, K, nullptr, nullptr)) return fail(ONMT_ESIZE, "step workspace too small");
   hipStream_t st = (hipStream_t)stream;
   const int N = B * K;
-  std::vector<int32_t> ht(N), hp(parent ? N : 0);
-  HIP_TRY(hipMemcpyAsync(ht.data(), prev_tok, sizeof(int32_t) * N, hipMemcpyDeviceToHost, st));
-  if (parent) HIP_TRY(hipMemcpyAsync(hp.data(), parent, sizeof(int32_t) * N, hipMemcpyDeviceToHost, st));
-  HIP_TRY(hipStreamSynchronize(st));
-  for (int r = 0; r < N; ++r) {
-    if (ht[r] < 0 || ht[r] >= m->cfg.tgt_vocab) return fail(ONMT_EINVAL, "prev_tok[%d] = %d out of range", r, ht[r]);
-    if (parent && (hp[r] < 0 || hp[r] >= N)) return fail(ONMT_EINVAL, "parent[%d] = %d out of range", r, hp[r]);
+  StepWs sw;
+  step_layout(m->d, B, S, K, (char*)step_ws, &sw);
+  if (m->validation == ONMT_VALIDATE_DEVICE) {
+    HIP_TRY(sanitize_step(prev_tok, parent, N, m->cfg.tgt_vocab, sw.tok_s, sw.par_s, m->err_host, st));
+    prev_tok = sw.tok_s;
+    parent = parent ? sw.par_s : nullptr;
+  } else {
+    std::vector<int32_t> ht(N), hp(parent ? N : 0);
+    HIP_TRY(hipMemcpyAsync(ht.data(), prev_tok, sizeof(int32_t) * N, hipMemcpyDeviceToHost, st));
+    if (parent) HIP_TRY(hipMemcpyAsync(hp.data(), parent, sizeof(int32_t) * N, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    for (int r = 0; r < N; ++r) {
+      if (ht[r] < 0 || ht[r] >= m->cfg.tgt_vocab) return fail(ONMT_EINVAL, "prev_tok[%d] = %d out of range", r, ht[r]);
+      if (parent && (hp[r] < 0 || hp[r] >= N)) return fail(ONMT_EINVAL, "parent[%d] = %d out of range", r, hp[r]);
+    }
   }
   EncWs w;
   enc_layout(m->d, B, S, (char*)enc_ws, &w);
   State si, so;
   state_layout(m->d, N, (char*)state_in, &si);
   state_layout(m->d, N, (char*)state_out, &so);
-  StepWs sw;
-  step_layout(m->d, B, S, K, (char*)step_ws, &sw);
   rc = decode_compute(m, w, B, S, K, si, so, prev_tok, parent, mode, logp, ids, lse, attn, sw, st);
   if (m->prof) {
     HIP_TRY(hipStreamSynchronize(st));
     time_collect(m);
   }
   return rc;
+}
+
+int onmt_set_validation(onmt_model* m, int mode) {
+  if (!m) return fail(ONMT_EINVAL, "model is NULL");
+  if (mode != ONMT_VALIDATE_HOST && mode != ONMT_VALIDATE_DEVICE)
+    return fail(ONMT_EINVAL, "validation mode must be ONMT_VALIDATE_HOST or ONMT_VALIDATE_DEVICE");
+  m->validation = mode;
+  return ONMT_OK;
+}
+
+int onmt_device_status(onmt_model* m, int* code) {
+  if (!m || !code) return fail(ONMT_EINVAL, "NULL argument");
+  volatile int32_t* e = m->err_host;
+  const int32_t kind = *e;
+  *e = 0;
+  *code = kind ? ONMT_EINVAL : ONMT_OK;
+  if (kind) {
+    static const char* what[] = {"", "a source length outside [1, S_max]", "a source id outside [0, src_vocab)",
+                                 "a previous token outside [0, tgt_vocab)", "a parent row outside [0, B * beam)"};
+    fail(ONMT_EINVAL, "device validation found %s (replaced by a safe value)", kind >= 1 && kind <= 4 ? what[kind] : "an invalid input");
+  }
+  return ONMT_OK;
 }
 
 size_t onmt_search_ws_bytes(const onmt_model* m, int B, int S, const onmt_search_params* p) {
@@ -1187,12 +1294,14 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
   int rc = check_beam(m, S, K);
   if (rc) return rc;
+  if ((rc = check_ws_limits(m->d, B, S, K, 0))) return rc;
   if (ws_bytes < search_layout(m->d, B, S, K, T, nullptr, nullptr)) return fail(ONMT_ESIZE, "search workspace too small");
   hipStream_t st = (hipStream_t)stream;
   SearchWs w;
   search_layout(m->d, B, S, K, T, (char*)ws, &w);
   int mx = 0;
-  rc = check_len_src(m, src, len, B, S, st, &mx, w.enc.src, w.enc.rowmap);
+  const int32_t* lsrc = nullptr;
+  rc = checked_source(m, src, len, B, S, w.enc, st, &mx, &lsrc);
   if (rc) return rc;
 
   BeamParams bp = w.bp;
@@ -1209,7 +1318,7 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   bp.tr_cand = trace ? trace->cand : nullptr;
 
   GenPartials gp{w.step.pmax, w.step.psum, w.step.pval, w.step.pid, w.step.ntiles};
-  rc = encode_compute(m, src, len, B, S, mx, w.enc, st);
+  rc = encode_compute(m, src, lsrc, B, S, mx, w.enc, st);
   if (rc) return rc;
   rc = decode_init_compute(m, w.enc, B, K, w.st[0], st);
   if (rc) return rc;
@@ -1276,6 +1385,15 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
   return ONMT_OK;
 }
 
+int onmt_replace_unk(onmt_model* m, const int32_t* src, int B, int S, const int32_t* out_tok, const int32_t* out_len,
+                     const int32_t* out_align, int T, int32_t* out_src, void* stream) {
+  if (!m || !src || !out_tok || !out_len || !out_align || !out_src) return fail(ONMT_EINVAL, "NULL argument");
+  if (B < 1 || S < 1 || T < 1) return fail(ONMT_EINVAL, "B, S_max and max_len must be >= 1");
+  if ((long long)B * T > (1LL << 30) || (long long)B * S > (1LL << 30)) return fail(ONMT_EUNSUPPORTED, "batch too large");
+  HIP_TRY(replace_unk(src, B, S, out_tok, out_len, out_align, T, m->cfg.unk_id, out_src, (hipStream_t)stream));
+  return ONMT_OK;
+}
+
 size_t onmt_score_ws_bytes(const onmt_model* m, int B, int S, int T) {
   if (!m || B < 1 || S < 1 || T < 1) return 0;
   return score_layout(m->d, B, S, T, nullptr, nullptr);
@@ -1290,6 +1408,7 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
   if (T < 1 || T > 100000) return fail(ONMT_EINVAL, "T_max %d outside [1, 100000]", T);
   int rc = check_beam(m, S, 1);
   if (rc) return rc;
+  if ((rc = check_ws_limits(m->d, B, S, 1, T))) return rc;
   if (ws_bytes < score_layout(m->d, B, S, T, nullptr, nullptr)) return fail(ONMT_ESIZE, "score workspace too small");
   hipStream_t st = (hipStream_t)stream;
   ScoreWs w;

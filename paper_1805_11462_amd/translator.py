@@ -183,11 +183,16 @@ class Translator:
                                         _stream()))
         return buf
 
-    @staticmethod
-    def replace_unk(tokens, align, src_row, unk_id):
-        """Unknown-word replacement on the host (Section 4.2 OOV handling): each UNK output token takes
-        the source token at its aligned position; returns ('src', id) for copied tokens, ('tgt', id) else."""
-        return [("src", int(src_row[a])) if int(t) == unk_id else ("tgt", int(t)) for t, a in zip(tokens, align)]
+    def replace_unk(self, src, buf):
+        """Unknown-word replacement (Section 4.2 OOV handling) on the device for a search run with
+        align=True: [B, max_len] int32, the source id at the aligned position of every UNK output token,
+        -1 elsewhere (onmt_replace_unk)."""
+        B, S = src.shape
+        T = buf["tok"].shape[1]
+        out = torch.empty(B, T, dtype=torch.int32, device=self.device)
+        check(self.lib.onmt_replace_unk(self.handle, _ptr(src), B, S, _ptr(buf["tok"]), _ptr(buf["len"]),
+                                        _ptr(buf["align"]), T, _ptr(out), _stream()))
+        return out
 
     # ---------------------------------------------------------------- teacher-forced scoring
     def score_buffers(self, B, S, T):

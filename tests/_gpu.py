@@ -69,18 +69,27 @@ def check_search(s, buf, sentences, K, T, alpha, golden=None, log=None):
         assert (g_tok[b, n:] == W.PAD_ID).all()
         assert abs(g_lp[b, :n].astype(np.float64).sum() - g_raw[b]) < 1e-6 * max(1, n)
         assert abs(g_norm[b] - g_raw[b] / O.length_penalty(n, alpha)) < 1e-9 * max(1.0, abs(g_raw[b]))
-    # the oracle's own search: tokens, raw score and decision margin per sentence
+    # the oracle's own search: tokens, raw score, decision margins and per-step record per sentence
     if golden is None:
-        res = O.beam_search(s.model, s.src[sel], s.lens[sel], K, T, alpha)
+        res = O.beam_search(s.model, s.src[sel], s.lens[sel], K, T, alpha, record=True)
         o_tok = {b: res.tokens[i] for i, b in enumerate(sel)}
         o_raw = {b: res.raw[i] for i, b in enumerate(sel)}
         o_margin = {b: res.margin[i] for i, b in enumerate(sel)}
+        o_trace = res.trace
     else:
         assert (golden["src"] == s.src).all() and (golden["lens"] == s.lens).all()
         o_tok = {b: [int(x) for x in golden["tokens"][b, :int(golden["len"][b])]] for b in sel}
         o_raw = {b: golden["raw"][b] for b in sel}
         o_margin = {b: golden["margin"][b] for b in sel}
+        o_trace = {"slot": [a[sel] for a in golden["trace_slot"]], "tok": [a[sel] for a in golden["trace_tok"]],
+                   "margin": [a[sel] for a in golden["trace_margin"]]}
     say(f"oracle search ready for {len(sel)} sentences")
+    # P3 per step: the same hypotheses as the oracle at every step before its first margin within 2 tau
+    g_trace = {k: [a[sel] for a in trace[k]] for k in ("slot", "tok")}
+    bad, n_cmp = O.prefix_agreement(o_trace, g_trace, range(len(sel)), K, 2 * tau)
+    assert bad == [], [f"sentence {sel[int(x.split()[0][1:].rstrip(':'))]}: {x}" for x in bad[:10]]
+    say(f"P3 per step: choices identical over the oracle's first {int(np.median(list(n_cmp.values())))} steps "
+        f"(median; {sum(n_cmp.values())} sentence-steps) before a decision margin within 2 tau")
     # teacher-forced rescoring of every GPU 1-best, all listed sentences in one batch
     forced, _ = O.score_batch(s.model, s.src[sel], s.lens[sel], g_tok[sel], g_len[sel])
     for i, b in enumerate(sel):

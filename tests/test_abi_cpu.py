@@ -117,3 +117,30 @@ def test_library_resolves_every_kernel_it_launches():
     out = subprocess.run([nm, "-C", "--undefined-only", path], capture_output=True, text=True, check=True).stdout
     missing = [l for l in out.splitlines() if "onmt::" in l]
     assert missing == []
+
+
+@pytest.mark.parametrize("wdtype,field,ok,too_big", [
+    # E_src [src_vocab, emb]: 2^20 x 500 fp32 = 2.0e9 bytes fits, 2^20 x 512 = 2^31 does not
+    ("fp32", "src_vocab_emb", (1 << 20, 500), (1 << 20, 512)),
+    # the same table in bf16: 2^20 x 1016 fits, 2^20 x 1024 does not
+    ("bf16", "src_vocab_emb", (1 << 20, 1016), (1 << 20, 1024)),
+    # W_s [tgt_vocab, pad(hidden)]: 131072 x 3968 fp32 fits; hidden 4000 pads to 4096 columns = 2^31 bytes
+    ("fp32", "tgt_vocab_hidden", (131072, 3968), (131072, 4000)),
+])
+def test_operands_past_the_descriptor_limit_are_refused(wdtype, field, ok, too_big):
+    # buffer descriptors address at most 2 GiB: a config whose embedding table or packed weight matrix
+    # reaches that is refused up front (ONMT_EUNSUPPORTED), never silently read as zeros
+    lib = _lib.load()
+    for (a, b), want_ok in ((ok, True), (too_big, False)):
+        w = W.get("tiny")
+        kw = {"src_vocab": a, "emb": b} if field == "src_vocab_emb" else {"tgt_vocab": a, "hidden": b}
+        w = W.Workload(**{**w.as_dict(), "wdtype": wdtype, **kw})
+        cfg = cfg_of(w)
+        n = lib.onmt_num_weights(ctypes.byref(cfg))
+        if want_ok:
+            assert n > 0, lib.onmt_last_error()
+            assert lib.onmt_model_bytes(ctypes.byref(cfg)) > 0
+        else:
+            assert n == _lib.ONMT_EUNSUPPORTED
+            assert lib.onmt_model_bytes(ctypes.byref(cfg)) == 0
+            assert b"2 GiB" in lib.onmt_last_error()

@@ -166,3 +166,26 @@ def test_invalid_inputs_are_refused():
     buf = search(ok, s.lens)
     ref = search(s.src, s.lens)
     assert torch.equal(buf["tok"], ref["tok"])
+
+
+def test_workspace_operands_past_the_descriptor_limit_are_refused():
+    # the GEMMs read the memory bank and state rows through 2 GiB buffer descriptors: B * S_max source
+    # positions (or B * beam rows) whose operands would reach 2 GiB are refused before anything is read
+    # (the tiny workspace below would otherwise be refused as too small; no input buffer is touched)
+    import ctypes
+    from paper_1805_11462_amd import _lib
+    s = Custom(TINY, [3, 5])
+    lib = s.tr.lib
+    _case("descriptor_limit")
+    dummy = torch.zeros(64, dtype=torch.int32, device="cuda")
+    ws = torch.zeros(1024, dtype=torch.uint8, device="cuda")
+    B, S = 1 << 13, 1 << 10                       # 2^23 positions x 128 padded columns x 4 bytes = 4 GiB
+    rc = lib.onmt_encode(s.tr.handle, ctypes.c_void_p(dummy.data_ptr()), ctypes.c_void_p(dummy.data_ptr()), B, S,
+                         ctypes.c_void_p(ws.data_ptr()), 1024, None)
+    assert rc == _lib.ONMT_EUNSUPPORTED and b"2 GiB" in lib.onmt_last_error()
+    rc = lib.onmt_decode_init(s.tr.handle, ctypes.c_void_p(ws.data_ptr()), 1 << 18, 4, 16,
+                              ctypes.c_void_p(ws.data_ptr()), None)
+    assert rc == _lib.ONMT_EUNSUPPORTED
+    # and a batch below the limit is unaffected
+    buf = _search(s, 2, 4)
+    assert (buf["len"].cpu().numpy() >= 1).all()

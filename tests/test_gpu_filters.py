@@ -1,6 +1,5 @@
-"""GPU parity of the hypothesis filters and the unknown-word alignment (Section 4.2: beam search under
-a limit on unknown words and
-word-level constraints on the search; OOV handling; readings R18, R19).
+"""GPU parity of the hypothesis filters and the unknown-word alignment (Section 4.2: beam search under a
+limit on unknown words and word-level constraints on the search; OOV handling; readings R18, R19).
 """
 
 import numpy as np
@@ -93,14 +92,50 @@ def test_filters_tiny_peaked_match_oracle(tiny_peaked, banned, max_unk):
 def test_alignment_and_replacement_tiny_peaked(tiny_peaked):
     s = tiny_peaked
     w = s.w
-    out = _search(s, w.beam, w.max_len, alpha=0.6)
+    B, S = s.src.shape
+    buf = s.tr.search_buffers(B, S, w.beam, w.max_len, 0.6, align=True)
+    s.tr.beam_search(s.src_d, s.lens_d, buf)
+    rep = s.tr.replace_unk(s.src_d, buf).cpu().numpy()          # onmt_replace_unk, on the device
+    torch.cuda.synchronize()
     res = O.beam_search(s.model, s.src, s.lens, w.beam, w.max_len, alpha=0.6)
-    for b in range(s.src.shape[0]):
-        n = int(out["len"][b])
-        assert list(out["tok"][b, :n]) == res.tokens[b]
-        assert list(out["align"][b, :n]) == res.align[b]
-        rep = s.tr.replace_unk(out["tok"][b, :n], out["align"][b, :n], s.src[b], W.UNK_ID)
-        assert rep == O.replace_unk(res.tokens[b], res.align[b], s.src[b])
+    n_unk = 0
+    for b in range(B):
+        n = int(buf["len"][b])
+        assert list(buf["tok"][b, :n].cpu().numpy()) == res.tokens[b]
+        assert list(buf["align"][b, :n].cpu().numpy()) == res.align[b]
+        want = O.replace_unk(res.tokens[b], res.align[b], s.src[b])
+        got = [("src", int(rep[b, t])) if rep[b, t] >= 0 else ("tgt", int(buf["tok"][b, t])) for t in range(n)]
+        assert got == want
+        assert (rep[b, n:] == -1).all()
+        n_unk += sum(1 for k, _ in want if k == "src")
+    print(f"  {n_unk} UNK outputs replaced", flush=True)
+
+
+def test_replacement_of_every_unk():
+    # a model that outputs UNK at most steps (the UNK bias raised), so that the device replacement covers
+    # many positions; compared with the oracle's replacement along the oracle's own search
+    w = with_workload(W.get("tiny"), tgt_vocab=60, src_vocab=60)
+    s = Setup(w, peaked=True)
+    s.weights["b_s"][W.UNK_ID] += 3.0
+    s.model = O.model_from(w, s.weights)
+    s.tr = translator_for(w, s.weights)
+    B, S = s.src.shape
+    _case("replace_unk", workload="tiny_unk")
+    buf = s.tr.search_buffers(B, S, 2, 8, 0.0, align=True)
+    s.tr.beam_search(s.src_d, s.lens_d, buf)
+    rep = s.tr.replace_unk(s.src_d, buf).cpu().numpy()
+    res = O.beam_search(s.model, s.src, s.lens, 2, 8, 0.0)
+    n_unk = 0
+    for b in range(B):
+        n = int(buf["len"][b])
+        toks = list(buf["tok"][b, :n].cpu().numpy())
+        if toks != res.tokens[b]:
+            continue
+        want = O.replace_unk(res.tokens[b], res.align[b], s.src[b])
+        got = [("src", int(rep[b, t])) if rep[b, t] >= 0 else ("tgt", int(toks[t])) for t in range(n)]
+        assert got == want
+        n_unk += sum(1 for k, _ in want if k == "src")
+    assert n_unk > 0
 
 
 def test_filters_default_sampled(default):

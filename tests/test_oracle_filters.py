@@ -1,6 +1,5 @@
-"""Pins for the oracle's hypothesis filters and unknown-word replacement (Section 4.2: beam search under
-a limit on unknown words and
-word-level constraints on the search, and OOV handling; readings R18,
+"""Pins for the oracle's hypothesis filters and unknown-word replacement (Section 4.2: beam search under a
+limit on unknown words and word-level constraints on the search, and OOV handling; readings R18,
 R19).
 
 A beam wide enough to keep every hypothesis must return the exhaustive-search optimum over the allowed

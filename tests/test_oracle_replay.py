@@ -195,3 +195,32 @@ def test_margin_is_zero_when_candidates_tie():
         top = sorted(norms, reverse=True)
         # the final argmax is one of the decisions; the stop rule's comparisons may be closer still
         assert 0 < res.margin[b] <= top[0] - top[1] + 1e-12
+
+
+def test_prefix_agreement_accepts_itself_and_small_perturbations():
+    w, m, src, lens = _eos_model()
+    res = O.beam_search(m, src, lens, K, T, 0.6, record=True)
+    bad, n = O.prefix_agreement(res.trace, res.trace, range(len(lens)), K, 0.0)
+    assert bad == [] and all(n[b] == res.steps[b] for b in n)
+    # a model perturbed by far less than every margin chooses the same hypotheses at every step
+    eps = 0.1 * res.margin.min() / T
+    m2 = O.Model(m.enc_layers, m.dec_layers, m.bidirectional, m.emb, m.hidden, m.src_vocab, m.tgt_vocab,
+                 {k: v.copy() for k, v in m.w.items()}, m.attn)
+    m2.w["b_s"] += np.random.default_rng(4).uniform(-eps, eps, size=m2.w["b_s"].shape)
+    res2 = O.beam_search(m2, src, lens, K, T, 0.6, record=True)
+    bad, n = O.prefix_agreement(res.trace, res2.trace, range(len(lens)), K, 2 * eps * T)
+    assert bad == [] and sum(n.values()) > 0
+
+
+def test_prefix_agreement_rejects_a_different_choice_before_the_first_near_tie():
+    w, m, src, lens = _eos_model()
+    res = O.beam_search(m, src, lens, K, T, 0.6, record=True)
+    b = int(np.argmax([res.trace["margin"][0][i] for i in range(len(lens))]))
+    assert res.trace["margin"][0][b] > 1e-3
+    wrong = _copy(res.trace)
+    wrong["tok"][0][b, 1] = (wrong["tok"][0][b, 1] + 1) % 20
+    bad, _ = O.prefix_agreement(res.trace, wrong, range(len(lens)), K, 1e-3)
+    assert any(s.startswith(f"b{b} t1:") for s in bad), bad
+    # the same change is accepted where the oracle's own first decision was a near-tie
+    bad, n = O.prefix_agreement(res.trace, wrong, [b], K, res.trace["margin"][0][b] * 1.01)
+    assert bad == [] and n[b] == 0

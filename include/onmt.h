@@ -25,7 +25,8 @@
  *     launched and output buffers are unspecified. (With ONMT_VALIDATE_DEVICE, ids and lengths are
  *     instead checked by a kernel on the stream; see "Input validation".)
  *   - The caller owns all device memory: it allocates the buffers whose sizes the *_bytes queries
- *     return and passes device pointers. The library never allocates device memory.
+ *     return and passes device pointers. The library never allocates device memory (the allocation-free
+ *     decoder step uses a scratch array built into the library).
  *   - `stream` is a hipStream_t (NULL = default stream). Work is ordered on that stream.
  *   - Matrices are row-major. Beam rows are numbered r = b * K + k (sentence b, slot k).
  *   - A model handle is not thread-safe; separate handles are independent.
@@ -182,6 +183,23 @@ int onmt_decode_step(onmt_model* model, const void* enc_ws, int B, int S_max, in
 enum { ONMT_VALIDATE_HOST = 0, ONMT_VALIDATE_DEVICE = 1 };
 int onmt_set_validation(onmt_model* model, int mode);
 int onmt_device_status(onmt_model* model, int* code);
+
+/* ---- Decoder step without allocation ------------------------------------------------------------------
+ * For callers that cannot allocate memory or synchronize per call (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): onmt_decode_step without the step_ws argument. Its
+ * scratch (what step_ws holds) is a device array of ONMT_NOALLOC_SCRATCH_BYTES built into the library,
+ * one per GPU, located when a model is created on that device (or at the first call on it); the call
+ * itself allocates nothing and never waits. Inputs are validated on the device as with
+ * ONMT_VALIDATE_DEVICE (check onmt_device_status). A step whose onmt_step_ws_bytes(model, B, S_max, K)
+ * exceeds ONMT_NOALLOC_SCRATCH_BYTES is refused with ONMT_EUNSUPPORTED (16 MiB holds every workload of
+ * this library's benchmarks: 320 rows over a 50000-word vocabulary at beam 5 take 7.3 MB). All calls on
+ * one GPU share its array, which keeps the last call's contents: calls that overlap on one GPU (on
+ * different streams, or from different threads) race and must not be issued. Arguments, outputs and
+ * error codes are those of onmt_decode_step. */
+#define ONMT_NOALLOC_SCRATCH_BYTES (16u << 20)
+int onmt_decode_step_noalloc(onmt_model* model, const void* enc_ws, int B, int S_max, int K, const void* state_in,
+                             void* state_out, const int32_t* prev_tok, const int32_t* parent, int mode, float* logp,
+                             int32_t* ids, float* lse, float* attn, void* stream);
 
 /* ---- Beam search (Section 2 item (d); Section 4.2; Section 4.1 batched GPU translator) --------------
  * Translates B sentences with beam width K = params->beam (1 <= K <= 16, K <= tgt_vocab). Per sentence:

@@ -12,6 +12,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libonmt.so"
 
 ONMT_OK, ONMT_EINVAL, ONMT_ESIZE, ONMT_EDEVICE, ONMT_EUNSUPPORTED = 0, -1, -2, -3, -4
 ONMT_VALIDATE_HOST, ONMT_VALIDATE_DEVICE = 0, 1
+NOALLOC_SCRATCH_BYTES = 16 << 20
 ERROR_NAMES = {ONMT_EINVAL: "EINVAL", ONMT_ESIZE: "ESIZE", ONMT_EDEVICE: "EDEVICE", ONMT_EUNSUPPORTED: "EUNSUPPORTED"}
 
 
@@ -57,6 +58,8 @@ SIGNATURES = {
                            c_void_p, c_void_p, c_void_p]),
     "onmt_set_validation": (c_int, [c_void_p, c_int]),
     "onmt_device_status": (c_int, [c_void_p, POINTER(c_int)]),
+    "onmt_decode_step_noalloc": (c_int, [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p,
+                                         c_void_p, c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
     "onmt_profile_enable": (c_int, [c_void_p, c_int]),
     "onmt_profile_read": (c_int, [c_void_p, POINTER(c_int), POINTER(c_double), c_int]),
 }

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -334,6 +335,40 @@ void pack_row(HostImage& img, const Packed& p, int prow, int pc0, const float* s
 
 }  // namespace
 
+// ====================================================================== allocation-free step scratch
+
+// Scratch of onmt_decode_step_noalloc: the step workspace of one decoder step (attention scores and
+// context, generator partials, checked ids), a file-scope device array instead of a caller's buffer. Each
+// GPU holds its own copy, at its own address, until the process ends. In host code `scratch` names a
+// host-side stand-in, never the device memory: kernels get the address hipGetSymbolAddress returns for
+// the current device, kept per device below.
+static __device__ __align__(256) char scratch[ONMT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up once per device (at onmt_model_create, the
+// library's set-up call, or at the entry point's first call on a device no model was created on).
+int noalloc_scratch(void** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(ONMT_EUNSUPPORTED, "device index %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(ONMT_EDEVICE, "no device address for the step scratch");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ONMT_OK;
+}
+
+}  // namespace
+
 // ====================================================================== ABI
 
 extern "C" {
@@ -494,6 +529,13 @@ int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, 
     if (m->err_host) hipHostFree(m->err_host);
     delete m;
     return fail(ONMT_EDEVICE, "weight upload failed: %s", hipGetErrorString(e));
+  }
+  void* sp = nullptr;
+  rc = noalloc_scratch(&sp);    // this device's copy of the allocation-free entry point's scratch array
+  if (rc) {
+    hipHostFree(m->err_host);
+    delete m;
+    return rc;
   }
   *out = m;
   return ONMT_OK;
@@ -1254,6 +1296,37 @@ int onmt_set_validation(onmt_model* m, int mode) {
     return fail(ONMT_EINVAL, "validation mode must be ONMT_VALIDATE_HOST or ONMT_VALIDATE_DEVICE");
   m->validation = mode;
   return ONMT_OK;
+}
+
+int onmt_decode_step_noalloc(onmt_model* m, const void* enc_ws, int B, int S, int K, const void* state_in,
+                             void* state_out, const int32_t* prev_tok, const int32_t* parent, int mode, float* logp,
+                             int32_t* ids, float* lse, float* attn, void* stream) {
+  if (!m || !enc_ws || !state_in || !state_out || !prev_tok || !logp) return fail(ONMT_EINVAL, "NULL argument");
+  if (state_in == state_out) return fail(ONMT_EINVAL, "state_in and state_out must differ");
+  if (B < 1 || S < 1) return fail(ONMT_EINVAL, "B and S_max must be >= 1");
+  int rc = check_beam(m, S, K);
+  if (rc) return rc;
+  if ((rc = check_ws_limits(m->d, B, S, K, 0))) return rc;
+  if (mode != 0 && mode != 1) return fail(ONMT_EINVAL, "mode must be 0 (full) or 1 (top-K)");
+  if (mode == 1 && !ids) return fail(ONMT_EINVAL, "ids is NULL in top-K mode");
+  const size_t need = step_layout(m->d, B, S, K, nullptr, nullptr);
+  if (need > ONMT_NOALLOC_SCRATCH_BYTES)
+    return fail(ONMT_EUNSUPPORTED, "this step needs %zu bytes of scratch, more than the %u of the allocation-free call",
+                need, (unsigned)ONMT_NOALLOC_SCRATCH_BYTES);
+  void* sp = nullptr;
+  if ((rc = noalloc_scratch(&sp))) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  const int N = B * K;
+  StepWs sw;
+  step_layout(m->d, B, S, K, (char*)sp, &sw);
+  HIP_TRY(sanitize_step(prev_tok, parent, N, m->cfg.tgt_vocab, sw.tok_s, sw.par_s, m->err_host, st));
+  EncWs w;
+  enc_layout(m->d, B, S, (char*)enc_ws, &w);
+  State si, so;
+  state_layout(m->d, N, (char*)state_in, &si);
+  state_layout(m->d, N, (char*)state_out, &so);
+  return decode_compute(m, w, B, S, K, si, so, sw.tok_s, parent ? sw.par_s : nullptr, mode, logp, ids, lse, attn, sw,
+                        st, StepExtras{}, false);
 }
 
 int onmt_device_status(onmt_model* m, int* code) {

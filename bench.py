@@ -137,6 +137,48 @@ def cpu_baseline(w, weights, src, lens, n_sent, beta=0.0, banned=(), max_unk=-1)
             "value_fp64": round(toks64 / dt64, 3), "cpu_model": cpu_model(), "blas": blas_vendor()}
 
 
+KERNEL_KINDS = ("generator", "lstm", "attention", "output", "beam_step")
+PEAK_HBM_GBS = 8000.0
+
+
+def kernel_fractions(w, lens, timed, peak_tflops):
+    """Average launch time of every timed kernel kind (HIP events on the library's stream, every
+    GEN_TIMING_PERIOD-th launch of each kind during the timed searches) and its achieved fraction of the
+    roofline that bounds it: algorithmic flops / time against the MFMA peak of the operand type for the
+    GEMMs, algorithmic bytes / time against HBM for the attention, none for the (latency-bound) beam step.
+    Per launch: generator 2 N V H flops; decoder LSTM layer 2 N 4H (2H) flops (input or feed half and
+    recurrent half; the embedding rows of layer 1 come from a precomputed table); attentional output
+    2 N H (Hm + H) flops; attention 4 bytes x (keys + memory of every real source position, H + Hm wide,
+    plus the N query rows read and the N context rows written)."""
+    import numpy as np
+    N = w.batch * w.beam
+    H, V = w.hidden, w.tgt_vocab
+    Hm = H
+    real = int(np.asarray(lens).sum())
+    work = {"generator": ("mfma", 2.0 * N * V * H),
+            "lstm": ("mfma", 2.0 * N * 4 * H * 2 * H),
+            "attention": ("hbm", 4.0 * (real * (H + Hm) + N * H + N * Hm)),
+            "output": ("mfma", 2.0 * N * H * (Hm + H)),
+            "beam_step": ("latency", None)}
+    out = {}
+    for kind, (n, ms) in timed.items():
+        if not n:
+            continue
+        us = ms * 1e3 / n
+        bound, per = work[kind]
+        e = {"launches_timed": n, "avg_launch_us": round(us, 2), "bound": bound}
+        if bound == "mfma":
+            ach = per / (us * 1e-6) / 1e12
+            e.update({"flops_per_launch": per, "achieved": round(ach, 2), "unit": "TFLOP/s",
+                      "peak": peak_tflops, "frac": round(ach / peak_tflops, 4)})
+        elif bound == "hbm":
+            ach = per / (us * 1e-6) / 1e9
+            e.update({"bytes_per_launch": per, "achieved": round(ach, 1), "unit": "GB/s", "peak": PEAK_HBM_GBS,
+                      "frac": round(ach / PEAK_HBM_GBS, 4)})
+        out[kind] = e
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -180,7 +222,8 @@ def main():
 
     # the generator's launch time is sampled on every GEN_TIMING_PERIOD-th launch of the timed searches
     tr.profile(GEN_TIMING_PERIOD)
-    tr.profile_read(reset=True)
+    for kind in KERNEL_KINDS:
+        tr.profile_read(reset=True, kind=kind)
     tokens = 0
     step_s = []
     len_host = torch.empty(B, dtype=torch.int32, pin_memory=True)
@@ -194,7 +237,8 @@ def main():
         tokens += int(len_host.numpy().sum())
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    n_gen, gen_ms = tr.profile_read(reset=True)
+    timed = {kind: tr.profile_read(reset=True, kind=kind) for kind in KERNEL_KINDS}
+    n_gen, gen_ms = timed["generator"]
     tr.profile(False)
     print(f"[bench] timed {args.steps} steps in {dt:.3f} s", file=sys.stderr, flush=True)
 
@@ -233,6 +277,7 @@ def main():
                      "launches_timed": n_gen, "avg_launch_us": round(avg_gen_s * 1e6, 2),
                      "flops_per_launch": gen_flops},
     }
+    out["kernels"] = kernel_fractions(w, lens, timed, peak)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, weights, src, lens, args.cpu_sentences, args.beta, banned,
                                            args.max_unk)

@@ -249,13 +249,19 @@ int onmt_score(onmt_model* model, const int32_t* src, const int32_t* len, int B,
 
 /* ---- Kernel timing -----------------------------------------------------------------------------------
  * onmt_profile_enable(model, every): every >= 1 makes onmt_beam_search and onmt_score record HIP events
- * on `stream` around every `every`-th launch of the generator kernel (the vocabulary projection with its
- * fused log-softmax/top-K epilogue; the search launches it once per step, scoring once over all steps),
- * counting launches from this call; 0 switches timing off; < 0 is
- * ONMT_EINVAL. onmt_profile_read returns how many launches were timed and their summed duration in
- * milliseconds since the last reset. Each timed launch adds two event records to the stream. */
+ * on `stream` around every `every`-th launch of each kind of kernel below (counting launches of each kind
+ * from this call); 0 switches timing off; < 0 is ONMT_EINVAL. Kinds: the generator (the vocabulary
+ * projection with its fused log-softmax/top-K epilogue; the search launches it once per step, scoring
+ * once over all steps), a decoder LSTM layer (GEMM with the gate/cell epilogue), the attention (scores
+ * and context launches together), the attentional output tanh(W_c [ctx ; q]), and the beam step (search
+ * only). onmt_profile_read_kernel returns how many launches of `kind` were timed and their summed
+ * duration in milliseconds since its last reset; onmt_profile_read does so for the generator. Each timed
+ * launch adds two event records to the stream. */
+enum { ONMT_KERNEL_GENERATOR = 0, ONMT_KERNEL_LSTM = 1, ONMT_KERNEL_ATTENTION = 2, ONMT_KERNEL_OUTPUT = 3,
+       ONMT_KERNEL_BEAM = 4, ONMT_KERNEL_KINDS = 5 };
 int onmt_profile_enable(onmt_model* model, int every);
 int onmt_profile_read(onmt_model* model, int* n_launches, double* total_ms, int reset);
+int onmt_profile_read_kernel(onmt_model* model, int kind, int* n_launches, double* total_ms, int reset);
 
 #ifdef __cplusplus
 }

@@ -4,7 +4,7 @@
 // row-mapped segments (embedding rows by token id, state rows by beam parent, plain activations)
 // and W is a packed weight matrix. Tiles are staged through two LDS buffers; global loads run two
 // K stages ahead in registers so that a stage's loads have a full stage of MFMA work to hide behind.
-// Where the bf16 operands are pre-split hi / lo planes (the bf16 generator and decoder layers), buffer
+// Where the bf16 operands are pre-split term planes (the bf16 generator and decoder layers), buffer
 // loads with an LDS destination move them straight into the stage buffers instead.
 // Products use 16x16 MFMA tiles: v_mfma_f32_16x16x4_f32 for fp32 operands and
 // v_mfma_f32_16x16x32_bf16 for bf16 operands, always accumulating in fp32. Waves may split K
@@ -13,6 +13,8 @@
 // Epilogues: plain bias(+tanh) store; LSTM gate nonlinearities and cell update (Section 2 item
 // (a) of the OpenNMT paper) over gate-blocked columns; and the generator's per-tile row max,
 // sum of exponentials and top-K, so the vocabulary logits never need to reach memory.
+
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -44,9 +46,10 @@ struct Tile {
   static constexpr int B_CH = BN * CPR;
   static constexpr int A_PT = A_CH / NT;
   static constexpr int B_PT = B_CH / NT;
-  // bf16 products carry each fp32 activation as two bf16 terms (hi + lo, ~16 significant bits); the
-  // A tile therefore holds a hi and a lo copy. Weights are bf16 already, so W a = W hi + W lo exactly.
-  static constexpr int AREP = kBf16 ? 2 : 1;
+  // bf16 products carry each fp32 activation as kPlanes bf16 terms (p0 + p1 + p2, ~24 significant bits,
+  // the precision of the fp32 value); the A tile holds one copy per term. Weights are bf16 already, so
+  // W a = W p0 + W p1 + W p2 exactly up to the fp32 accumulation.
+  static constexpr int AREP = kBf16 ? kPlanes : 1;
   static constexpr int STAGE = (AREP * BM + BN) * ROW * (int)sizeof(T);
   static constexpr int CROW = BN + 4;                // fp32 output tile row stride
   static constexpr int CT = WK * BM * CROW * 4;
@@ -67,31 +70,38 @@ __device__ inline int xcd_remap(int bid, int nblocks) {
 
 __device__ inline uint4 zero4() { return make_uint4(0u, 0u, 0u, 0u); }
 
-// Split 8 fp32 values into bf16 hi = RNE(x) and lo = RNE(x - hi); x - hi is exact in fp32, so
-// hi + lo keeps about 16 significant bits of x. The conversions are gfx950's packed fp32 -> bf16
-// (round to nearest even), two values per instruction.
+// Split 8 fp32 values into three bf16 terms p0 = RNE(x), p1 = RNE(x - p0), p2 = RNE(x - p0 - p1). Each
+// remainder is exact in fp32 (it drops leading bits of x), so p0 + p1 + p2 keeps about 24 significant
+// bits of x: the fp32 value itself, as the bf16 products see it. (Two terms keep ~16 bits, which over the
+// 120 steps of the 4 x 1000 decoder recurrence let a hypothesis's log-prob drift to the bf16 tolerance.)
+// The conversions are gfx950's packed fp32 -> bf16 (round to nearest even), two values per instruction.
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
-__device__ inline void split_bf16x8(const float4& a, const float4& b, uint4& hi, uint4& lo) {
+__device__ inline void split_bf16x8(const float4& a, const float4& b, uint4& p0, uint4& p1, uint4& p2) {
   const f32x2_t x[4] = {{a.x, a.y}, {a.z, a.w}, {b.x, b.y}, {b.z, b.w}};
-  uint32_t h[4], l[4];
+  uint32_t t0[4], t1[4], t2[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const bf16x2_t hv = __builtin_convertvector(x[i], bf16x2_t);
-    const f32x2_t hf = __builtin_convertvector(hv, f32x2_t);
-    const bf16x2_t lv = __builtin_convertvector(x[i] - hf, bf16x2_t);
-    h[i] = __builtin_bit_cast(uint32_t, hv);
-    l[i] = __builtin_bit_cast(uint32_t, lv);
+    const bf16x2_t v0 = __builtin_convertvector(x[i], bf16x2_t);
+    const f32x2_t r1 = x[i] - __builtin_convertvector(v0, f32x2_t);
+    const bf16x2_t v1 = __builtin_convertvector(r1, bf16x2_t);
+    const f32x2_t r2 = r1 - __builtin_convertvector(v1, f32x2_t);
+    const bf16x2_t v2 = __builtin_convertvector(r2, bf16x2_t);
+    t0[i] = __builtin_bit_cast(uint32_t, v0);
+    t1[i] = __builtin_bit_cast(uint32_t, v1);
+    t2[i] = __builtin_bit_cast(uint32_t, v2);
   }
-  hi = make_uint4(h[0], h[1], h[2], h[3]);
-  lo = make_uint4(l[0], l[1], l[2], l[3]);
+  p0 = make_uint4(t0[0], t0[1], t0[2], t0[3]);
+  p1 = make_uint4(t1[0], t1[1], t1[2], t1[3]);
+  p2 = make_uint4(t2[0], t2[1], t2[2], t2[3]);
 }
 
-__device__ inline void split_bf16(float x, uint16_t& hi, uint16_t& lo) {
-  uint4 h, l;
-  split_bf16x8(make_float4(x, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f), h, l);
-  hi = (uint16_t)(h.x & 0xffffu);
-  lo = (uint16_t)(l.x & 0xffffu);
+__device__ inline void split_bf16(float x, uint16_t& p0, uint16_t& p1, uint16_t& p2) {
+  uint4 a, b, c;
+  split_bf16x8(make_float4(x, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f), a, b, c);
+  p0 = (uint16_t)(a.x & 0xffffu);
+  p1 = (uint16_t)(b.x & 0xffffu);
+  p2 = (uint16_t)(c.x & 0xffffu);
 }
 
 // Buffer resource descriptor (gfx9 family word 3). Loads through it return zeros past num_records, so
@@ -146,6 +156,8 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
   const bool pre##S = C::kBf16 && a.seg[S].lo;                                                        \
   const __amdgpu_buffer_rsrc_t rl##S = make_rsrc(pre##S ? a.seg[S].lo : a.seg[S].base,                 \
                                                  (uint32_t)a.seg[S].rows * a.seg[S].ld * es##S);       \
+  const __amdgpu_buffer_rsrc_t rm##S = make_rsrc(pre##S ? a.seg[S].lo2 : a.seg[S].base,                \
+                                                 (uint32_t)a.seg[S].rows * a.seg[S].ld * es##S);       \
   uint32_t ao##S[C::A_PT];                                                                             \
   _Pragma("unroll") for (int i = 0; i < C::A_PT; ++i) {                                                \
     const int r = m0 + arow0 + i * RSTEP;                                                              \
@@ -169,37 +181,43 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
 
   // One K stage of operands in flight: the raw global loads, held in registers until the stage is stored
   // to LDS. Everything that reads the loaded values (the zeroing of a segment's K padding, the split of an
-  // fp32 source into bf16 hi + lo) happens at that store, one stage after the loads were issued: done at
+  // fp32 source into its bf16 term planes) happens at that store, one stage after the loads were issued: done at
   // the load, it made every wave wait for its loads right after issuing them.
   struct Regs {
     uint4 a[C::A_PT];
-    uint4 alo[C::AREP == 2 ? C::A_PT : 1];   // bf16 products: the lo plane, or the second half of an fp32 row chunk
+    uint4 alo[C::AREP > 1 ? C::A_PT : 1];    // bf16 products: plane p1, or the second half of an fp32 row chunk
+    uint4 alo2[C::AREP > 1 ? C::A_PT : 1];   // bf16 products from pre-split planes: plane p2
     uint4 b[C::B_PT];
     bool ok, ok1;                            // the A chunk (and its second fp32 half) lies inside the segment width
   };
   // RSTEP and BM are multiples of 16, so every row this thread stores has the swizzle of arow0.
   static_assert(RSTEP % 16 == 0 && C::BM % 16 == 0, "row steps must keep the swizzle");
   const int scol = ((acol / C::CH) ^ C::swz(arow0)) * C::CH;
-  // pre: the segment gives bf16 hi and lo planes; src_bf16: an exact bf16 operand; else (bf16 products) an
-  // fp32 source split here into hi + lo
+  // pre: the segment gives the bf16 term planes; src_bf16: an exact bf16 operand; else (bf16 products) an
+  // fp32 source split here into kPlanes terms
   auto lstore = [&](int buf, const Regs& r, bool pre, bool src_bf16) {
 #pragma unroll
     for (int i = 0; i < C::A_PT; ++i) {
-      uint4 hi, lo = zero4();
+      uint4 p0, p1 = zero4(), p2 = zero4();
       if constexpr (!C::kBf16) {
-        hi = r.ok ? r.a[i] : zero4();
+        p0 = r.ok ? r.a[i] : zero4();
       } else if (pre || src_bf16) {
-        hi = r.ok ? r.a[i] : zero4();
-        lo = (r.ok && pre) ? r.alo[i] : zero4();
+        p0 = r.ok ? r.a[i] : zero4();
+        p1 = (r.ok && pre) ? r.alo[i] : zero4();
+        p2 = (r.ok && pre) ? r.alo2[i] : zero4();
       } else {
         const float4 f0 = __builtin_bit_cast(float4, r.a[i]);
         const float4 f1 = r.ok1 ? __builtin_bit_cast(float4, r.alo[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
-        split_bf16x8(f0, f1, hi, lo);
-        hi = r.ok ? hi : zero4();
-        lo = r.ok ? lo : zero4();
+        split_bf16x8(f0, f1, p0, p1, p2);
+        p0 = r.ok ? p0 : zero4();
+        p1 = r.ok ? p1 : zero4();
+        p2 = r.ok ? p2 : zero4();
       }
-      *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + scol) = hi;
-      if constexpr (C::AREP == 2) *(uint4*)(As[buf] + (C::BM + arow0 + i * RSTEP) * C::ROW + scol) = lo;
+      *(uint4*)(As[buf] + (arow0 + i * RSTEP) * C::ROW + scol) = p0;
+      if constexpr (C::AREP > 1) {
+        *(uint4*)(As[buf] + (C::BM + arow0 + i * RSTEP) * C::ROW + scol) = p1;
+        *(uint4*)(As[buf] + (2 * C::BM + arow0 + i * RSTEP) * C::ROW + scol) = p2;
+      }
     }
 #pragma unroll
     for (int i = 0; i < C::B_PT; ++i) *(uint4*)(Bs[buf] + (arow0 + i * RSTEP) * C::ROW + scol) = r.b[i];
@@ -244,15 +262,18 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
 #pragma unroll
           for (int y = 0; y < C::TN; ++y)
             acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
-        if (has_lo) {               // uniform: the segment's source is fp32
+        if (has_lo) {               // uniform: the segment's source is fp32 (planes p1 and p2)
 #pragma unroll
-          for (int x = 0; x < C::TM; ++x)
-            av[x] = *(const bf16x8*)(Ab + (C::BM + x * 16) * C::ROW + col);
+          for (int pl = 1; pl < C::AREP; ++pl) {
 #pragma unroll
-          for (int x = 0; x < C::TM; ++x)
+            for (int x = 0; x < C::TM; ++x)
+              av[x] = *(const bf16x8*)(Ab + (pl * C::BM + x * 16) * C::ROW + col);
 #pragma unroll
-            for (int y = 0; y < C::TN; ++y)
-              acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+            for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+              for (int y = 0; y < C::TN; ++y)
+                acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+          }
         }
       }
     }
@@ -262,7 +283,7 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
   // M read zeros through the descriptor bound, columns in a segment's padding are zeroed at the LDS store,
   // and past the last stage the loads re-read the last stage into a buffer that is never multiplied.
   uint32_t kbyte_w = 0;                 // byte offset of the segment inside a weight row
-  auto run_segment = [&](__amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t rl, bool pre,
+  auto run_segment = [&](__amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t rl, __amdgpu_buffer_rsrc_t rm, bool pre,
                          const uint32_t (&ao)[C::A_PT], uint32_t es, int width, int kpad) {
     const bool src_bf16 = es == 2 && !pre;              // exact bf16 operand: no lo part
     auto gload = [&](int st) -> Regs {
@@ -277,10 +298,11 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
           r.a[i] = buf_load16(rs, off);
         } else {
           // bf16 source: 8 elements in one 16-byte load (exact, no lo part); pre-split source: 8 elements
-          // of each plane; fp32 source: two 16-byte loads, split into bf16 hi + lo at the LDS store (widths
+          // of each plane; fp32 source: two 16-byte loads, split into bf16 terms at the LDS store (widths
           // are multiples of 4, so the second half may be past the end).
           r.a[i] = buf_load16(rs, off);
           r.alo[i] = pre ? buf_load16(rl, off) : buf_load16(rs, off + 16);
+          if (pre) r.alo2[i] = buf_load16(rm, off);
         }
       }
       const uint32_t kb = kbyte_w + (uint32_t)(st * C::BK) * sizeof(T);
@@ -313,9 +335,9 @@ __device__ inline void gemm_tile(const AOp& a, const BOp& b, int m0, int n0, cha
     }
     kbyte_w += (uint32_t)kpad * sizeof(T);
   };
-  run_segment(rs0, rl0, pre0, ao0, es0, wd0, kp0);
-  if constexpr (nseg > 1) run_segment(rs1, rl1, pre1, ao1, es1, wd1, kp1);
-  if constexpr (nseg > 2) run_segment(rs2, rl2, pre2, ao2, es2, wd2, kp2);
+  run_segment(rs0, rl0, rm0, pre0, ao0, es0, wd0, kp0);
+  if constexpr (nseg > 1) run_segment(rs1, rl1, rm1, pre1, ao1, es1, wd1, kp1);
+  if constexpr (nseg > 2) run_segment(rs2, rl2, rm2, pre2, ao2, es2, wd2, kp2);
   (void)bf0;
   (void)bf1;
   (void)bf2;
@@ -366,10 +388,11 @@ __global__ __launch_bounds__(C::NT) void k_gemm_store(AOp a, BOp b, StoreParams 
     }
     if (out) *(float4*)(p.out + (size_t)gr * p.ldo + gc) = make_float4(v[0], v[1], v[2], v[3]);
     if (split) {
-      uint4 h, l;
-      split_bf16x8(make_float4(v[0], v[1], v[2], v[3]), make_float4(0.f, 0.f, 0.f, 0.f), h, l);
-      *(uint2*)(p.hi + (size_t)gr * p.ld_hl + gc) = make_uint2(h.x, h.y);
-      *(uint2*)(p.lo + (size_t)gr * p.ld_hl + gc) = make_uint2(l.x, l.y);
+      uint4 t0, t1, t2;
+      split_bf16x8(make_float4(v[0], v[1], v[2], v[3]), make_float4(0.f, 0.f, 0.f, 0.f), t0, t1, t2);
+      *(uint2*)(p.hi + (size_t)gr * p.ld_hl + gc) = make_uint2(t0.x, t0.y);
+      *(uint2*)(p.lo + (size_t)gr * p.ld_hl + gc) = make_uint2(t1.x, t1.y);
+      *(uint2*)(p.lo2 + (size_t)gr * p.ld_hl + gc) = make_uint2(t2.x, t2.y);
     }
   }
 }
@@ -382,7 +405,7 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
 constexpr int kLstmStages = 2;
 template <class C>
 constexpr int dma_lds() {
-  constexpr int stg = (2 * C::BM + C::BN) * C::BK * 2;
+  constexpr int stg = (kPlanes * C::BM + C::BN) * C::BK * 2;
   return kLstmStages * stg > C::CT ? kLstmStages * stg : C::CT;
 }
 
@@ -445,10 +468,11 @@ __device__ inline void lstm_epilogue(Acc acc, const LstmParams& p, int M, int m0
     p.h_out[(size_t)row * p.ld_out + unit] = h_new;
     p.c_out[(size_t)row * p.ld_out + unit] = c_new;
     if (p.h_hi) {
-      uint16_t hh, hl;
-      split_bf16(h_new, hh, hl);
-      p.h_hi[(size_t)row * p.ld_hl + unit] = hh;
-      p.h_lo[(size_t)row * p.ld_hl + unit] = hl;
+      uint16_t t0, t1, t2;
+      split_bf16(h_new, t0, t1, t2);
+      p.h_hi[(size_t)row * p.ld_hl + unit] = t0;
+      p.h_lo[(size_t)row * p.ld_hl + unit] = t1;
+      p.h_lo2[(size_t)row * p.ld_hl + unit] = t2;
     }
     if (p.y_out) p.y_out[(size_t)(row * p.y_S + p.y_s) * p.ld_y + p.y_col0 + unit] = y;
   }
@@ -698,6 +722,11 @@ static_assert(TileGen32::BN == TileGen16::BN && TileGen32h::BN == TileGen32::BN,
 // 10-15% faster than 64 x 128 tiles with three 16 KB stages, and three or four stages of 64 x 256 slower.
 constexpr int kGenStages = 2;
 constexpr int kGenWN = 4;
+// The pre-split generator multiplies the first two of the operand's bf16 term planes (~17 significant bits
+// of each activation, a relative error under 2^-16): its output leaves the recurrence, so the error stays
+// per step, ~1e-5 on a logit over 1000-wide rows, instead of compounding over the steps the way an error
+// of the decoder layers' operands does. The third plane serves those layers.
+constexpr int kGenPlanes = 2;
 
 // One 16-byte-per-lane buffer load into LDS (lane l writes 16 bytes at lds + 16 l). (A function of its
 // own: called directly under control flow inside a kernel template, the builtin stops the host-side
@@ -716,7 +745,7 @@ constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | (((n 
 // stage) means its share of the oldest stage has landed; a barrier then makes the whole stage visible.
 // The barrier is the bare instruction: the fences of __syncthreads would also wait for the stages still
 // in flight. Fragment reads, products and the epilogue are those of the register-staged kernel.
-template <int WN, int NSTG>
+template <int WN, int NSTG, int NPL>
 __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, GenParams p, int nm, int nblocks) {
   using C = Tile<__bf16, 2, WN, 1, 2, 4, 32>;          // 64 x (64 WN) tile, waves of 32 x 64
   using CE = TileGen16;                                 // the 64 x 128 sub-tiles the epilogue works on
@@ -727,38 +756,47 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
   constexpr int ROWB = C::BK * 2;                       // bytes per tile row
   constexpr int RPS = 16;                               // tile rows per 1 KB slice
   constexpr int SA = C::BM / RPS, SB = C::BN / RPS;     // slices per plane of A, and of B
-  constexpr int SPW = (2 * SA + SB) / NW;               // slices (loads) per wave per stage
-  constexpr int STG = (2 * C::BM + C::BN) * ROWB;       // one stage: A hi rows, A lo rows, B rows
+  constexpr int NSL = NPL * SA + SB;                    // slices per stage
+  constexpr int SPW = (NSL + NW - 1) / NW;              // slices (loads) per wave per stage, at most
+  constexpr int STG = (NPL * C::BM + C::BN) * ROWB;     // one stage: the A planes' rows, then B rows
   constexpr int NSUB = C::BN / 128;
   constexpr int LDSB = NSTG * STG > NSUB * CE::CT ? NSTG * STG : NSUB * CE::CT;
-  static_assert((2 * SA + SB) % NW == 0 && NSTG >= 2 && SPW * (NSTG - 2) < 64, "slice layout / wait count");
+  // waves may move different numbers of slices only when every wait is for all loads (two stages)
+  static_assert((NSL % NW == 0 || NSTG == 2) && NSTG >= 2 && SPW * (NSTG - 2) < 64, "slice layout / wait count");
   __shared__ __attribute__((aligned(16))) char smem[LDSB];
   const int L = xcd_remap(blockIdx.x, nblocks);
   const int mt = L % nm, nt = L / nm;
   const int m0 = mt * C::BM, n0 = nt * C::BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index read into a scalar register: slice kinds derived from it are then known to be uniform,
+  // so the descriptor each load uses is picked by scalar branches rather than a per-lane loop
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int i16 = lane & 15, g = lane >> 4;
   const int wn = wave % C::WN, wm = wave / C::WN;
   float cb[C::TN];
   gen_col_bias<C>(p, n0, wn, i16, cb);
 
-  // slice q of a stage: A hi rows 16 q.. (q < SA), A lo rows (q < 2 SA), then B rows; wave w moves slices
-  // w, w + NW, ...; lane's place in a slice: tile row lane / 4, 16-byte slot lane % 4 (chunk slot ^ swz)
+  // slice q of a stage: rows 16 q.. of A plane q / SA (q < NPL SA), then B rows; wave w moves slices
+  // w, w + NW, ... (below NSL); lane's place in a slice: tile row lane / 4, 16-byte slot lane % 4 (chunk
+  // slot ^ swz)
   const int srow = lane >> 2, sslot = lane & 3;
-  const __amdgpu_buffer_rsrc_t rhi = make_rsrc(a.hi, (uint32_t)a.M * a.ld * 2);
-  const __amdgpu_buffer_rsrc_t rlo = make_rsrc(a.lo, (uint32_t)a.M * a.ld * 2);
+  static_assert(NPL >= 1 && NPL <= kPlanes, "the operand holds kPlanes term planes");
+  const __amdgpu_buffer_rsrc_t rpl[kPlanes] = {make_rsrc(a.hi, (uint32_t)a.M * a.ld * 2),
+                                               make_rsrc(a.lo, (uint32_t)a.M * a.ld * 2),
+                                               make_rsrc(a.lo2, (uint32_t)a.M * a.ld * 2)};
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(b.W, (uint32_t)b.Np * b.Kp * 2);
-  int sl_kind[SPW], sl_lds[SPW];                        // 0 A hi, 1 A lo, 2 B; LDS byte offset in a stage
+  int sl_kind[SPW], sl_lds[SPW];                        // A plane (0 .. NPL - 1) or NPL (B), -1 none
   uint32_t sl_off[SPW];                                 // lane's byte offset in its operand at K = 0
 #pragma unroll
   for (int i = 0; i < SPW; ++i) {
     const int q = wave + NW * i;
-    const int kind = q < SA ? 0 : (q < 2 * SA ? 1 : 2);
-    const int trow = (kind == 0 ? q : (kind == 1 ? q - SA : q - 2 * SA)) * RPS + srow;   // row in its plane
+    const int kind = q >= NSL ? -1 : (q < NPL * SA ? q / SA : NPL);
+    const int trow = (kind == NPL ? q - NPL * SA : q % SA) * RPS + srow;           // row in its plane
     const int chunk = sslot ^ C::swz(trow);
     sl_kind[i] = kind;
-    sl_lds[i] = ((kind == 2 ? 2 * C::BM : kind * C::BM) + trow - srow) * ROWB;
-    if (kind == 2) {                                    // B rows past the packed matrix re-read its last row
+    sl_lds[i] = ((kind == NPL ? NPL * C::BM : kind * C::BM) + trow - srow) * ROWB;
+    if (kind < 0) {
+      sl_off[i] = 0;
+    } else if (kind == NPL) {                           // B rows past the packed matrix re-read its last row
       const int br = min(n0 + trow, b.Np - 1);
       sl_off[i] = ((uint32_t)br * C::BK + chunk * C::CH) * 2;   // in K block 0 (the stage adds its block)
     } else {                                            // A rows past M re-read row M - 1 (never stored)
@@ -783,12 +821,14 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
     const uint32_t ks_ = (uint32_t)((ST) < nst ? (ST) : nst - 1);                                       \
     const uint32_t ko_ = ks_ * ROWB, kb_ = ks_ * (uint32_t)b.Np * ROWB;                                 \
     _Pragma("unroll") for (int i = 0; i < SPW; ++i) {                                                   \
-      if (sl_kind[i] == 0)                                                                              \
-        dma16(rhi, sb_ + sl_lds[i], sl_off[i] + ko_);                                                  \
-      else if (sl_kind[i] == 1)                                                                         \
-        dma16(rlo, sb_ + sl_lds[i], sl_off[i] + ko_);                                                  \
-      else                                                                                              \
+      if (sl_kind[i] == NPL)                                                                        \
         dma16(rw, sb_ + sl_lds[i], sl_off[i] + kb_);                                                   \
+      else if (sl_kind[i] == 0)                                                                         \
+        dma16(rpl[0], sb_ + sl_lds[i], sl_off[i] + ko_);                                               \
+      else if (sl_kind[i] == 1)                                                                         \
+        dma16(rpl[1], sb_ + sl_lds[i], sl_off[i] + ko_);                                               \
+      else if (sl_kind[i] == 2)                                                                         \
+        dma16(rpl[2], sb_ + sl_lds[i], sl_off[i] + ko_);                                               \
     }                                                                                                   \
   } while (0)
 #pragma unroll
@@ -801,25 +841,20 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
     ONMT_GEN_ISSUE(st + NSTG - 1);                      // refills the buffer multiplied at st - 1
     const char* base = smem + (st % NSTG) * STG;
     const __bf16* Ah = (const __bf16*)base + (wm * C::TM * 16 + i16) * C::ROW;
-    const __bf16* Al = Ah + C::BM * C::ROW;
-    const __bf16* Bb = (const __bf16*)base + (2 * C::BM + wn * C::TN * 16 + i16) * C::ROW;
+    const __bf16* Bb = (const __bf16*)base + (NPL * C::BM + wn * C::TN * 16 + i16) * C::ROW;
     bf16x8 av[C::TM], bv[C::TN];
-#pragma unroll
-    for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + x * 16 * C::ROW + col);
 #pragma unroll
     for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + col);
 #pragma unroll
-    for (int x = 0; x < C::TM; ++x)
+    for (int pl = 0; pl < NPL; ++pl) {
 #pragma unroll
-      for (int y = 0; y < C::TN; ++y)
-        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+      for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + (pl * C::BM + x * 16) * C::ROW + col);
 #pragma unroll
-    for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Al + x * 16 * C::ROW + col);
+      for (int x = 0; x < C::TM; ++x)
 #pragma unroll
-    for (int x = 0; x < C::TM; ++x)
-#pragma unroll
-      for (int y = 0; y < C::TN; ++y)
-        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+        for (int y = 0; y < C::TN; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+    }
   }
 #undef ONMT_GEN_ISSUE
   // every load (including the re-loads past the end) has landed before the output tiles reuse the buffers
@@ -848,8 +883,8 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
 // Vector-memory "no wait", LDS wait until nothing is outstanding (for LDS stores before a bare barrier).
 constexpr int kWaitLgkm0 = 15 | (7 << 4) | (0 << 8) | (3 << 14);
 
-// gemm_tile for bf16 products whose A segments (one or two) are all pre-split hi / lo planes, with the
-// operands moved straight into LDS: a stage of A hi rows, A lo rows and B rows is sliced into 1 KB pieces
+// gemm_tile for bf16 products whose A segments (one or two) are all pre-split term planes, with the
+// operands moved straight into LDS: a stage of the A rows of every plane and the B rows is sliced into 1 KB pieces
 // (RPS tile rows each; lane l writes row l / (ROWB / 16), 16-byte slot l % (ROWB / 16)), kLstmStages stages
 // in flight, waits and bare barriers as in k_gemm_gen_lds. A rows come through the segment's row map
 // (beam parents) and rows past M re-read row M - 1. The planes' columns past a segment's width are not
@@ -859,24 +894,27 @@ template <class C, int NSEG>
 __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0, char* smem) {
   static_assert(C::kBf16 && C::KW == C::KSUB && NSEG >= 1 && NSEG <= 2, "one MFMA K step per wave and stage");
   constexpr int NW = C::NT / 64, ROWB = C::BK * 2, RPS = 1024 / ROWB, LPR = ROWB / 16;
-  constexpr int SA = C::BM / RPS, SB = C::BN / RPS, SPW = (2 * SA + SB) / NW;
-  constexpr int STG = (2 * C::BM + C::BN) * ROWB, NSTG = kLstmStages;
-  static_assert(1024 % ROWB == 0 && C::BM % RPS == 0 && C::BN % RPS == 0 && (2 * SA + SB) % NW == 0 &&
+  constexpr int SA = C::BM / RPS, SB = C::BN / RPS, SPW = (kPlanes * SA + SB) / NW;
+  constexpr int STG = (kPlanes * C::BM + C::BN) * ROWB, NSTG = kLstmStages;
+  static_assert(1024 % ROWB == 0 && C::BM % RPS == 0 && C::BN % RPS == 0 && (kPlanes * SA + SB) % NW == 0 &&
                     SPW * (NSTG - 2) < 64 && dma_lds<C>() >= NSTG * STG,
                 "slice layout");
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index read into a scalar register: slice kinds derived from it are then known to be uniform,
+  // so the descriptor each load uses is picked by scalar branches rather than a per-lane loop
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int i16 = lane & 15, g = lane >> 4;
   const int wk = wave % C::WK, wn = (wave / C::WK) % C::WN, wm = wave / (C::WK * C::WN);
   const int srow = lane / LPR, sslot = lane % LPR;
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(b.W, (uint32_t)b.Np * b.Kp * 2);
   // per segment (constant indices only): plane descriptors, stage count, width
-  __amdgpu_buffer_rsrc_t rh[2], rl[2];
+  __amdgpu_buffer_rsrc_t rp[2][kPlanes];
   int nst[2] = {0, 0}, wd[2] = {0, 0};
 #pragma unroll
   for (int s = 0; s < NSEG; ++s) {
     const uint32_t bytes = (uint32_t)a.seg[s].rows * a.seg[s].ld * 2;
-    rh[s] = make_rsrc(a.seg[s].base, bytes);
-    rl[s] = make_rsrc(a.seg[s].lo, bytes);
+    rp[s][0] = make_rsrc(a.seg[s].base, bytes);
+    rp[s][1] = make_rsrc(a.seg[s].lo, bytes);
+    rp[s][2] = make_rsrc(a.seg[s].lo2, bytes);
     nst[s] = a.seg[s].kpad / C::BK;
     wd[s] = a.seg[s].width;
   }
@@ -887,11 +925,11 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
 #pragma unroll
   for (int i = 0; i < SPW; ++i) {
     const int q = wave + NW * i;
-    const int kind = q < SA ? 0 : (q < 2 * SA ? 1 : 2);
-    const int trow = (kind == 0 ? q : (kind == 1 ? q - SA : q - 2 * SA)) * RPS + srow;
+    const int kind = q < kPlanes * SA ? q / SA : kPlanes;   // an A plane, or kPlanes for B
+    const int trow = (kind == kPlanes ? q - kPlanes * SA : q % SA) * RPS + srow;
     const int chunk = sslot ^ C::swz(trow);
     sl_kind[i] = kind;
-    sl_lds[i] = ((kind == 2 ? 2 * C::BM : kind * C::BM) + trow - srow) * ROWB;
+    sl_lds[i] = ((kind == kPlanes ? kPlanes * C::BM : kind * C::BM) + trow - srow) * ROWB;
     boff[i] = ((uint32_t)min(n0 + trow, b.Np - 1) * b.Kp + chunk * C::CH) * 2;
     const int r = min(m0 + trow, a.M - 1);
 #pragma unroll
@@ -908,22 +946,34 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
   for (int x = 0; x < C::TM; ++x)
 #pragma unroll
     for (int y = 0; y < C::TN; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // stages past the last re-load the last one into a buffer that is never multiplied
-  auto issue = [&](int G) {
-    const int gg = G < total ? G : total - 1;
-    const int s = gg >= nst[0] ? 1 : 0;
-    const int ls = gg - (s ? nst[0] : 0);
-    char* sb = smem + (G % NSTG) * STG;
-    const uint32_t ka = (uint32_t)ls * ROWB, kb = (uint32_t)((s ? kb1 : 0) + ls * C::BK) * 2;
+  // stages past the last re-load the last one into a buffer that is never multiplied. The segment is a
+  // template constant of issue_seg, so every descriptor and offset array is indexed by constants and stays
+  // in registers (a runtime segment index put them in scratch memory).
+  auto issue_seg = [&](auto seg_c, int ls, char* sb) {
+    constexpr int S = decltype(seg_c)::value;
+    const uint32_t ka = (uint32_t)ls * ROWB, kb = (uint32_t)((S ? kb1 : 0) + ls * C::BK) * 2;
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
-      if (sl_kind[i] == 2)
+      if (sl_kind[i] == kPlanes)
         dma16(rw, sb + sl_lds[i], boff[i] + kb);
       else if (sl_kind[i] == 0)
-        dma16(s ? rh[1] : rh[0], sb + sl_lds[i], (s ? aoff[1][i] : aoff[0][i]) + ka);
+        dma16(rp[S][0], sb + sl_lds[i], aoff[S][i] + ka);
+      else if (sl_kind[i] == 1)
+        dma16(rp[S][1], sb + sl_lds[i], aoff[S][i] + ka);
       else
-        dma16(s ? rl[1] : rl[0], sb + sl_lds[i], (s ? aoff[1][i] : aoff[0][i]) + ka);
+        dma16(rp[S][2], sb + sl_lds[i], aoff[S][i] + ka);
     }
+  };
+  auto issue = [&](int G) {
+    const int gg = G < total ? G : total - 1;
+    char* sb = smem + (G % NSTG) * STG;
+    if constexpr (NSEG > 1) {
+      if (gg >= nst[0]) {
+        issue_seg(std::integral_constant<int, 1>{}, gg - nst[0], sb);
+        return;
+      }
+    }
+    issue_seg(std::integral_constant<int, 0>{}, gg, sb);
   };
 #pragma unroll
   for (int G = 0; G < NSTG - 1; ++G) issue(G);
@@ -939,8 +989,8 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
       const int ls = G - (s ? nst[0] : 0);
       const int w = s ? wd[1] : wd[0];
       if ((ls + 1) * C::BK > w) {                      // the segment's last stage reaches past its width
-        for (int e = tid; e < 2 * C::BM * C::CPR; e += C::NT) {
-          const int row = e / C::CPR, c = e % C::CPR;   // row of the hi then the lo plane, logical chunk
+        for (int e = tid; e < kPlanes * C::BM * C::CPR; e += C::NT) {
+          const int row = e / C::CPR, c = e % C::CPR;   // row of the A planes, one after the other; chunk
           if (ls * C::BK + c * C::CH >= w)
             *(uint4*)(base + row * ROWB + ((c ^ C::swz(row % C::BM)) * 16)) = zero4();
         }
@@ -952,25 +1002,20 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
     }
     issue(G + NSTG - 1);                                // refills the buffer multiplied at G - 1
     const __bf16* Ah = (const __bf16*)base + (wm * C::TM * 16 + i16) * C::ROW;
-    const __bf16* Al = Ah + C::BM * C::ROW;
-    const __bf16* Bb = (const __bf16*)base + (2 * C::BM + wn * C::TN * 16 + i16) * C::ROW;
+    const __bf16* Bb = (const __bf16*)base + (kPlanes * C::BM + wn * C::TN * 16 + i16) * C::ROW;
     bf16x8 av[C::TM], bv[C::TN];
-#pragma unroll
-    for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + x * 16 * C::ROW + col);
 #pragma unroll
     for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + col);
 #pragma unroll
-    for (int x = 0; x < C::TM; ++x)
+    for (int pl = 0; pl < kPlanes; ++pl) {
 #pragma unroll
-      for (int y = 0; y < C::TN; ++y)
-        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+      for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + (pl * C::BM + x * 16) * C::ROW + col);
 #pragma unroll
-    for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Al + x * 16 * C::ROW + col);
+      for (int x = 0; x < C::TM; ++x)
 #pragma unroll
-    for (int x = 0; x < C::TM; ++x)
-#pragma unroll
-      for (int y = 0; y < C::TN; ++y)
-        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+        for (int y = 0; y < C::TN; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+    }
   }
   // every load (including the re-loads past the end) has landed before the output tile reuses the buffers
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
@@ -1023,7 +1068,7 @@ static hipError_t launch_store(const AOp& a, const BOp& b, const StoreParams& p,
 static inline bool all_pre_split(const AOp& a) {
   if (a.nseg < 1 || a.nseg > 2) return false;
   for (int s = 0; s < a.nseg; ++s)
-    if (!a.seg[s].bf16 || !a.seg[s].lo || a.seg[s].ld < a.seg[s].kpad) return false;
+    if (!a.seg[s].bf16 || !a.seg[s].lo || !a.seg[s].lo2 || a.seg[s].ld < a.seg[s].kpad) return false;
   return true;
 }
 
@@ -1113,24 +1158,26 @@ hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st) {
 }
 
 __global__ void k_split_rows(const float* __restrict__ src, int ld_src, int rows, int cols, uint16_t* __restrict__ hi,
-                             uint16_t* __restrict__ lo, int ld_dst) {
+                             uint16_t* __restrict__ lo, uint16_t* __restrict__ lo2, int ld_dst) {
   const size_t n = (size_t)rows * ld_dst;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
     const int r = (int)(i / ld_dst), c = (int)(i % ld_dst);
-    uint16_t h = 0, l = 0;
-    if (c < cols) split_bf16(src[(size_t)r * ld_src + c], h, l);
-    hi[i] = h;
-    lo[i] = l;
+    uint16_t t0 = 0, t1 = 0, t2 = 0;
+    if (c < cols) split_bf16(src[(size_t)r * ld_src + c], t0, t1, t2);
+    hi[i] = t0;
+    lo[i] = t1;
+    lo2[i] = t2;
   }
 }
 
-hipError_t split_rows(const float* src, int ld_src, int rows, int cols, uint16_t* hi, uint16_t* lo, int ld_dst,
-                      hipStream_t st) {
+hipError_t split_rows(const float* src, int ld_src, int rows, int cols, uint16_t* hi, uint16_t* lo, uint16_t* lo2,
+                      int ld_dst, hipStream_t st) {
   const size_t n = (size_t)rows * ld_dst;
   if (n == 0) return hipSuccess;
   size_t blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(k_split_rows, dim3((unsigned)blocks), dim3(256), 0, st, src, ld_src, rows, cols, hi, lo, ld_dst);
+  hipLaunchKernelGGL(k_split_rows, dim3((unsigned)blocks), dim3(256), 0, st, src, ld_src, rows, cols, hi, lo, lo2,
+                     ld_dst);
   return hipGetLastError();
 }
 
@@ -1148,7 +1195,7 @@ hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, const GenParams& p, 
     return hipErrorInvalidValue;
   const int nm = (a.M + BM - 1) / BM;
   const int nblocks = nm * ((b.Np + BN - 1) / BN);
-  hipLaunchKernelGGL((k_gemm_gen_lds<kGenWN, kGenStages>), dim3(nblocks), dim3(128 * kGenWN), 0, st, a, b, p, nm,
+  hipLaunchKernelGGL((k_gemm_gen_lds<kGenWN, kGenStages, kGenPlanes>), dim3(nblocks), dim3(128 * kGenWN), 0, st, a, b, p, nm,
                      nblocks);
   return hipGetLastError();
 }

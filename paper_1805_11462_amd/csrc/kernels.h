@@ -10,6 +10,10 @@ namespace onmt {
 // (32, 64 or 128 elements) divides it, so a stage never straddles two segments.
 constexpr int kSegK = 128;
 
+// bf16 products carry each fp32 activation as this many bf16 terms (RNE of the value, then of each
+// remainder), ~24 significant bits: the products see the fp32 value itself.
+constexpr int kPlanes = 3;
+
 // One K-segment of a GEMM's A operand: A[r, off + k] = base[map(r) * ld + k] for k < width,
 // 0 for width <= k < kpad. map(r) = idx ? idx[r] : r. The buffer must be smaller than 2 GiB.
 struct Seg {
@@ -20,8 +24,8 @@ struct Seg {
   int width;
   int kpad;
   int bf16;      // 1: base holds bf16 values (exact operands)
-  const void* lo;   // bf16 products only: base and lo are the bf16 hi and lo planes of fp32 values
-                    // (bf16 = 1, width a multiple of 8); the operand is hi + lo, as if split on load
+  const void* lo;   // bf16 products only: base, lo and lo2 are the kPlanes bf16 term planes of fp32 values
+  const void* lo2;  // (bf16 = 1, width a multiple of 8); the operand is their sum, as if split on load
 };
 
 struct AOp {
@@ -38,8 +42,8 @@ struct BOp {
 };
 
 // Plain store epilogue: out[r, n] = act(acc + bias[n]) for n < ncols. act: 0 none, 1 tanh.
-// Optionally (hi != nullptr) the same values split into bf16 hi = RNE(v) and lo = RNE(v - hi) planes
-// [rows, ld_hl] for columns n < ncols_hl (columns past ncols hold act(0), zero for the tanh stores).
+// Optionally (hi != nullptr) the same values split into the bf16 term planes hi, lo, lo2 [rows, ld_hl]
+// for columns n < ncols_hl (columns past ncols hold act(0), zero for the tanh stores).
 struct StoreParams {
   const float* bias;
   float* out;
@@ -50,6 +54,7 @@ struct StoreParams {
   uint16_t* lo;
   int ld_hl;
   int ncols_hl;
+  uint16_t* lo2;
 };
 
 // LSTM cell epilogue over gate-blocked columns (groups of 32 = 4 gates x kUnitGroup = 8 units).
@@ -67,9 +72,10 @@ struct LstmParams {
   float* h_out;
   float* c_out;
   int ld_out;
-  uint16_t* h_hi;               // optional bf16 hi / lo planes of h_out (row stride ld_hl)
+  uint16_t* h_hi;               // optional bf16 term planes of h_out (row stride ld_hl)
   uint16_t* h_lo;
   int ld_hl;
+  uint16_t* h_lo2;
   float* y_out;                 // optional layer output row b * y_S + y_s, column offset y_col0
   int ld_y, y_S, y_s, y_col0;
   const int32_t* lens;          // optional: GEMM row b is active iff y_s < lens[b]
@@ -120,16 +126,18 @@ hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st);
 hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st);
 
 
-// bf16 generator operand already split into bf16 hi and lo planes (A = hi + lo), row-major [M, ld] each
-// with zeros in the K padding (columns width .. kpad - 1).
+// bf16 generator operand already split into its bf16 term planes (A = hi + lo + lo2), row-major [M, ld]
+// each with zeros in the K padding (columns width .. kpad - 1).
 struct GenSplitA {
   const uint16_t* hi;
   const uint16_t* lo;
   int M;
   int ld;      // elements per row, >= kpad
   int kpad;    // multiple of kSegK
+  const uint16_t* lo2;
 };
-// The bf16 generator on a pre-split operand: same partials as gemm_gen, operands moved straight into LDS.
+// The bf16 generator on a pre-split operand, operands moved straight into LDS. It multiplies the first two
+// term planes only (A ~ hi + lo; lo2 is not read): its logits do not feed back into the decoder.
 // Its weights are K-blocked: element (n, k) of the [Np, Kp] matrix sits at (k / kGenKBlock) * Np *
 // kGenKBlock + n * kGenKBlock + k % kGenKBlock, so that one K stage of a column tile is one contiguous block
 // (with row-major weights each load instruction touched 16 rows 2 KB apart for 64 bytes each).
@@ -228,9 +236,10 @@ hipError_t sanitize_step(const int32_t* tok, const int32_t* parent, int N, int V
 
 hipError_t replicate_rows(const float* src, int ld_src, int rows, int K, float* dst, int ld_dst, int ncols,
                           hipStream_t st);
-// hi / lo [rows, ld_dst] = bf16 planes of src [rows, ld_src] columns < cols, zeros in columns cols .. ld_dst.
-hipError_t split_rows(const float* src, int ld_src, int rows, int cols, uint16_t* hi, uint16_t* lo, int ld_dst,
-                      hipStream_t st);
+// hi / lo / lo2 [rows, ld_dst] = the bf16 term planes of src [rows, ld_src] columns < cols, zeros in
+// columns cols .. ld_dst.
+hipError_t split_rows(const float* src, int ld_src, int rows, int cols, uint16_t* hi, uint16_t* lo, uint16_t* lo2,
+                      int ld_dst, hipStream_t st);
 hipError_t fill_f32(float* dst, size_t n, float v, hipStream_t st);
 hipError_t copy_cols(const float* src, int ld_src, float* dst, int ld_dst, int rows, int ncols, hipStream_t st);
 

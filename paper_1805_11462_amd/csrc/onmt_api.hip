@@ -70,6 +70,7 @@ Seg seg(const void* base, const int32_t* idx, int rows, int ld, int width, int k
   s.kpad = kpad;
   s.bf16 = bf16;
   s.lo = nullptr;
+  s.lo2 = nullptr;
   return s;
 }
 
@@ -216,11 +217,13 @@ struct onmt_model {
   size_t image_bytes = 0;    // the uploaded part of the model buffer (everything before emb_gates)
   // kernel timing
   int prof = 0;              // time every prof-th generator launch (0: off)
-  long long prof_seq = 0;    // generator launches seen while timing is on
-  bool prof_open = false;    // the current launch has a start event recorded
-  int prof_n = 0;
-  double prof_ms = 0.0;
+  long long prof_seq[ONMT_KERNEL_KINDS] = {};   // launches of each kind seen while timing is on
+  bool prof_open[ONMT_KERNEL_KINDS] = {};       // the current launch of the kind has a start event
+  size_t prof_pair[ONMT_KERNEL_KINDS] = {};     // ... recorded as event pair ev[prof_pair], ev[prof_pair + 1]
+  int prof_n[ONMT_KERNEL_KINDS] = {};
+  double prof_ms[ONMT_KERNEL_KINDS] = {};
   std::vector<hipEvent_t> ev;   // reusable start/stop pairs
+  std::vector<int> ev_kind;     // kind of each recorded pair
   size_t ev_used = 0;
   // finish checks of the beam search: two pinned host words the done count is copied into, one event each
   int32_t* done_host = nullptr;
@@ -597,12 +600,14 @@ struct State {
   float* h;      // [L, N, H]
   float* c;
   float* feed;   // [N, H]
-  // bf16 models: h and feed as bf16 hi / lo planes, [L, N, pad(H)] and [N, pad(H)] (the operands of the
-  // decoder's products, split once by their producers)
+  // bf16 models: h and feed as their kPlanes bf16 term planes, [L, N, pad(H)] and [N, pad(H)] each (the
+  // operands of the decoder's products, split once by their producers)
   uint16_t* h_hi;
   uint16_t* h_lo;
+  uint16_t* h_lo2;
   uint16_t* feed_hi;
   uint16_t* feed_lo;
+  uint16_t* feed_lo2;
 };
 
 size_t state_layout(const Dims& d, int N, char* base, State* s) {
@@ -615,8 +620,10 @@ size_t state_layout(const Dims& d, int N, char* base, State* s) {
   const size_t pl = d.bf16 ? (size_t)N * d.pad(d.H) : 0;
   t.h_hi = d.bf16 ? c.take<uint16_t>(d.L * pl) : nullptr;
   t.h_lo = d.bf16 ? c.take<uint16_t>(d.L * pl) : nullptr;
+  t.h_lo2 = d.bf16 ? c.take<uint16_t>(d.L * pl) : nullptr;
   t.feed_hi = d.bf16 ? c.take<uint16_t>(pl) : nullptr;
   t.feed_lo = d.bf16 ? c.take<uint16_t>(pl) : nullptr;
+  t.feed_lo2 = d.bf16 ? c.take<uint16_t>(pl) : nullptr;
   if (s) *s = t;
   return align_up(c.off);
 }
@@ -723,8 +730,9 @@ struct ScoreWs {
   int32_t* want;       // [T, B] target predicted at step t
   int32_t* tlen;       // [B]
   float* feeds;        // [T, B, H] attentional vector of every step (the generator's input)
-  uint16_t* feeds_hi;  // bf16 models: [T, B, pad(H)] the same as bf16 hi + lo planes
+  uint16_t* feeds_hi;  // bf16 models: [T, B, pad(H)] each, the same as bf16 term planes
   uint16_t* feeds_lo;
+  uint16_t* feeds_lo2;
   float* gpmax;        // [T * B, ntiles] generator partials of all steps
   float* gpsum;
   float* want_logit;   // [T, B]
@@ -752,6 +760,7 @@ size_t score_layout(const Dims& d, int B, int S, int T, char* base, ScoreWs* w) 
   t.feeds = c.take<float>((size_t)T * B * d.H);
   t.feeds_hi = d.bf16 ? c.take<uint16_t>((size_t)T * B * d.pad(d.H)) : nullptr;
   t.feeds_lo = d.bf16 ? c.take<uint16_t>((size_t)T * B * d.pad(d.H)) : nullptr;
+  t.feeds_lo2 = d.bf16 ? c.take<uint16_t>((size_t)T * B * d.pad(d.H)) : nullptr;
   t.gpmax = c.take<float>((size_t)T * B * t.step.ntiles);
   t.gpsum = c.take<float>((size_t)T * B * t.step.ntiles);
   t.want_logit = c.take<float>((size_t)T * B);
@@ -1011,36 +1020,41 @@ int decode_init_compute(onmt_model* m, const EncWs& w, int B, int K, const State
   }
   HIP_TRY(fill_f32(s.feed, (size_t)N * d.H, 0.f, st));
   if (d.bf16) {   // the operand planes of the first step
-    HIP_TRY(split_rows(s.h, d.H, d.L * N, d.H, s.h_hi, s.h_lo, d.pad(d.H), st));
-    HIP_TRY(split_rows(s.feed, d.H, N, d.H, s.feed_hi, s.feed_lo, d.pad(d.H), st));
+    HIP_TRY(split_rows(s.h, d.H, d.L * N, d.H, s.h_hi, s.h_lo, s.h_lo2, d.pad(d.H), st));
+    HIP_TRY(split_rows(s.feed, d.H, N, d.H, s.feed_hi, s.feed_lo, s.feed_lo2, d.pad(d.H), st));
   }
   return ONMT_OK;
 }
 
-void time_begin(onmt_model* m, hipStream_t st) {
-  m->prof_open = false;
-  if (!m->prof || (m->prof_seq++ % m->prof) != 0) return;
+// Kernel timing: an event pair around every prof-th launch of each kind (ONMT_KERNEL_*), on the stream the
+// kernel is launched on; the pairs are read back by time_collect once the stream has been synchronized.
+void time_begin(onmt_model* m, hipStream_t st, int kind = ONMT_KERNEL_GENERATOR) {
+  m->prof_open[kind] = false;
+  if (!m->prof || (m->prof_seq[kind]++ % m->prof) != 0) return;
   while (m->ev.size() < m->ev_used + 2) {
     hipEvent_t e;
     // timing-only events: no system-scope fence, so recording them does not stall the next kernel
     if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return;
     m->ev.push_back(e);
   }
+  if (m->ev_kind.size() < m->ev.size()) m->ev_kind.resize(m->ev.size());
   hipEventRecord(m->ev[m->ev_used], st);
+  m->ev_kind[m->ev_used] = kind;
+  m->prof_pair[kind] = m->ev_used;
   m->ev_used += 2;
-  m->prof_open = true;
+  m->prof_open[kind] = true;
 }
-void time_end(onmt_model* m, hipStream_t st) {
-  if (!m->prof_open || m->ev_used < 2) return;
-  m->prof_open = false;
-  hipEventRecord(m->ev[m->ev_used - 1], st);
+void time_end(onmt_model* m, hipStream_t st, int kind = ONMT_KERNEL_GENERATOR) {
+  if (!m->prof_open[kind]) return;
+  m->prof_open[kind] = false;
+  hipEventRecord(m->ev[m->prof_pair[kind] + 1], st);
 }
 void time_collect(onmt_model* m) {
   for (size_t i = 0; i + 1 < m->ev_used; i += 2) {
     float ms = 0.f;
     if (hipEventSynchronize(m->ev[i + 1]) == hipSuccess && hipEventElapsedTime(&ms, m->ev[i], m->ev[i + 1]) == hipSuccess) {
-      m->prof_ms += ms;
-      m->prof_n += 1;
+      m->prof_ms[m->ev_kind[i]] += ms;
+      m->prof_n[m->ev_kind[i]] += 1;
     }
   }
   m->ev_used = 0;
@@ -1053,9 +1067,10 @@ void time_collect(onmt_model* m) {
 // all steps at once.
 // Optional work of a decoder step beyond the log-distribution.
 struct StepExtras {
-  // bf16 models: where the attentional vector's hi/lo planes go (default: the output state's)
+  // bf16 models: where the attentional vector's term planes go (default: the output state's)
   uint16_t* feed_hi = nullptr;
   uint16_t* feed_lo = nullptr;
+  uint16_t* feed_lo2 = nullptr;
   const int32_t* want = nullptr;        // the logit of column want[r] of every row goes to want_logit[r]
   float* want_logit = nullptr;
   const Coverage* cov = nullptr;        // attention coverage and its penalty
@@ -1077,10 +1092,11 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
   const size_t LP = (size_t)N * pH;
   // bf16 models read the pre-split planes of h and feed (widths that are multiples of 8)
   const bool pre = d.bf16 && d.H % 8 == 0;
-  auto act = [&](const float* x, const uint16_t* hi, const uint16_t* lo, const int32_t* idx) {
+  auto act = [&](const float* x, const uint16_t* hi, const uint16_t* lo, const uint16_t* lo2, const int32_t* idx) {
     if (!pre) return seg(x, idx, N, d.H, d.H, pH, 0);
     Seg s = seg(hi, idx, N, pH, d.H, pH, 1);
     s.lo = lo;
+    s.lo2 = lo2;
     return s;
   };
   for (int l = 0; l < d.L; ++l) {
@@ -1092,8 +1108,8 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     if (l == 0) {
       // [feed ; h] against the feed and recurrent columns; the embedding columns' product is the
       // precomputed row of the previous token (emb_gates), added in the epilogue
-      a.seg[0] = act(in.feed, in.feed_hi, in.feed_lo, parent);
-      a.seg[1] = act(in.h, in.h_hi, in.h_lo, parent);
+      a.seg[0] = act(in.feed, in.feed_hi, in.feed_lo, in.feed_lo2, parent);
+      a.seg[1] = act(in.h, in.h_hi, in.h_lo, in.h_lo2, parent);
       wb.W = (const char*)wb.W + (size_t)d.pad(d.E) * d.esz;
       lp.gx = m->emb_gates;
       lp.gx_idx = prev_tok;
@@ -1101,12 +1117,14 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
       lp.ld_gx = 4 * d.H_pad;
     } else {
       a.seg[0] = act(out.h + (l - 1) * LH, pre ? out.h_hi + (l - 1) * LP : nullptr,
-                     pre ? out.h_lo + (l - 1) * LP : nullptr, nullptr);
-      a.seg[1] = act(in.h + l * LH, pre ? in.h_hi + l * LP : nullptr, pre ? in.h_lo + l * LP : nullptr, parent);
+                     pre ? out.h_lo + (l - 1) * LP : nullptr, pre ? out.h_lo2 + (l - 1) * LP : nullptr, nullptr);
+      a.seg[1] = act(in.h + l * LH, pre ? in.h_hi + l * LP : nullptr, pre ? in.h_lo + l * LP : nullptr,
+                     pre ? in.h_lo2 + l * LP : nullptr, parent);
     }
     if (d.bf16) {
       lp.h_hi = out.h_hi + l * LP;
       lp.h_lo = out.h_lo + l * LP;
+      lp.h_lo2 = out.h_lo2 + l * LP;
       lp.ld_hl = pH;
     }
     lp.bias = m->dec_bias[l];
@@ -1117,7 +1135,9 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     lp.c_out = out.c + l * LH;
     lp.ld_out = d.H;
     lp.H = d.H;
+    if (timing) time_begin(m, st, ONMT_KERNEL_LSTM);
     HIP_TRY(gemm_lstm(d.bf16, lstm_shape(d, N, m->dec_w[l].Np), a, wb, lp, st));
+    if (timing) time_end(m, st, ONMT_KERNEL_LSTM);
   }
   const float* q = out.h + (d.L - 1) * LH;
   const float* sq = q;
@@ -1131,8 +1151,10 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     sq = sw.qproj;
   }
   const AttnExtra ax{ex.cov, ex.align};
+  if (timing) time_begin(m, st, ONMT_KERNEL_ATTENTION);
   HIP_TRY(attention(sq, d.H, w.keys, m->v_a, w.memory, w.lens, B, S, d.H, d.Hm, K, sw.scores, sw.ctx, attn, ax,
                     st));
+  if (timing) time_end(m, st, ONMT_KERNEL_ATTENTION);
   {
     AOp a{};
     a.M = N;
@@ -1143,9 +1165,12 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     if (d.bf16) {            // the generator's operand, split once here instead of in every column tile
       sp.hi = ex.feed_hi ? ex.feed_hi : out.feed_hi;
       sp.lo = ex.feed_lo ? ex.feed_lo : out.feed_lo;
+      sp.lo2 = ex.feed_lo2 ? ex.feed_lo2 : out.feed_lo2;
       sp.ld_hl = sp.ncols_hl = d.pad(d.H);
     }
+    if (timing) time_begin(m, st, ONMT_KERNEL_OUTPUT);
     HIP_TRY(gemm_store(d.bf16, small_shape(N, m->W_c.Np), a, bop(m->W_c), sp, st));
+    if (timing) time_end(m, st, ONMT_KERNEL_OUTPUT);
   }
   if (mode == 3) return ONMT_OK;
   {
@@ -1173,7 +1198,8 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     gp.pfmax = ex.pfmax;
     if (timing) time_begin(m, st);
     if (d.bf16)
-      HIP_TRY(gemm_gen_split(GenSplitA{out.feed_hi, out.feed_lo, N, d.pad(d.H), d.pad(d.H)}, bop(m->W_s), gp, st));
+      HIP_TRY(gemm_gen_split(GenSplitA{out.feed_hi, out.feed_lo, N, d.pad(d.H), d.pad(d.H), out.feed_lo2},
+                             bop(m->W_s), gp, st));
     else
       HIP_TRY(gemm_gen(0, a, bop(m->W_s), gp, st));
     if (timing) time_end(m, st);
@@ -1436,7 +1462,9 @@ int onmt_beam_search(onmt_model* m, const int32_t* src, const int32_t* len, int 
     rc = decode_compute(m, w.enc, B, S, K, w.st[cur], w.st[cur ^ 1], bp.tok, bp.parent, 2, nullptr, nullptr,
                         nullptr, nullptr, w.step, st, ex);
     if (rc) return rc;
+    time_begin(m, st, ONMT_KERNEL_BEAM);
     HIP_TRY(beam_step(bp, gp, t, st));
+    time_end(m, st, ONMT_KERNEL_BEAM);
     cur ^= 1;
     if (t < T && t % every == 0) {
       // this step's done count goes to the host asynchronously and the host waits only for the previous
@@ -1531,6 +1559,7 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
       if (d.bf16) {
         in.feed_hi = w.feeds_hi + (size_t)(t - 1) * B * d.pad(d.H);
         in.feed_lo = w.feeds_lo + (size_t)(t - 1) * B * d.pad(d.H);
+        in.feed_lo2 = w.feeds_lo2 + (size_t)(t - 1) * B * d.pad(d.H);
       }
     }
     out.feed = w.feeds + (size_t)t * B * d.H;
@@ -1538,6 +1567,7 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
     if (d.bf16) {
       ex.feed_hi = w.feeds_hi + (size_t)t * B * d.pad(d.H);
       ex.feed_lo = w.feeds_lo + (size_t)t * B * d.pad(d.H);
+      ex.feed_lo2 = w.feeds_lo2 + (size_t)t * B * d.pad(d.H);
     }
     rc = decode_compute(m, w.enc, B, S, 1, in, out, w.in_tok + (size_t)t * B, nullptr, 3, nullptr, nullptr, nullptr,
                         nullptr, w.step, st, ex);
@@ -1562,7 +1592,8 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
     gp.want_logit = w.want_logit;
     time_begin(m, st);
     if (d.bf16)
-      HIP_TRY(gemm_gen_split(GenSplitA{w.feeds_hi, w.feeds_lo, M, d.pad(d.H), d.pad(d.H)}, bop(m->W_s), gp, st));
+      HIP_TRY(gemm_gen_split(GenSplitA{w.feeds_hi, w.feeds_lo, M, d.pad(d.H), d.pad(d.H), w.feeds_lo2}, bop(m->W_s),
+                             gp, st));
     else
       HIP_TRY(gemm_gen(0, a, bop(m->W_s), gp, st));
     time_end(m, st);
@@ -1578,19 +1609,24 @@ int onmt_profile_enable(onmt_model* m, int every) {
   if (!m) return fail(ONMT_EINVAL, "model is NULL");
   if (every < 0) return fail(ONMT_EINVAL, "timing period must be >= 0");
   m->prof = every;
-  m->prof_seq = 0;
+  for (auto& q : m->prof_seq) q = 0;
+  return ONMT_OK;
+}
+
+int onmt_profile_read_kernel(onmt_model* m, int kind, int* n, double* ms, int reset) {
+  if (!m || !n || !ms) return fail(ONMT_EINVAL, "NULL argument");
+  if (kind < 0 || kind >= ONMT_KERNEL_KINDS) return fail(ONMT_EINVAL, "kernel kind %d unknown", kind);
+  *n = m->prof_n[kind];
+  *ms = m->prof_ms[kind];
+  if (reset) {
+    m->prof_n[kind] = 0;
+    m->prof_ms[kind] = 0.0;
+  }
   return ONMT_OK;
 }
 
 int onmt_profile_read(onmt_model* m, int* n, double* ms, int reset) {
-  if (!m || !n || !ms) return fail(ONMT_EINVAL, "NULL argument");
-  *n = m->prof_n;
-  *ms = m->prof_ms;
-  if (reset) {
-    m->prof_n = 0;
-    m->prof_ms = 0.0;
-  }
-  return ONMT_OK;
+  return onmt_profile_read_kernel(m, ONMT_KERNEL_GENERATOR, n, ms, reset);
 }
 
 }  // extern "C"

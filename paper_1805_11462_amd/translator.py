@@ -218,8 +218,10 @@ class Translator:
         """Time every ``every``-th generator launch of later searches (0 or False: off)."""
         check(self.lib.onmt_profile_enable(self.handle, int(every)))
 
-    def profile_read(self, reset=True):
+    def profile_read(self, reset=True, kind="generator"):
+        """(launches timed, their summed milliseconds) of one kernel kind since the last reset."""
         n = ctypes.c_int()
         ms = ctypes.c_double()
-        check(self.lib.onmt_profile_read(self.handle, ctypes.byref(n), ctypes.byref(ms), 1 if reset else 0))
+        check(self.lib.onmt_profile_read_kernel(self.handle, _lib.KERNEL_KINDS[kind], ctypes.byref(n),
+                                                ctypes.byref(ms), 1 if reset else 0))
         return n.value, ms.value

@@ -248,9 +248,10 @@ int onmt_score(onmt_model* model, const int32_t* src, const int32_t* len, int B,
                void* stream);
 
 /* ---- Kernel timing -----------------------------------------------------------------------------------
- * onmt_profile_enable(model, every): every >= 1 makes onmt_beam_search and onmt_score record HIP events
- * on `stream` around every `every`-th launch of each kind of kernel below (counting launches of each kind
- * from this call); 0 switches timing off; < 0 is ONMT_EINVAL. Kinds: the generator (the vocabulary
+ * onmt_profile_enable(model, every, kinds): every >= 1 makes onmt_beam_search and onmt_score record HIP
+ * events on `stream` around every `every`-th launch of each kind of kernel below whose bit
+ * (1 << ONMT_KERNEL_*) is set in `kinds` (counting launches of each kind from this call); every = 0
+ * switches timing off; every < 0, or kinds outside ONMT_KERNEL_ALL, is ONMT_EINVAL. Kinds: the generator (the vocabulary
  * projection with its fused log-softmax/top-K epilogue; the search launches it once per step, scoring
  * once over all steps), a decoder LSTM layer (GEMM with the gate/cell epilogue), the attention (scores
  * and context launches together), the attentional output tanh(W_c [ctx ; q]), and the beam step (search
@@ -258,8 +259,8 @@ int onmt_score(onmt_model* model, const int32_t* src, const int32_t* len, int B,
  * duration in milliseconds since its last reset; onmt_profile_read does so for the generator. Each timed
  * launch adds two event records to the stream. */
 enum { ONMT_KERNEL_GENERATOR = 0, ONMT_KERNEL_LSTM = 1, ONMT_KERNEL_ATTENTION = 2, ONMT_KERNEL_OUTPUT = 3,
-       ONMT_KERNEL_BEAM = 4, ONMT_KERNEL_KINDS = 5 };
-int onmt_profile_enable(onmt_model* model, int every);
+       ONMT_KERNEL_BEAM = 4, ONMT_KERNEL_KINDS = 5, ONMT_KERNEL_ALL = (1 << 5) - 1 };
+int onmt_profile_enable(onmt_model* model, int every, unsigned kinds);
 int onmt_profile_read(onmt_model* model, int* n_launches, double* total_ms, int reset);
 int onmt_profile_read_kernel(onmt_model* model, int kind, int* n_launches, double* total_ms, int reset);
 

@@ -6,13 +6,14 @@ library has not been built (``python -m paper_1805_11462_amd.build``); there is 
 
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_double, c_int, c_int64, c_size_t, c_void_p
+from ctypes import POINTER, c_char_p, c_double, c_int, c_int64, c_size_t, c_uint, c_void_p
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libonmt.so")
 
 ONMT_OK, ONMT_EINVAL, ONMT_ESIZE, ONMT_EDEVICE, ONMT_EUNSUPPORTED = 0, -1, -2, -3, -4
 ONMT_VALIDATE_HOST, ONMT_VALIDATE_DEVICE = 0, 1
 KERNEL_KINDS = {"generator": 0, "lstm": 1, "attention": 2, "output": 3, "beam_step": 4}
+KERNEL_ALL = (1 << len(KERNEL_KINDS)) - 1
 NOALLOC_SCRATCH_BYTES = 16 << 20
 ERROR_NAMES = {ONMT_EINVAL: "EINVAL", ONMT_ESIZE: "ESIZE", ONMT_EDEVICE: "EDEVICE", ONMT_EUNSUPPORTED: "EUNSUPPORTED"}
 
@@ -61,7 +62,7 @@ SIGNATURES = {
     "onmt_device_status": (c_int, [c_void_p, POINTER(c_int)]),
     "onmt_decode_step_noalloc": (c_int, [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p,
                                          c_void_p, c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
-    "onmt_profile_enable": (c_int, [c_void_p, c_int]),
+    "onmt_profile_enable": (c_int, [c_void_p, c_int, c_uint]),
     "onmt_profile_read": (c_int, [c_void_p, POINTER(c_int), POINTER(c_double), c_int]),
     "onmt_profile_read_kernel": (c_int, [c_void_p, c_int, POINTER(c_int), POINTER(c_double), c_int]),
 }

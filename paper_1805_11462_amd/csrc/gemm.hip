@@ -727,6 +727,13 @@ constexpr int kGenWN = 4;
 // per step, ~1e-5 on a logit over 1000-wide rows, instead of compounding over the steps the way an error
 // of the decoder layers' operands does. The third plane serves those layers.
 constexpr int kGenPlanes = 2;
+// Three weight planes (fp32 weights): 64 x 128 tiles (four waves, two 36 KB stages, two workgroups per
+// CU). At 320 rows the generator took 108 us against 121 us with 64 x 256 tiles (one workgroup per CU)
+// and 140 us with the fp32 MFMA kernel. Where the last 64-row tile would be at most half full, the fp32
+// kernel's 32-row tiles win instead (160 rows: 84 us against 88 us; 32-row tiles of the three-plane
+// kernel, two waves per workgroup and one wave per SIMD, took 140 us), so those row counts stay on it.
+constexpr int kGen3WN = 2;
+bool gemm_gen_split_rows(int M) { return !gen_rows32(M); }
 
 // One 16-byte-per-lane buffer load into LDS (lane l writes 16 bytes at lds + 16 l). (A function of its
 // own: called directly under control flow inside a kernel template, the builtin stops the host-side
@@ -745,20 +752,25 @@ constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | (((n 
 // stage) means its share of the oldest stage has landed; a barrier then makes the whole stage visible.
 // The barrier is the bare instruction: the fences of __syncthreads would also wait for the stages still
 // in flight. Fragment reads, products and the epilogue are those of the register-staged kernel.
-template <int WN, int NSTG, int NPL>
-__global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, GenParams p, int nm, int nblocks) {
-  using C = Tile<__bf16, 2, WN, 1, 2, 4, 32>;          // 64 x (64 WN) tile, waves of 32 x 64
-  using CE = TileGen16;                                 // the 64 x 128 sub-tiles the epilogue works on
-  static_assert(C::BM == 64 && C::BK == 32 && C::CPR == 4 && C::WK == 1 && CE::BN == 128 && C::BN % 128 == 0,
-                "the slice layout below is written for 64-row bf16 generator tiles with 64-byte rows");
+template <int WM, int WN, int NSTG, int NPA, int NPB>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, GenParams p, int nm,
+                                                              int nblocks) {
+  using C = Tile<__bf16, WM, WN, 1, 2, 4, 32>;         // (32 WM) x (64 WN) tile, waves of 32 x 64
+  using CE = Tile<__bf16, WM, 2, 1, 2, 4, 32>;          // the (32 WM) x 128 sub-tiles the epilogue works on
+  static_assert((C::BM == 32 || C::BM == 64) && C::BK == 32 && C::CPR == 4 && C::WK == 1 && CE::BN == 128 &&
+                    C::BN % 128 == 0 && CE::BM == C::BM,
+                "the slice layout below is written for 32- or 64-row bf16 generator tiles with 64-byte rows");
   static_assert(C::BK == kGenKBlock, "a K stage is one block of the K-blocked weights");
   constexpr int NW = C::NT / 64;
   constexpr int ROWB = C::BK * 2;                       // bytes per tile row
   constexpr int RPS = 16;                               // tile rows per 1 KB slice
   constexpr int SA = C::BM / RPS, SB = C::BN / RPS;     // slices per plane of A, and of B
-  constexpr int NSL = NPL * SA + SB;                    // slices per stage
+  constexpr int NSL = NPA * SA + NPB * SB;              // slices per stage
   constexpr int SPW = (NSL + NW - 1) / NW;              // slices (loads) per wave per stage, at most
-  constexpr int STG = (NPL * C::BM + C::BN) * ROWB;     // one stage: the A planes' rows, then B rows
+  constexpr int STG = (NPA * C::BM + NPB * C::BN) * ROWB;   // one stage: the A planes' rows, then B's
+  // term products kept: plane pair (pa, pb) with pa + pb < NPROD_MAX (two A planes against exact bf16
+  // weights; the six leading pairs of three planes each)
+  constexpr int NPROD_MAX = NPA > NPB ? NPA : NPB;
   constexpr int NSUB = C::BN / 128;
   constexpr int LDSB = NSTG * STG > NSUB * CE::CT ? NSTG * STG : NSUB * CE::CT;
   // waves may move different numbers of slices only when every wait is for all loads (two stages)
@@ -775,28 +787,31 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
   float cb[C::TN];
   gen_col_bias<C>(p, n0, wn, i16, cb);
 
-  // slice q of a stage: rows 16 q.. of A plane q / SA (q < NPL SA), then B rows; wave w moves slices
+  // slice q of a stage: rows 16 q.. of A plane q / SA (q < NPA SA), then of the B planes; wave w moves slices
   // w, w + NW, ... (below NSL); lane's place in a slice: tile row lane / 4, 16-byte slot lane % 4 (chunk
   // slot ^ swz)
   const int srow = lane >> 2, sslot = lane & 3;
-  static_assert(NPL >= 1 && NPL <= kPlanes, "the operand holds kPlanes term planes");
+  static_assert(NPA >= 1 && NPA <= kPlanes && (NPB == 1 || NPB == 3), "term planes of the operands");
   const __amdgpu_buffer_rsrc_t rpl[kPlanes] = {make_rsrc(a.hi, (uint32_t)a.M * a.ld * 2),
                                                make_rsrc(a.lo, (uint32_t)a.M * a.ld * 2),
                                                make_rsrc(a.lo2, (uint32_t)a.M * a.ld * 2)};
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(b.W, (uint32_t)b.Np * b.Kp * 2);
-  int sl_kind[SPW], sl_lds[SPW];                        // A plane (0 .. NPL - 1) or NPL (B), -1 none
+  const uint32_t wplane = (uint32_t)b.Np * b.Kp * 2;    // bytes per weight plane
+  __amdgpu_buffer_rsrc_t rw[NPB];
+#pragma unroll
+  for (int pb = 0; pb < NPB; ++pb) rw[pb] = make_rsrc((const char*)b.W + (size_t)pb * wplane, wplane);
+  int sl_kind[SPW], sl_lds[SPW];                        // A plane pa (pa), B plane pb (NPA + pb), -1 none
   uint32_t sl_off[SPW];                                 // lane's byte offset in its operand at K = 0
 #pragma unroll
   for (int i = 0; i < SPW; ++i) {
     const int q = wave + NW * i;
-    const int kind = q >= NSL ? -1 : (q < NPL * SA ? q / SA : NPL);
-    const int trow = (kind == NPL ? q - NPL * SA : q % SA) * RPS + srow;           // row in its plane
+    const int kind = q >= NSL ? -1 : (q < NPA * SA ? q / SA : NPA + (q - NPA * SA) / SB);
+    const int trow = (kind >= NPA ? (q - NPA * SA) % SB : q % SA) * RPS + srow;   // row in its plane
     const int chunk = sslot ^ C::swz(trow);
     sl_kind[i] = kind;
-    sl_lds[i] = ((kind == NPL ? NPL * C::BM : kind * C::BM) + trow - srow) * ROWB;
+    sl_lds[i] = ((kind >= NPA ? NPA * C::BM + (kind - NPA) * C::BN : kind * C::BM) + trow - srow) * ROWB;
     if (kind < 0) {
       sl_off[i] = 0;
-    } else if (kind == NPL) {                           // B rows past the packed matrix re-read its last row
+    } else if (kind >= NPA) {                           // B rows past the packed matrix re-read its last row
       const int br = min(n0 + trow, b.Np - 1);
       sl_off[i] = ((uint32_t)br * C::BK + chunk * C::CH) * 2;   // in K block 0 (the stage adds its block)
     } else {                                            // A rows past M re-read row M - 1 (never stored)
@@ -821,13 +836,17 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
     const uint32_t ks_ = (uint32_t)((ST) < nst ? (ST) : nst - 1);                                       \
     const uint32_t ko_ = ks_ * ROWB, kb_ = ks_ * (uint32_t)b.Np * ROWB;                                 \
     _Pragma("unroll") for (int i = 0; i < SPW; ++i) {                                                   \
-      if (sl_kind[i] == NPL)                                                                        \
-        dma16(rw, sb_ + sl_lds[i], sl_off[i] + kb_);                                                   \
+      if (sl_kind[i] == NPA)                                                                            \
+        dma16(rw[0], sb_ + sl_lds[i], sl_off[i] + kb_);                                                 \
+      else if (NPB > 1 && sl_kind[i] == NPA + 1)                                                        \
+        dma16(rw[NPB > 1 ? 1 : 0], sb_ + sl_lds[i], sl_off[i] + kb_);                                   \
+      else if (NPB > 2 && sl_kind[i] == NPA + 2)                                                        \
+        dma16(rw[NPB > 2 ? 2 : 0], sb_ + sl_lds[i], sl_off[i] + kb_);                                   \
       else if (sl_kind[i] == 0)                                                                         \
         dma16(rpl[0], sb_ + sl_lds[i], sl_off[i] + ko_);                                               \
       else if (sl_kind[i] == 1)                                                                         \
         dma16(rpl[1], sb_ + sl_lds[i], sl_off[i] + ko_);                                               \
-      else if (sl_kind[i] == 2)                                                                         \
+      else if (NPA > 2 && sl_kind[i] == 2)                                                              \
         dma16(rpl[2], sb_ + sl_lds[i], sl_off[i] + ko_);                                               \
     }                                                                                                   \
   } while (0)
@@ -841,27 +860,33 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_gen_lds(GenSplitA a, BOp b, G
     ONMT_GEN_ISSUE(st + NSTG - 1);                      // refills the buffer multiplied at st - 1
     const char* base = smem + (st % NSTG) * STG;
     const __bf16* Ah = (const __bf16*)base + (wm * C::TM * 16 + i16) * C::ROW;
-    const __bf16* Bb = (const __bf16*)base + (NPL * C::BM + wn * C::TN * 16 + i16) * C::ROW;
-    bf16x8 av[C::TM], bv[C::TN];
+    const __bf16* Bb = (const __bf16*)base + (NPA * C::BM + wn * C::TN * 16 + i16) * C::ROW;
+    bf16x8 av[C::TM], bv[NPB][C::TN];
 #pragma unroll
-    for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + col);
+    for (int pb = 0; pb < NPB; ++pb)
 #pragma unroll
-    for (int pl = 0; pl < NPL; ++pl) {
+      for (int y = 0; y < C::TN; ++y) bv[pb][y] = *(const bf16x8*)(Bb + (pb * C::BN + y * 16) * C::ROW + col);
 #pragma unroll
-      for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + (pl * C::BM + x * 16) * C::ROW + col);
+    for (int pa = 0; pa < NPA; ++pa) {
 #pragma unroll
-      for (int x = 0; x < C::TM; ++x)
+      for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + (pa * C::BM + x * 16) * C::ROW + col);
 #pragma unroll
-        for (int y = 0; y < C::TN; ++y)
-          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+      for (int pb = 0; pb < NPB; ++pb) {
+        if (pa + pb >= NPROD_MAX) continue;
+#pragma unroll
+        for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+          for (int y = 0; y < C::TN; ++y)
+            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[pb][y], acc[x][y], 0, 0, 0);
+      }
     }
   }
 #undef ONMT_GEN_ISSUE
   // every load (including the re-loads past the end) has landed before the output tiles reuse the buffers
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   __syncthreads();
-  // the 64 x BN output as BN / 128 sub-tiles of 64 x 128, each in the epilogue's layout, reduced at once
-  // (threads 256 s .. 256 s + 255 take sub-tile s, one partials tile of 128 columns); staging the
+  // the BM x BN output as BN / 128 sub-tiles of BM x 128, each in the epilogue's layout, reduced at once
+  // (threads CE::NT s .. take sub-tile s, one partials tile of 128 columns); staging the
   // sub-tiles one after the other through one buffer measured far slower
   {
     const int sub = (wn * C::TN * 16) / 128, c0 = (wn * C::TN * 16) % 128;
@@ -1186,17 +1211,22 @@ hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hi
   return gen_rows32(a.M) ? launch_gen<float, TileGen32h>(a, b, p, st) : launch_gen<float, TileGen32>(a, b, p, st);
 }
 
-hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, const GenParams& p, hipStream_t st) {
-  constexpr int BM = 64, BN = 64 * kGenWN;
+hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, int b_planes, const GenParams& p, hipStream_t st) {
+  if (b_planes != 1 && b_planes != 3) return hipErrorInvalidValue;
   const uint64_t lim = 1ull << 31;
   // the K-blocked weights are read up to the operand's padded width: a.kpad == b.Kp
   if (a.M < 1 || a.kpad % kSegK || a.kpad != b.Kp || a.ld < a.kpad || b.Np % 128 ||
       (uint64_t)a.M * a.ld * 2 >= lim || (uint64_t)b.Np * b.Kp * 2 >= lim)
     return hipErrorInvalidValue;
-  const int nm = (a.M + BM - 1) / BM;
-  const int nblocks = nm * ((b.Np + BN - 1) / BN);
-  hipLaunchKernelGGL((k_gemm_gen_lds<kGenWN, kGenStages, kGenPlanes>), dim3(nblocks), dim3(128 * kGenWN), 0, st, a, b, p, nm,
-                     nblocks);
+  auto launch = [&](auto kernel, int BM, int BN, int threads) {
+    const int nm = (a.M + BM - 1) / BM;
+    const int nblocks = nm * ((b.Np + BN - 1) / BN);
+    hipLaunchKernelGGL(kernel, dim3(nblocks), dim3(threads), 0, st, a, b, p, nm, nblocks);
+  };
+  if (b_planes == 1)
+    launch(k_gemm_gen_lds<2, kGenWN, kGenStages, kGenPlanes, 1>, 64, 64 * kGenWN, 128 * kGenWN);
+  else
+    launch(k_gemm_gen_lds<2, kGen3WN, kGenStages, kPlanes, 3>, 64, 64 * kGen3WN, 128 * kGen3WN);
   return hipGetLastError();
 }
 

@@ -136,13 +136,20 @@ struct GenSplitA {
   int kpad;    // multiple of kSegK
   const uint16_t* lo2;
 };
-// The bf16 generator on a pre-split operand, operands moved straight into LDS. It multiplies the first two
-// term planes only (A ~ hi + lo; lo2 is not read): its logits do not feed back into the decoder.
+// The generator on a pre-split operand, operands moved straight into LDS, the weights given as b_planes
+// bf16 term planes (plane p of the K-blocked [Np, Kp] matrix at element offset p * Np * Kp).
+// b_planes = 1 (bf16 weights): the first two term planes of A are multiplied (A ~ hi + lo; lo2 is not
+// read), since the logits do not feed back into the decoder. b_planes = 3 (fp32 weights as three bf16
+// terms): the six term products whose order of magnitude is at least 2^-16 of the leading one
+// (hi.hi, hi.lo, lo.hi, lo.lo, hi.lo2, lo2.hi), accumulated in fp32: the six-product bf16 scheme of
+// Henry, Tang and Heinecke (ARITH 2019), whose dropped products lie below one fp32 rounding.
 // Its weights are K-blocked: element (n, k) of the [Np, Kp] matrix sits at (k / kGenKBlock) * Np *
 // kGenKBlock + n * kGenKBlock + k % kGenKBlock, so that one K stage of a column tile is one contiguous block
 // (with row-major weights each load instruction touched 16 rows 2 KB apart for 64 bytes each).
 constexpr int kGenKBlock = 32;
-hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, const GenParams& p, hipStream_t st);
+hipError_t gemm_gen_split(const GenSplitA& a, const BOp& b, int b_planes, const GenParams& p, hipStream_t st);
+// fp32 models: whether M rows take the three-plane generator (else the fp32 MFMA kernel, gemm_gen).
+bool gemm_gen_split_rows(int M);
 int gen_tile_cols();
 
 // Attention coverage of the hypotheses (optional): out[r, s] = in[parent[r], s] + a[r, s] for the real

@@ -88,6 +88,11 @@ struct Dims {
   bool bf16;
   int esz;             // operand element size
   int attn;            // ONMT_ATTN_GENERAL / _DOT / _CONCAT
+  // The generator's weights packed K-blocked as gwp bf16 term planes (bf16 models: 1, their exact values;
+  // fp32 models: 3, each fp32 value as the sum of three bf16 terms, multiplied in six term products),
+  // read with the attentional vector's term planes (split by the W_c epilogue). fp32 models also keep
+  // the fp32 matrix for the row counts where the fp32 MFMA kernel is faster (gemm_gen_split_rows).
+  int gwp;
   // Every K segment of a GEMM operand is padded to a multiple of kSegK so that no K stage of any tile
   // shape straddles two segments.
   int pad(int w) const { return ceil_to(w, kSegK); }
@@ -108,6 +113,7 @@ bool dims_of(const onmt_config* c, Dims* d) {
   d->bf16 = c->wdtype == 1;
   d->esz = d->bf16 ? 2 : 4;
   d->attn = c->attn_type;
+  d->gwp = d->bf16 ? 1 : 3;
   return true;
 }
 
@@ -210,6 +216,7 @@ struct onmt_model {
   Packed W_q;                              // concat: the query columns of W_a
   const float* v_a = nullptr;              // concat [H]
   Packed W_c, W_s;
+  Packed W_s32;        // fp32 models: the generator's fp32 weights, row-major
   const float* b_s = nullptr;
   // decoder layer 0's input-projection rows for every target token, E_tgt[v] W_e^T in the packed (gate-
   // blocked) column order, fp32 [Vt, 4 H_pad]; computed on the device when the model is created
@@ -217,6 +224,7 @@ struct onmt_model {
   size_t image_bytes = 0;    // the uploaded part of the model buffer (everything before emb_gates)
   // kernel timing
   int prof = 0;              // time every prof-th generator launch (0: off)
+  unsigned prof_kinds = 0;                      // bit k: launches of kind k are timed
   long long prof_seq[ONMT_KERNEL_KINDS] = {};   // launches of each kind seen while timing is on
   bool prof_open[ONMT_KERNEL_KINDS] = {};       // the current launch of the kind has a start event
   size_t prof_pair[ONMT_KERNEL_KINDS] = {};     // ... recorded as event pair ev[prof_pair], ev[prof_pair + 1]
@@ -284,7 +292,15 @@ size_t model_layout(const onmt_config* c, onmt_model* m, std::vector<uint64_t>* 
   Packed wq = d.attn == ONMT_ATTN_CONCAT ? mat(ceil_to(d.H, 128), d.pad(d.H)) : Packed{};
   const size_t va = d.attn == ONMT_ATTN_CONCAT ? vec(d.H) : 0;
   Packed wc = mat(ceil_to(d.H, 128), d.pad(d.Hm) + d.pad(d.H));
-  Packed ws = mat(ceil_to(d.Vt, 128), d.pad(d.H));
+  Packed ws;         // K-blocked bf16 planes, each read through its own descriptor
+  cv.off = align_up(cv.off);
+  ws.off = cv.off;
+  ws.Np = ceil_to(d.Vt, 128);
+  ws.Kp = d.pad(d.H);
+  const uint64_t plane = (uint64_t)ws.Np * ws.Kp * 2;
+  cv.off += plane * d.gwp;
+  if (mats) mats->push_back(plane);
+  Packed ws32 = d.bf16 ? Packed{} : mat(ceil_to(d.Vt, 128), d.pad(d.H));
   size_t bs = vec(ceil_to(d.Vt, 128));
   const size_t image = align_up(cv.off);
   const size_t eg = vec((size_t)d.Vt * 4 * d.H_pad);
@@ -310,6 +326,7 @@ size_t model_layout(const onmt_config* c, onmt_model* m, std::vector<uint64_t>* 
     }
     m->W_c = fix(wc);
     m->W_s = fix(ws);
+    if (!d.bf16) m->W_s32 = fix(ws32);
     m->b_s = (const float*)(base + bs);
     m->emb_gates = (float*)(base + eg);
     m->image_bytes = image;
@@ -499,15 +516,22 @@ int onmt_model_create(const onmt_config* cfg, const float* const* host_weights, 
       pack_row(img, m->W_c, r, d.pad(d.Hm), Wc + (size_t)r * (d.Hm + d.H), d.Hm, d.H);
     }
     const float* Ws = host_weights[wi++];
-    if (d.bf16) {   // K-blocked for the pre-split generator (see gemm_gen_split)
-      const size_t o = m->W_s.off, Np = (size_t)m->W_s.Np;
+    {   // K-blocked bf16 term planes for the pre-split generator (see gemm_gen_split)
+      const size_t Np = (size_t)m->W_s.Np, plane = Np * m->W_s.Kp;
+      uint16_t* o = (uint16_t*)(img.buf.data() + m->W_s.off);
       for (int r = 0; r < d.Vt; ++r)
-        for (int k = 0; k < d.H; ++k)
-          img.put(o, (size_t)(k / kGenKBlock) * Np * kGenKBlock + (size_t)r * kGenKBlock + k % kGenKBlock,
-                  Ws[(size_t)r * d.H + k]);
-    } else {
-      for (int r = 0; r < d.Vt; ++r) pack_row(img, m->W_s, r, 0, Ws + (size_t)r * d.H, 0, d.H);
+        for (int k = 0; k < d.H; ++k) {
+          const size_t at = (size_t)(k / kGenKBlock) * Np * kGenKBlock + (size_t)r * kGenKBlock + k % kGenKBlock;
+          float x = Ws[(size_t)r * d.H + k];
+          for (int p = 0; p < d.gwp; ++p) {   // RNE of the value, then of each remainder
+            const uint16_t t = f32_to_bf16_bits(x);
+            o[p * plane + at] = t;
+            x -= host_bf16_to_f32(t);
+          }
+        }
     }
+    if (!d.bf16)
+      for (int r = 0; r < d.Vt; ++r) pack_row(img, m->W_s32, r, 0, Ws + (size_t)r * d.H, 0, d.H);
     const float* bs = host_weights[wi++];
     const size_t bo = off_of(m->b_s);
     for (int r = 0; r < d.Vt; ++r) img.putf(bo, r, bs[r]);
@@ -617,13 +641,13 @@ size_t state_layout(const Dims& d, int N, char* base, State* s) {
   t.h = c.take<float>((size_t)d.L * N * d.H);
   t.c = c.take<float>((size_t)d.L * N * d.H);
   t.feed = c.take<float>((size_t)N * d.H);
-  const size_t pl = d.bf16 ? (size_t)N * d.pad(d.H) : 0;
+  const size_t pl = (size_t)N * d.pad(d.H);
   t.h_hi = d.bf16 ? c.take<uint16_t>(d.L * pl) : nullptr;
   t.h_lo = d.bf16 ? c.take<uint16_t>(d.L * pl) : nullptr;
   t.h_lo2 = d.bf16 ? c.take<uint16_t>(d.L * pl) : nullptr;
-  t.feed_hi = d.bf16 ? c.take<uint16_t>(pl) : nullptr;
-  t.feed_lo = d.bf16 ? c.take<uint16_t>(pl) : nullptr;
-  t.feed_lo2 = d.bf16 ? c.take<uint16_t>(pl) : nullptr;
+  t.feed_hi = c.take<uint16_t>(pl);
+  t.feed_lo = c.take<uint16_t>(pl);
+  t.feed_lo2 = c.take<uint16_t>(pl);
   if (s) *s = t;
   return align_up(c.off);
 }
@@ -758,9 +782,9 @@ size_t score_layout(const Dims& d, int B, int S, int T, char* base, ScoreWs* w) 
   t.want = c.take<int32_t>((size_t)T * B);
   t.tlen = c.take<int32_t>(B);
   t.feeds = c.take<float>((size_t)T * B * d.H);
-  t.feeds_hi = d.bf16 ? c.take<uint16_t>((size_t)T * B * d.pad(d.H)) : nullptr;
-  t.feeds_lo = d.bf16 ? c.take<uint16_t>((size_t)T * B * d.pad(d.H)) : nullptr;
-  t.feeds_lo2 = d.bf16 ? c.take<uint16_t>((size_t)T * B * d.pad(d.H)) : nullptr;
+  t.feeds_hi = c.take<uint16_t>((size_t)T * B * d.pad(d.H));
+  t.feeds_lo = c.take<uint16_t>((size_t)T * B * d.pad(d.H));
+  t.feeds_lo2 = c.take<uint16_t>((size_t)T * B * d.pad(d.H));
   t.gpmax = c.take<float>((size_t)T * B * t.step.ntiles);
   t.gpsum = c.take<float>((size_t)T * B * t.step.ntiles);
   t.want_logit = c.take<float>((size_t)T * B);
@@ -1030,7 +1054,7 @@ int decode_init_compute(onmt_model* m, const EncWs& w, int B, int K, const State
 // kernel is launched on; the pairs are read back by time_collect once the stream has been synchronized.
 void time_begin(onmt_model* m, hipStream_t st, int kind = ONMT_KERNEL_GENERATOR) {
   m->prof_open[kind] = false;
-  if (!m->prof || (m->prof_seq[kind]++ % m->prof) != 0) return;
+  if (!m->prof || !((m->prof_kinds >> kind) & 1u) || (m->prof_seq[kind]++ % m->prof) != 0) return;
   while (m->ev.size() < m->ev_used + 2) {
     hipEvent_t e;
     // timing-only events: no system-scope fence, so recording them does not stall the next kernel
@@ -1162,7 +1186,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     a.seg[0] = seg(sw.ctx, nullptr, N, d.Hm, d.Hm, d.pad(d.Hm), 0);
     a.seg[1] = seg(q, nullptr, N, d.H, d.H, d.pad(d.H), 0);
     StoreParams sp{nullptr, out.feed, d.H, d.H, 1};
-    if (d.bf16) {            // the generator's operand, split once here instead of in every column tile
+    {                        // the generator's operand, split once here instead of in every column tile
       sp.hi = ex.feed_hi ? ex.feed_hi : out.feed_hi;
       sp.lo = ex.feed_lo ? ex.feed_lo : out.feed_lo;
       sp.lo2 = ex.feed_lo2 ? ex.feed_lo2 : out.feed_lo2;
@@ -1197,11 +1221,11 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
     gp.max_unk = ex.max_unk;
     gp.pfmax = ex.pfmax;
     if (timing) time_begin(m, st);
-    if (d.bf16)
+    if (d.bf16 || gemm_gen_split_rows(N))
       HIP_TRY(gemm_gen_split(GenSplitA{out.feed_hi, out.feed_lo, N, d.pad(d.H), d.pad(d.H), out.feed_lo2},
-                             bop(m->W_s), gp, st));
+                             bop(m->W_s), d.gwp, gp, st));
     else
-      HIP_TRY(gemm_gen(0, a, bop(m->W_s), gp, st));
+      HIP_TRY(gemm_gen(0, a, bop(m->W_s32), gp, st));
     if (timing) time_end(m, st);
   }
   if (mode == 2) return ONMT_OK;
@@ -1564,7 +1588,7 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
     }
     out.feed = w.feeds + (size_t)t * B * d.H;
     StepExtras ex;
-    if (d.bf16) {
+    {
       ex.feed_hi = w.feeds_hi + (size_t)t * B * d.pad(d.H);
       ex.feed_lo = w.feeds_lo + (size_t)t * B * d.pad(d.H);
       ex.feed_lo2 = w.feeds_lo2 + (size_t)t * B * d.pad(d.H);
@@ -1591,11 +1615,11 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
     gp.want = w.want;
     gp.want_logit = w.want_logit;
     time_begin(m, st);
-    if (d.bf16)
+    if (d.bf16 || gemm_gen_split_rows(M))
       HIP_TRY(gemm_gen_split(GenSplitA{w.feeds_hi, w.feeds_lo, M, d.pad(d.H), d.pad(d.H), w.feeds_lo2}, bop(m->W_s),
-                             gp, st));
+                             d.gwp, gp, st));
     else
-      HIP_TRY(gemm_gen(0, a, bop(m->W_s), gp, st));
+      HIP_TRY(gemm_gen(0, a, bop(m->W_s32), gp, st));
     time_end(m, st);
     HIP_TRY(score_rows(w.gpmax, w.gpsum, w.step.ntiles, w.want_logit, w.tlen, B, steps, out_logp, T, w.nll, st));
   }
@@ -1605,10 +1629,12 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
   return ONMT_OK;
 }
 
-int onmt_profile_enable(onmt_model* m, int every) {
+int onmt_profile_enable(onmt_model* m, int every, unsigned kinds) {
   if (!m) return fail(ONMT_EINVAL, "model is NULL");
   if (every < 0) return fail(ONMT_EINVAL, "timing period must be >= 0");
+  if (kinds & ~(unsigned)ONMT_KERNEL_ALL) return fail(ONMT_EINVAL, "kernel kind mask 0x%x unknown", kinds);
   m->prof = every;
+  m->prof_kinds = kinds;
   for (auto& q : m->prof_seq) q = 0;
   return ONMT_OK;
 }

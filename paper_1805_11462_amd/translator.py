@@ -214,9 +214,12 @@ class Translator:
         return buf["logp"], buf["nll"]
 
     # ---------------------------------------------------------------- timing
-    def profile(self, every):
-        """Time every ``every``-th generator launch of later searches (0 or False: off)."""
-        check(self.lib.onmt_profile_enable(self.handle, int(every)))
+    def profile(self, every, kinds=("generator",)):
+        """Time every ``every``-th launch of each listed kernel kind in later searches (0 or False: off)."""
+        mask = 0
+        for k in kinds:
+            mask |= 1 << _lib.KERNEL_KINDS[k]
+        check(self.lib.onmt_profile_enable(self.handle, int(every), mask))
 
     def profile_read(self, reset=True, kind="generator"):
         """(launches timed, their summed milliseconds) of one kernel kind since the last reset."""

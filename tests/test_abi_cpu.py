@@ -84,6 +84,7 @@ def test_null_handles_are_rejected_without_a_device():
     n = ctypes.c_int()
     ms = ctypes.c_double()
     assert lib.onmt_profile_read(None, ctypes.byref(n), ctypes.byref(ms), 0) == _lib.ONMT_EINVAL
+    assert lib.onmt_profile_enable(None, 1, _lib.KERNEL_ALL) == _lib.ONMT_EINVAL
 
 
 def test_model_create_rejects_bad_arguments_before_touching_memory():
@@ -124,8 +125,11 @@ def test_library_resolves_every_kernel_it_launches():
     ("fp32", "src_vocab_emb", (1 << 20, 500), (1 << 20, 512)),
     # the same table in bf16: 2^20 x 1016 fits, 2^20 x 1024 does not
     ("bf16", "src_vocab_emb", (1 << 20, 1016), (1 << 20, 1024)),
-    # W_s [tgt_vocab, pad(hidden)]: 131072 x 3968 fp32 fits; hidden 4000 pads to 4096 columns = 2^31 bytes
+    # W_s [tgt_vocab, pad(hidden)]: fp32 models keep it in fp32 (131072 x 3968 fits; hidden 4000 pads to
+    # 4096 columns = 2^31 bytes) besides its bf16 term planes, one descriptor each (131072 x 8064 x 2 bytes
+    # fits, hidden 8100 pads to 8192 columns = 2^31 bytes)
     ("fp32", "tgt_vocab_hidden", (131072, 3968), (131072, 4000)),
+    ("bf16", "tgt_vocab_hidden", (131072, 8064), (131072, 8100)),
 ])
 def test_operands_past_the_descriptor_limit_are_refused(wdtype, field, ok, too_big):
     # buffer descriptors address at most 2 GiB: a config whose embedding table or packed weight matrix

@@ -189,3 +189,35 @@ def test_workspace_operands_past_the_descriptor_limit_are_refused():
     # and a batch below the limit is unaffected
     buf = _search(s, 2, 4)
     assert (buf["len"].cpu().numpy() >= 1).all()
+
+
+def test_kernel_timing_follows_the_kind_mask():
+    # timing is a side channel: the searches' outputs do not change, and only the selected kinds are timed
+    s = Custom(TINY, [3, 10, 5, 1])
+    _case("kernel_timing_mask")
+    K, T = 2, 6
+    ref = _search(s, K, T)
+    kinds = ("generator", "lstm", "attention", "output", "beam_step")
+    for sel in (("lstm",), ("generator", "beam_step"), kinds):
+        s.tr.profile(1, kinds=sel)
+        for k in kinds:
+            s.tr.profile_read(reset=True, kind=k)
+        buf = _search(s, K, T)
+        got = {k: s.tr.profile_read(reset=True, kind=k) for k in kinds}
+        s.tr.profile(False)
+        for k in kinds:
+            n, ms = got[k]
+            if k in sel:
+                assert n > 0 and ms > 0, (sel, k)
+            else:
+                assert n == 0 and ms == 0, (sel, k)
+        for key in ("tok", "len", "raw", "norm"):
+            assert torch.equal(buf[key], ref[key]), key
+    # every decode step runs each decoder layer once (the tiny model has one): as many LSTM launches as
+    # generator launches
+    s.tr.profile(1, kinds=("generator", "lstm"))
+    _search(s, K, T)
+    n_gen = s.tr.profile_read(reset=True, kind="generator")[0]
+    n_lstm = s.tr.profile_read(reset=True, kind="lstm")[0]
+    s.tr.profile(False)
+    assert n_lstm == n_gen * TINY.dec_layers

@@ -757,9 +757,9 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_gen_lds(GenSplitA a, BOp 
                                                               int nblocks) {
   using C = Tile<__bf16, WM, WN, 1, 2, 4, 32>;         // (32 WM) x (64 WN) tile, waves of 32 x 64
   using CE = Tile<__bf16, WM, 2, 1, 2, 4, 32>;          // the (32 WM) x 128 sub-tiles the epilogue works on
-  static_assert((C::BM == 32 || C::BM == 64) && C::BK == 32 && C::CPR == 4 && C::WK == 1 && CE::BN == 128 &&
+  static_assert(C::BM % 16 == 0 && C::BK == 32 && C::CPR == 4 && C::WK == 1 && CE::BN == 128 &&
                     C::BN % 128 == 0 && CE::BM == C::BM,
-                "the slice layout below is written for 32- or 64-row bf16 generator tiles with 64-byte rows");
+                "the slice layout below is written for bf16 generator tiles of 16-row slices with 64-byte rows");
   static_assert(C::BK == kGenKBlock, "a K stage is one block of the K-blocked weights");
   constexpr int NW = C::NT / 64;
   constexpr int ROWB = C::BK * 2;                       // bytes per tile row

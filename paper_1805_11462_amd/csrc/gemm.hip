@@ -405,7 +405,7 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
 constexpr int kLstmStages = 2;
 template <class C>
 constexpr int dma_lds() {
-  constexpr int stg = (kPlanes * C::BM + C::BN) * C::BK * 2;
+  constexpr int stg = ((C::kBf16 ? kPlanes : 1) * C::BM + C::BN) * C::BK * (C::kBf16 ? 2 : 4);
   return kLstmStages * stg > C::CT ? kLstmStages * stg : C::CT;
 }
 
@@ -908,8 +908,9 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_gen_lds(GenSplitA a, BOp 
 // Vector-memory "no wait", LDS wait until nothing is outstanding (for LDS stores before a bare barrier).
 constexpr int kWaitLgkm0 = 15 | (7 << 4) | (0 << 8) | (3 << 14);
 
-// gemm_tile for bf16 products whose A segments (one or two) are all pre-split term planes, with the
-// operands moved straight into LDS: a stage of the A rows of every plane and the B rows is sliced into 1 KB pieces
+// gemm_tile for fp32 products, or bf16 products whose A segments (one or two) are all pre-split term
+// planes, with the operands moved straight into LDS: a stage of the A rows of every plane (fp32: one) and
+// the B rows is sliced into 1 KB pieces
 // (RPS tile rows each; lane l writes row l / (ROWB / 16), 16-byte slot l % (ROWB / 16)), kLstmStages stages
 // in flight, waits and bare barriers as in k_gemm_gen_lds. A rows come through the segment's row map
 // (beam parents) and rows past M re-read row M - 1. The planes' columns past a segment's width are not
@@ -917,11 +918,13 @@ constexpr int kWaitLgkm0 = 15 | (7 << 4) | (0 << 8) | (3 << 14);
 // their order and the output tile (WK partial planes) are those of gemm_tile, so the results are equal.
 template <class C, int NSEG>
 __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0, char* smem) {
-  static_assert(C::kBf16 && C::KW == C::KSUB && NSEG >= 1 && NSEG <= 2, "one MFMA K step per wave and stage");
-  constexpr int NW = C::NT / 64, ROWB = C::BK * 2, RPS = 1024 / ROWB, LPR = ROWB / 16;
-  constexpr int SA = C::BM / RPS, SB = C::BN / RPS, SPW = (kPlanes * SA + SB) / NW;
-  constexpr int STG = (kPlanes * C::BM + C::BN) * ROWB, NSTG = kLstmStages;
-  static_assert(1024 % ROWB == 0 && C::BM % RPS == 0 && C::BN % RPS == 0 && (kPlanes * SA + SB) % NW == 0 &&
+  static_assert(C::KW == C::KSUB && NSEG >= 1 && NSEG <= 2, "one MFMA K step per wave and stage");
+  // bf16 products: kPlanes term planes of A; fp32 products: A itself
+  constexpr int ES = C::kBf16 ? 2 : 4, NPA = C::kBf16 ? kPlanes : 1;
+  constexpr int NW = C::NT / 64, ROWB = C::BK * ES, RPS = 1024 / ROWB, LPR = ROWB / 16;
+  constexpr int SA = C::BM / RPS, SB = C::BN / RPS, SPW = (NPA * SA + SB) / NW;
+  constexpr int STG = (NPA * C::BM + C::BN) * ROWB, NSTG = kLstmStages;
+  static_assert(1024 % ROWB == 0 && C::BM % RPS == 0 && C::BN % RPS == 0 && (NPA * SA + SB) % NW == 0 &&
                     SPW * (NSTG - 2) < 64 && dma_lds<C>() >= NSTG * STG,
                 "slice layout");
   // the wave index read into a scalar register: slice kinds derived from it are then known to be uniform,
@@ -930,16 +933,16 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
   const int i16 = lane & 15, g = lane >> 4;
   const int wk = wave % C::WK, wn = (wave / C::WK) % C::WN, wm = wave / (C::WK * C::WN);
   const int srow = lane / LPR, sslot = lane % LPR;
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(b.W, (uint32_t)b.Np * b.Kp * 2);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(b.W, (uint32_t)b.Np * b.Kp * ES);
   // per segment (constant indices only): plane descriptors, stage count, width
   __amdgpu_buffer_rsrc_t rp[2][kPlanes];
   int nst[2] = {0, 0}, wd[2] = {0, 0};
 #pragma unroll
   for (int s = 0; s < NSEG; ++s) {
-    const uint32_t bytes = (uint32_t)a.seg[s].rows * a.seg[s].ld * 2;
+    const uint32_t bytes = (uint32_t)a.seg[s].rows * a.seg[s].ld * ES;
     rp[s][0] = make_rsrc(a.seg[s].base, bytes);
-    rp[s][1] = make_rsrc(a.seg[s].lo, bytes);
-    rp[s][2] = make_rsrc(a.seg[s].lo2, bytes);
+    rp[s][1] = NPA > 1 ? make_rsrc(a.seg[s].lo, bytes) : rp[s][0];
+    rp[s][2] = NPA > 2 ? make_rsrc(a.seg[s].lo2, bytes) : rp[s][0];
     nst[s] = a.seg[s].kpad / C::BK;
     wd[s] = a.seg[s].width;
   }
@@ -950,19 +953,19 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
 #pragma unroll
   for (int i = 0; i < SPW; ++i) {
     const int q = wave + NW * i;
-    const int kind = q < kPlanes * SA ? q / SA : kPlanes;   // an A plane, or kPlanes for B
-    const int trow = (kind == kPlanes ? q - kPlanes * SA : q % SA) * RPS + srow;
+    const int kind = q < NPA * SA ? q / SA : NPA;           // an A plane, or NPA for B
+    const int trow = (kind == NPA ? q - NPA * SA : q % SA) * RPS + srow;
     const int chunk = sslot ^ C::swz(trow);
     sl_kind[i] = kind;
-    sl_lds[i] = ((kind == kPlanes ? kPlanes * C::BM : kind * C::BM) + trow - srow) * ROWB;
-    boff[i] = ((uint32_t)min(n0 + trow, b.Np - 1) * b.Kp + chunk * C::CH) * 2;
+    sl_lds[i] = ((kind == NPA ? NPA * C::BM : kind * C::BM) + trow - srow) * ROWB;
+    boff[i] = ((uint32_t)min(n0 + trow, b.Np - 1) * b.Kp + chunk * C::CH) * ES;
     const int r = min(m0 + trow, a.M - 1);
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       aoff[s][i] = 0;
       if (s < NSEG) {
         const int rr = a.seg[s].idx ? a.seg[s].idx[r] : r;
-        aoff[s][i] = ((uint32_t)rr * a.seg[s].ld + chunk * C::CH) * 2;
+        aoff[s][i] = ((uint32_t)rr * a.seg[s].ld + chunk * C::CH) * ES;
       }
     }
   }
@@ -976,12 +979,12 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
   // in registers (a runtime segment index put them in scratch memory).
   auto issue_seg = [&](auto seg_c, int ls, char* sb) {
     constexpr int S = decltype(seg_c)::value;
-    const uint32_t ka = (uint32_t)ls * ROWB, kb = (uint32_t)((S ? kb1 : 0) + ls * C::BK) * 2;
+    const uint32_t ka = (uint32_t)ls * ROWB, kb = (uint32_t)((S ? kb1 : 0) + ls * C::BK) * ES;
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
-      if (sl_kind[i] == kPlanes)
+      if (sl_kind[i] == NPA)
         dma16(rw, sb + sl_lds[i], boff[i] + kb);
-      else if (sl_kind[i] == 0)
+      else if (NPA == 1 || sl_kind[i] == 0)
         dma16(rp[S][0], sb + sl_lds[i], aoff[S][i] + ka);
       else if (sl_kind[i] == 1)
         dma16(rp[S][1], sb + sl_lds[i], aoff[S][i] + ka);
@@ -1014,7 +1017,7 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
       const int ls = G - (s ? nst[0] : 0);
       const int w = s ? wd[1] : wd[0];
       if ((ls + 1) * C::BK > w) {                      // the segment's last stage reaches past its width
-        for (int e = tid; e < kPlanes * C::BM * C::CPR; e += C::NT) {
+        for (int e = tid; e < NPA * C::BM * C::CPR; e += C::NT) {
           const int row = e / C::CPR, c = e % C::CPR;   // row of the A planes, one after the other; chunk
           if (ls * C::BK + c * C::CH >= w)
             *(uint4*)(base + row * ROWB + ((c ^ C::swz(row % C::BM)) * 16)) = zero4();
@@ -1026,20 +1029,37 @@ __device__ inline void gemm_tile_dma(const AOp& a, const BOp& b, int m0, int n0,
       }
     }
     issue(G + NSTG - 1);                                // refills the buffer multiplied at G - 1
-    const __bf16* Ah = (const __bf16*)base + (wm * C::TM * 16 + i16) * C::ROW;
-    const __bf16* Bb = (const __bf16*)base + (kPlanes * C::BM + wn * C::TN * 16 + i16) * C::ROW;
-    bf16x8 av[C::TM], bv[C::TN];
+    if constexpr (C::kBf16) {
+      const __bf16* Ah = (const __bf16*)base + (wm * C::TM * 16 + i16) * C::ROW;
+      const __bf16* Bb = (const __bf16*)base + (NPA * C::BM + wn * C::TN * 16 + i16) * C::ROW;
+      bf16x8 av[C::TM], bv[C::TN];
 #pragma unroll
-    for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + col);
+      for (int y = 0; y < C::TN; ++y) bv[y] = *(const bf16x8*)(Bb + y * 16 * C::ROW + col);
 #pragma unroll
-    for (int pl = 0; pl < kPlanes; ++pl) {
+      for (int pl = 0; pl < NPA; ++pl) {
 #pragma unroll
-      for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + (pl * C::BM + x * 16) * C::ROW + col);
+        for (int x = 0; x < C::TM; ++x) av[x] = *(const bf16x8*)(Ah + (pl * C::BM + x * 16) * C::ROW + col);
 #pragma unroll
-      for (int x = 0; x < C::TM; ++x)
+        for (int x = 0; x < C::TM; ++x)
 #pragma unroll
-        for (int y = 0; y < C::TN; ++y)
-          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+          for (int y = 0; y < C::TN; ++y)
+            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[x], bv[y], acc[x][y], 0, 0, 0);
+      }
+    } else {      // fp32: one 16-byte chunk (K = 4 g .. 4 g + 3) per lane and row, four K = 4 products
+      const float* Af = (const float*)base + (wm * C::TM * 16 + i16) * C::ROW;
+      const float* Bf = (const float*)base + (C::BM + wn * C::TN * 16 + i16) * C::ROW;
+      f32x4 av[C::TM], bv[C::TN];
+#pragma unroll
+      for (int x = 0; x < C::TM; ++x) av[x] = *(const f32x4*)(Af + x * 16 * C::ROW + col);
+#pragma unroll
+      for (int y = 0; y < C::TN; ++y) bv[y] = *(const f32x4*)(Bf + y * 16 * C::ROW + col);
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int x = 0; x < C::TM; ++x)
+#pragma unroll
+          for (int y = 0; y < C::TN; ++y)
+            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[x][m], bv[y][m], acc[x][y], 0, 0, 0);
     }
   }
   // every load (including the re-loads past the end) has landed before the output tile reuses the buffers
@@ -1089,11 +1109,21 @@ static hipError_t launch_store(const AOp& a, const BOp& b, const StoreParams& p,
   return hipGetLastError();
 }
 
-// The LDS-destination main loop applies to bf16 products whose one or two A segments are all pre-split.
+// The LDS-destination main loop applies to bf16 products whose one or two A segments are all pre-split ...
 static inline bool all_pre_split(const AOp& a) {
   if (a.nseg < 1 || a.nseg > 2) return false;
   for (int s = 0; s < a.nseg; ++s)
     if (!a.seg[s].bf16 || !a.seg[s].lo || !a.seg[s].lo2 || a.seg[s].ld < a.seg[s].kpad) return false;
+  return true;
+}
+
+// ... and to fp32 products whose one or two A segments have 16-byte aligned rows (widths and strides are
+// multiples of 4 elements): with the 16 x 32 fp32 LSTM tiles the decoder layers of the default workload
+// took 19.2 instead of 20.3 us (a 32 x 64 tile with two waves per K half, LDS-destination too, 26.4 us).
+static inline bool all_fp32_rows(const AOp& a) {
+  if (a.nseg < 1 || a.nseg > 2) return false;
+  for (int s = 0; s < a.nseg; ++s)
+    if (a.seg[s].bf16 || a.seg[s].ld % 4 || a.seg[s].width % 4) return false;
   return true;
 }
 
@@ -1103,6 +1133,15 @@ static hipError_t launch_lstm(const AOp& a, const BOp& b, const LstmParams& p, h
   grid_of<C>(a, b, nm, nb);
   if (!operands_fit<T>(a, b) || a.nseg < 1 || a.nseg > 3) return hipErrorInvalidValue;
   if (nb == 0) return hipSuccess;
+  if constexpr (!C::kBf16 && C::KW == C::KSUB) {
+    if (all_fp32_rows(a)) {
+      if (a.nseg == 1)
+        hipLaunchKernelGGL((k_gemm_lstm<T, C, 1, true>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+      else
+        hipLaunchKernelGGL((k_gemm_lstm<T, C, 2, true>), dim3(nb), dim3(C::NT), 0, st, a, b, p, nm, nb);
+      return hipGetLastError();
+    }
+  }
   if constexpr (C::kBf16 && C::KW == C::KSUB && C::CPR == 8) {
     if (all_pre_split(a)) {
       if (a.nseg == 1)

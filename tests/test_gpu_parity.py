@@ -227,3 +227,57 @@ def test_encoder_other_workloads(which, request):
     for l in range(s.w.dec_layers):
         np.testing.assert_allclose(fh[l].cpu().numpy(), enc.final_h[l], atol=tol, rtol=0)
         np.testing.assert_allclose(fc[l].cpu().numpy(), enc.final_c[l], atol=tol, rtol=0)
+
+
+# ------------------------------------------------------------------ generator precision (fp32 models)
+def _bf16_terms(x, n):
+    """x (float32 array) as n bf16 terms, RNE of the value and then of each remainder, as float64."""
+    out, r = [], x.astype(np.float32)
+    for _ in range(n):
+        u = r.view(np.uint32).astype(np.uint64)
+        t = (((u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000).astype(np.uint32)).view(np.float32)
+        out.append(t.astype(np.float64))
+        r = (r - t).astype(np.float32)
+    return out
+
+
+@pytest.fixture(scope="module")
+def default_peaked():
+    return Setup(W.get("default"), peaked=True)
+
+
+def test_generator_products_keep_fp32_accuracy(default_peaked):
+    # The fp32 generator multiplies each fp32 weight and activation as three bf16 terms and keeps the six
+    # term products down to 2^-16 of the leading one (Section 2 generator; fp32 workloads). On the GPU's
+    # own attentional vector, its logits must match the fp64 generator's to fp32 rounding. Compared as
+    # differences within a row (log-prob of every word minus that of word 0, so the row's log-sum-exp
+    # cancels), with W_s scaled by 10 so that logits reach tens: an fp32 product errs by ~3e-6 there, the
+    # cheaper three-product form (hi.hi + hi.lo + lo.hi) by ~2.4e-5, and the bound sits between them.
+    s = default_peaked
+    w = s.w
+    B, S = s.src.shape
+    K = w.beam
+    N = B * K
+    _print_case("generator_precision", workload=w.name, peaked=True, N=N)
+    tr = s.tr
+    ws = tr.encode(s.src_d, s.lens_d)
+    st = tr.decode_init(ws, B, S, K)
+    tok = torch.full((N,), W.BOS_ID, dtype=torch.int32, device="cuda")
+    st_out, logp, _, _, _ = tr.decode_step(ws, B, S, K, st, tok, None, mode=0)
+    torch.cuda.synchronize()
+    feed = tr.state_views(st_out, N)[2].cpu().numpy()
+    rows = slice(0, 64)                                  # 64 of the 320 rows: the fp64 reference over 50000 columns
+    ref = O.generator(s.model, feed[rows].astype(np.float64))
+
+    def dif(x):
+        return x - x[:, :1]
+
+    err = np.abs(dif(logp.cpu().numpy()[rows].astype(np.float64)) - dif(ref)).max()
+    # the three-product form of the same operands, in fp64 otherwise
+    a1, a2, _ = _bf16_terms(feed[rows], 3)
+    w1, w2, _ = _bf16_terms(s.model.w["W_s"].astype(np.float32), 3)
+    z3 = a1 @ w1.T + a1 @ w2.T + a2 @ w1.T + s.model.w["b_s"]
+    err3 = np.abs(dif(z3) - dif(ref)).max()
+    print(f"  max |logit difference - fp64| = {err:.3g}; three-product form: {err3:.3g}", flush=True)
+    assert err <= 8e-6
+    assert err3 > 8e-6

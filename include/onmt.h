@@ -58,8 +58,11 @@ typedef struct {
   int enc_layers, dec_layers, bidirectional;
   int emb, hidden;
   int src_vocab, tgt_vocab;
-  int wdtype;                      /* 0 = fp32 weights and products; 1 = bf16 weights and MFMA operands,
-                                      fp32 accumulation, cell state and softmax */
+  int wdtype;                      /* 0 = fp32 weights and fp32-accurate products (the vocabulary
+                                      projection runs them as six bf16 term products of three-term
+                                      splits of both operands, accumulated in fp32); 1 = bf16 weights
+                                      and MFMA operands (activations as bf16 terms), fp32 accumulation,
+                                      cell state and softmax */
   int pad_id, unk_id, bos_id, eos_id;
   int attn_type;                   /* attention score (Section 4.2 names three types, none with biases):
                                       ONMT_ATTN_GENERAL e_s = q . W_a m_s;

@@ -10,7 +10,7 @@ single precision, used only to time the CPU baseline; beam scores stay fp64), wr
 holding the OpenNMT paper
 (Klein et al., arXiv 1805.11462). The paper names the pieces but prints no
 equations, so the standard published forms of the cited works are written out
-here; every place where the paper is silent carries its reading (R1..R16, the
+here; every place where the paper is silent carries its reading (R1..R20, the
 same numbering as the design notes).
 
 What the paper fixes, and where:

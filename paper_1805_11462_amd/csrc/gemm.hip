@@ -703,10 +703,9 @@ using TileThin16 = Tile<__bf16, 1, 1, 4, 1, 4, 32>;
 // the weights are re-read by half as many row tiles, which matters more than the halved workgroup count
 // once the bf16 products are cheap (decoder layers at 320-512 rows: 16-32% faster).
 using TileMid16 = Tile<__bf16, 1, 2, 2, 2, 2, 32>;
-// Generator: the 64 x 128 tile of the wide shapes with a 16 (fp32) / 32 (bf16) element K stage, which
+// fp32 generator (fp32 MFMA): the 64 x 128 tile of the wide shapes with a 16-element K stage, which
 // halves the LDS stage buffers so that four workgroups fit on a CU.
 using TileGen32 = Tile<float, 2, 2, 1, 2, 4, 16>;
-using TileGen16 = Tile<__bf16, 2, 2, 1, 2, 4, 32>;
 // 32 x 128 fp32 generator tiles (two waves) where the last 64-row tile would be at most half full and the
 // rows are few: at 160 rows 91 us instead of 108 us (64-row tiles compute 192 rows), at 96 rows 64 instead
 // of 78 us; at multiples of 64 rows, and at 480, the 64-row tile is faster. Same partials, bitwise.
@@ -715,8 +714,8 @@ static inline bool gen_rows32(int M) {
   const int r = M % 64;
   return M <= 256 && r > 0 && r <= 32;
 }
-static_assert(TileGen32::BN == TileGen16::BN && TileGen32h::BN == TileGen32::BN,
-              "all generator tiles give the same column tiles");
+static_assert(TileGen32h::BN == TileGen32::BN && TileGen32::BN == 128,
+              "all generator tiles give the same 128-column partial tiles");
 // Pre-split bf16 generator: 64 x 256 tiles (8 waves of 32 x 64; the activations are re-read by half as
 // many column tiles as with 64 x 128) and two LDS stages of 24 KB; at 320 and 512 rows this measured
 // 10-15% faster than 64 x 128 tiles with three 16 KB stages, and three or four stages of 64 x 256 slower.
@@ -1245,8 +1244,7 @@ hipError_t split_rows(const float* src, int ld_src, int rows, int cols, uint16_t
   return hipGetLastError();
 }
 
-hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
-  if (bf16) return launch_gen<__bf16, TileGen16>(a, b, p, st);
+hipError_t gemm_gen(const AOp& a, const BOp& b, const GenParams& p, hipStream_t st) {
   return gen_rows32(a.M) ? launch_gen<float, TileGen32h>(a, b, p, st) : launch_gen<float, TileGen32>(a, b, p, st);
 }
 

@@ -123,7 +123,9 @@ hipError_t gemm_store(int bf16, int shape, const AOp& a, const BOp& b, const Sto
 hipError_t gemm_lstm(int bf16, int shape, const AOp& a, const BOp& b, const LstmParams& p, hipStream_t st);
 // Two independent thin-shape LSTM GEMMs in one launch (segment counts 1+1, 1+2 or 2+2).
 hipError_t gemm_lstm2(int bf16, int shape, const LstmPair& g, hipStream_t st);
-hipError_t gemm_gen(int bf16, const AOp& a, const BOp& b, const GenParams& p, hipStream_t st);
+// The generator with fp32 operands and the fp32 MFMA (fp32 models at the row counts gemm_gen_split_rows
+// leaves to it).
+hipError_t gemm_gen(const AOp& a, const BOp& b, const GenParams& p, hipStream_t st);
 
 
 // bf16 generator operand already split into its bf16 term planes (A = hi + lo + lo2), row-major [M, ld]

@@ -1225,7 +1225,7 @@ int decode_compute(onmt_model* m, const EncWs& w, int B, int S, int K, const Sta
       HIP_TRY(gemm_gen_split(GenSplitA{out.feed_hi, out.feed_lo, N, d.pad(d.H), d.pad(d.H), out.feed_lo2},
                              bop(m->W_s), d.gwp, gp, st));
     else
-      HIP_TRY(gemm_gen(0, a, bop(m->W_s32), gp, st));
+      HIP_TRY(gemm_gen(a, bop(m->W_s32), gp, st));
     if (timing) time_end(m, st);
   }
   if (mode == 2) return ONMT_OK;
@@ -1619,7 +1619,7 @@ int onmt_score(onmt_model* m, const int32_t* src, const int32_t* len, int B, int
       HIP_TRY(gemm_gen_split(GenSplitA{w.feeds_hi, w.feeds_lo, M, d.pad(d.H), d.pad(d.H), w.feeds_lo2}, bop(m->W_s),
                              d.gwp, gp, st));
     else
-      HIP_TRY(gemm_gen(0, a, bop(m->W_s32), gp, st));
+      HIP_TRY(gemm_gen(a, bop(m->W_s32), gp, st));
     time_end(m, st);
     HIP_TRY(score_rows(w.gpmax, w.gpsum, w.step.ntiles, w.want_logit, w.tlen, B, steps, out_logp, T, w.nll, st));
   }

@@ -304,23 +304,25 @@ def main():
 def bench_vendor(w):
     """Plain GEMMs of the vendor library (torch.matmul, which runs hipBLASLt on ROCm) at the shapes of one
     decoder step's GEMMs: a reference for what a library GEMM takes at these shapes without the gathers and
-    epilogues that the library's own kernels fuse in. bf16 workloads multiply hi + lo activation terms, so the
-    reference GEMM concatenates them along K (A = [hi | lo], W = [W | W]): the same MFMA work. Not part of the
+    epilogues that the library's own kernels fuse in. bf16 workloads multiply several bf16 terms of each
+    activation (two in the generator, three in the decoder layers and W_c), so the reference GEMM concatenates
+    that many copies along K (A = [p0 | p1 | ...], W = [W | W | ...]): the same MFMA work. Not part of the
     translation path; prints one JSON line per shape."""
     import torch
     if not torch.cuda.is_available():
         sys.exit("--mode vendor needs a GPU")
     N = w.batch * w.beam
     H, E, V = w.hidden, w.emb, w.tgt_vocab
-    Hm = 2 * w.hidden if w.bidirectional else w.hidden
+    Hm = w.hidden                     # memory width: a bidirectional encoder's directions have hidden / 2 units each
     bf16 = w.wdtype == "bf16"
     dt = torch.bfloat16 if bf16 else torch.float32
-    rep = 2 if bf16 else 1
     peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
-    shapes = [("generator", N, V, H), ("decoder LSTM layer (feed or input ; h)", N, 4 * H, 2 * H),
-              ("attentional output W_c ([ctx ; h])", N, H, Hm + H),
-              ("square 8192 (what the library reaches on a large GEMM)", 8192, 8192, 8192 // rep)]
-    for name, M, Ncol, K in shapes:
+    # (name, M, N, K, activation terms of the library's bf16 product)
+    shapes = [("generator", N, V, H, 2), ("decoder LSTM layer (feed or input ; h)", N, 4 * H, 2 * H, 3),
+              ("attentional output W_c ([ctx ; h])", N, H, Hm + H, 3),
+              ("square 8192 (what the library reaches on a large GEMM)", 8192, 8192, 8192, 1)]
+    for name, M, Ncol, K, terms in shapes:
+        rep = terms if bf16 else 1
         a = torch.randn(M, rep * K, device="cuda", dtype=dt)
         b = torch.randn(Ncol, rep * K, device="cuda", dtype=dt).t()
         out = torch.empty(M, Ncol, device="cuda", dtype=dt)
@@ -337,9 +339,10 @@ def bench_vendor(w):
         us = e0.elapsed_time(e1) * 1e3 / it
         flops = 2.0 * M * Ncol * K
         print(json.dumps({"vendor_gemm": name, "workload": w.name, "M": M, "N": Ncol, "K": K,
-                          "operands": "bf16 hi+lo along K" if bf16 else "fp32", "us": round(us, 2),
-                          "tflops": round(flops / us / 1e6, 1), "frac_of_peak": round(flops / us / 1e6 / peak, 3),
-                          "frac_counting_hi_lo": round(rep * flops / us / 1e6 / peak, 3)}), flush=True)
+                          "operands": f"bf16, {rep} activation terms along K" if bf16 else "fp32",
+                          "us": round(us, 2), "tflops": round(flops / us / 1e6, 1),
+                          "frac_of_peak": round(flops / us / 1e6 / peak, 3),
+                          "frac_counting_terms": round(rep * flops / us / 1e6 / peak, 3)}), flush=True)
 
 
 def bench_score(args, w, weights, tr, src, lens, src_d, lens_d):
